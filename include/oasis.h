@@ -1,0 +1,176 @@
+/*
+ * oasis.h - C ABI of the OASIS hot path on AMD MI355X (gfx950).
+ *
+ * OASIS (arXiv 2507.23035) multiplies non-uniformly (K-Means codebook)
+ * quantized activations and weights without dequantizing them: the products
+ * of every activation centroid with every weight centroid are precomputed in
+ * a Cartesian product LUT (Sec. III-B), activations are clustered per token
+ * at run time and the dynamic top-k outliers of each token are compensated
+ * in a separate branch (look-ahead computation + error compensation,
+ * Sec. III-C; outlier detection, Sec. IV-D).
+ *
+ * Conventions shared by every call
+ *  - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *    allocates no device memory and keeps no state between calls.  Pointers
+ *    documented as HOST pointers are read during the call only.
+ *  - fp16 values are passed as their IEEE binary16 bit patterns (uint16_t).
+ *  - Every call is asynchronous on `stream` (NULL = the null stream) and
+ *    returns an oasis_status code; argument errors are detected on the host
+ *    before anything is launched.  Nothing throws across the ABI.
+ *  - Index tensors hold one 4-bit code per nibble for every bit-width 1..4.
+ *  - Activations must be finite (NaN is outside the contract: memory stays
+ *    safe but results are unspecified).
+ *  - Calls are thread-compatible: concurrent calls must not share outputs.
+ *
+ * Index layouts
+ *  - idx_act : uint8 [n][d_in/2]; channel 2q in the low nibble of byte q.
+ *  - idx_w   : uint32 [d_in/8][d_out]; word (b, j) holds the codes of input
+ *              channels 8b..8b+7 of output column j, channel 8b+e in bits
+ *              4e..4e+3.  (Input-channel-major, so one input channel of all
+ *              output columns, which the compensation fetches, is one
+ *              contiguous row of words.)
+ *  - y       : fp32 [n][d_out], row-major.
+ */
+#ifndef OASIS_H
+#define OASIS_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum oasis_status {
+  OASIS_OK = 0,
+  OASIS_ERR_NULL = -1,        /* a required pointer is NULL                        */
+  OASIS_ERR_SHAPE = -2,       /* n/d_in/d_out negative, d_out < 1, d_in % 8 != 0   */
+  OASIS_ERR_BITS = -3,        /* bit-width outside 1..4                            */
+  OASIS_ERR_K = -4,           /* k < 0 or k > d_in                                 */
+  OASIS_ERR_CODEBOOK = -5,    /* activation codebook not strictly ascending, or a
+                                 codebook entry is not finite                      */
+  OASIS_ERR_ALIGN = -6,       /* a pointer is not aligned as documented            */
+  OASIS_ERR_MODE = -7,        /* unknown scale mode or algorithm                   */
+  OASIS_ERR_LAUNCH = -8,      /* the HIP runtime refused a launch                  */
+  OASIS_ERR_TOO_LARGE = -9    /* a size exceeds what a kernel supports             */
+};
+
+enum oasis_scale_mode {
+  OASIS_SCALE_ABSMAX = 0,     /* t_i = max_p |x_ip| (outliers included)            */
+  OASIS_SCALE_NONE = 1        /* t_i = 1                                           */
+};
+
+enum oasis_gemm_algo {
+  OASIS_ALGO_LUT = 0,         /* one LDS LUT lookup per (token, channel, column)   */
+  OASIS_ALGO_MFMA = 1         /* rank-1 LUT: exact fp16 factors on matrix cores    */
+};
+
+/* The LUT block: the Cartesian product LUT plus both codebooks, the content
+ * of the accelerator's on-chip LUT (Sec. IV-A: it stores the products and
+ * the activation and weight codebooks).  1088 bytes, 16-byte aligned. */
+typedef struct oasis_lut_block {
+  float lut[256];          /* lut[(a << b_w) | w] = C_A[a] * C_W[w], exact fp32; */
+                           /* entries at and beyond 2^(b_a+b_w) are 0            */
+  uint16_t cb_act[16];     /* C_A (fp16 bits), first 2^b_a used, rest 0          */
+  uint16_t cb_wgt[16];     /* C_W (fp16 bits), first 2^b_w used, rest 0          */
+} oasis_lut_block;
+
+/* Human-readable name of a status code (static string). */
+const char* oasis_status_str(int status);
+
+/* Library version string, e.g. "oasis 0.1 gfx950". */
+const char* oasis_version(void);
+
+/*
+ * oasis_build_lut - Cartesian product LUT (Sec. III-B; on-chip LUT, Sec. IV-A).
+ *   cb_act : HOST fp16 [2^b_a], strictly ascending, finite (the Clustering
+ *            Unit's binary search needs the order, Sec. IV-C).
+ *   cb_wgt : HOST fp16 [2^b_w], finite.
+ *   out    : DEVICE oasis_lut_block, 16-byte aligned; fully overwritten.
+ * Errors: NULL, BITS, CODEBOOK, ALIGN, LAUNCH.
+ */
+int oasis_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                    oasis_lut_block* out, hipStream_t stream);
+
+/*
+ * oasis_quantize_act - per-token activation quantization and dynamic top-k
+ * outlier detection (Sec. III-A, III-C1; Clustering Unit, Sec. IV-C;
+ * Orizuru, Sec. IV-D; Error Calculation Unit, Sec. IV-A).
+ *   x         : DEVICE fp16 [n][d_in], 16-byte aligned.
+ *   lut       : DEVICE LUT block built with the same b_a (its C_A is used).
+ *   k         : outliers per side per token, 0 <= k <= d_in.
+ *   scale_mode: OASIS_SCALE_ABSMAX or OASIS_SCALE_NONE.
+ * Outputs (DEVICE, fully overwritten):
+ *   idx_act   : uint8 [n][d_in/2] cluster index of EVERY channel, outliers
+ *               included: #{c : x >= fp32(t * b_c)} with
+ *               b_c = fp32(C_A[c] + C_A[c+1]) * 0.5 (half-open intervals).
+ *   act_scale : fp32 [n], t_i.
+ *   max_idx   : int32 [n][k], the k largest channels, largest first, ties to
+ *               the lower channel (-0 == +0).
+ *   min_idx   : int32 [n][k], the k smallest channels, smallest first, same
+ *               tie rule.
+ *   residual  : fp32 [n][2k]; [i][e] = fp32(x - fp32(t*C_A[a])) of max_idx
+ *               entry e, [i][k+e] the same for min_idx entry e, or 0 when
+ *               that channel is also in the token's max list (the union is
+ *               compensated once).
+ *   When k == 0, max_idx/min_idx/residual may be NULL.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, MODE, TOO_LARGE (d_in > 65536), LAUNCH.
+ */
+int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
+                       int k, int scale_mode, uint8_t* idx_act, float* act_scale,
+                       int32_t* max_idx, int32_t* min_idx, float* residual, hipStream_t stream);
+
+/*
+ * oasis_lut_gemm - look-ahead WAQ LUT-GEMM, the main branch (Sec. III-B,
+ * III-C1): Y*[i][j] = t_i * s_j * sum_p LUT[(a_ip << b_w) | w_pj].
+ *   idx_act, act_scale : from oasis_quantize_act (n tokens, d_in channels);
+ *               idx_act 16-byte aligned.
+ *   idx_w     : DEVICE uint32 [d_in/8][d_out] weight codes (layout above),
+ *               16-byte aligned.
+ *   w_scale   : DEVICE fp32 [d_out], s_j.
+ *   lut       : DEVICE LUT block (b_a, b_w as built).
+ *   algo      : OASIS_ALGO_LUT accumulates LUT entries fetched from LDS;
+ *               OASIS_ALGO_MFMA uses that the LUT is the outer product of
+ *               the codebooks, so the sum is a dense contraction of exact
+ *               fp16 centroid values, run on matrix cores (fp32 accumulate).
+ *               Both equal the definition up to fp32 summation order.
+ *   y         : DEVICE fp32 [n][d_out], 4-byte aligned.
+ *   accumulate != 0 : y += Y*  (merge into a compensation term written first);
+ *   accumulate == 0 : y  = Y*.
+ *   Partial sums over input-channel slices may be merged with fp32 atomics,
+ *   so the summation order (not the set of products) can vary run to run.
+ * Errors: NULL, SHAPE, BITS, ALIGN, MODE, LAUNCH.
+ */
+int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
+                   const uint32_t* idx_w, const float* w_scale, int d_out,
+                   const oasis_lut_block* lut, int b_a, int b_w, int algo, float* y,
+                   int accumulate, hipStream_t stream);
+
+/*
+ * oasis_outlier_compensate - error compensation of the outlier branch
+ * (Sec. III-C2; Dequant Unit and MAC units, Sec. IV-A):
+ *   Y'[i][j] = s_j * sum_e residual[i][e] * C_W[w(p_e, j)], p_e running over
+ *   max_idx[i][0..k) then min_idx[i][0..k).
+ *   accumulate != 0 : y += Y'   (merge into the main-branch result);
+ *   accumulate == 0 : y  = Y'.
+ *   Channel ids must lie in [0, d_in) (ids from oasis_quantize_act do).
+ *   k == 0 with accumulate != 0 is a no-op; with accumulate == 0 it zeroes y.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, LAUNCH.
+ */
+int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, const float* residual,
+                             int n, int k, const uint32_t* idx_w, const oasis_lut_block* lut,
+                             int b_w, const float* w_scale, int d_in, int d_out, float* y,
+                             int accumulate, hipStream_t stream);
+
+/*
+ * oasis_pack_weight_indices - HOST helper: pack w_idx uint8 [d_in][d_out]
+ * (codes 0..15, row-major, host memory) into the idx_w layout above
+ * (host memory, d_in/8 * d_out words).  Errors: NULL, SHAPE.
+ */
+int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OASIS_H */

@@ -280,12 +280,12 @@ def lut_gemm(a: np.ndarray, w_idx: np.ndarray, lut: np.ndarray, t: np.ndarray,
     """
     rows = range(a.shape[0]) if tokens is None else tokens
     lut64 = np.asarray(lut, dtype=np.float32).astype(np.float64)
-    w = np.asarray(w_idx).astype(np.int64)
+    w = np.asarray(w_idx, dtype=np.uint8)
     out = np.zeros((len(rows), w.shape[1]), dtype=np.float64)
     for r, i in enumerate(rows):
         acc = np.zeros(w.shape[1], dtype=np.float64)
         for p in range(w.shape[0]):
-            concat = (int(a[i, p]) << b_w) | w[p]
+            concat = (int(a[i, p]) << b_w) | w[p].astype(np.intp)
             acc += lut64[concat]
         out[r] = float(t[i]) * np.asarray(s_w, dtype=np.float64) * acc
     return out

@@ -1,0 +1,152 @@
+// C ABI of liboasis: host-side argument checking and kernel launches.
+// Every check happens before anything is enqueued, so an error status means
+// nothing ran.  No exception crosses the ABI.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "common.h"
+
+namespace {
+
+// IEEE binary16 bits -> float (host side, exact).
+float half_bits_to_float(uint16_t h) {
+  const uint32_t sign = (uint32_t)(h & 0x8000u) << 16;
+  const uint32_t exp = (h >> 10) & 0x1Fu;
+  const uint32_t man = h & 0x3FFu;
+  float out;
+  if (exp == 0) {
+    out = std::ldexp((float)man, -24);
+    if (sign) out = -out;
+    return out;
+  }
+  if (exp == 31) {
+    uint32_t bits = sign | 0x7F800000u | (man << 13);
+    std::memcpy(&out, &bits, 4);
+    return out;
+  }
+  uint32_t bits = sign | ((exp + 112u) << 23) | (man << 13);
+  std::memcpy(&out, &bits, 4);
+  return out;
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+bool bits_ok(int b) { return b >= 1 && b <= 4; }
+
+constexpr size_t kMaxLds = 160 * 1024;
+
+int launched(hipError_t e) { return e == hipSuccess ? OASIS_OK : OASIS_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+const char* oasis_status_str(int status) {
+  switch (status) {
+    case OASIS_OK: return "ok";
+    case OASIS_ERR_NULL: return "null pointer";
+    case OASIS_ERR_SHAPE: return "bad shape";
+    case OASIS_ERR_BITS: return "bit-width outside 1..4";
+    case OASIS_ERR_K: return "k outside 0..d_in";
+    case OASIS_ERR_CODEBOOK: return "codebook not finite or activation codebook not ascending";
+    case OASIS_ERR_ALIGN: return "misaligned pointer";
+    case OASIS_ERR_MODE: return "unknown scale mode or algorithm";
+    case OASIS_ERR_LAUNCH: return "HIP launch failed";
+    case OASIS_ERR_TOO_LARGE: return "size exceeds kernel limits";
+    default: return "unknown status";
+  }
+}
+
+const char* oasis_version(void) { return "oasis 0.1 gfx950"; }
+
+int oasis_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                    oasis_lut_block* out, hipStream_t stream) {
+  if (!cb_act || !cb_wgt || !out) return OASIS_ERR_NULL;
+  if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
+  for (int i = 0; i < (1 << b_a); ++i) {
+    const float v = half_bits_to_float(cb_act[i]);
+    if (!std::isfinite(v)) return OASIS_ERR_CODEBOOK;
+    if (i > 0 && !(v > half_bits_to_float(cb_act[i - 1]))) return OASIS_ERR_CODEBOOK;
+  }
+  for (int i = 0; i < (1 << b_w); ++i)
+    if (!std::isfinite(half_bits_to_float(cb_wgt[i]))) return OASIS_ERR_CODEBOOK;
+  if (!aligned(out, 16)) return OASIS_ERR_ALIGN;
+  return launched(oasis::launch_build_lut(cb_act, b_a, cb_wgt, b_w, out, stream));
+}
+
+int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
+                       int k, int scale_mode, uint8_t* idx_act, float* act_scale,
+                       int32_t* max_idx, int32_t* min_idx, float* residual, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
+  if (oasis::quantize_lds_bytes(d_in, k) > kMaxLds) return OASIS_ERR_TOO_LARGE;
+  if (n == 0) return OASIS_OK;
+  if (!x || !lut || !act_scale || (d_in > 0 && !idx_act)) return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(lut, 16) || !aligned(idx_act, 16) || !aligned(act_scale, 4) ||
+      !aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4))
+    return OASIS_ERR_ALIGN;
+  oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
+                     max_idx, min_idx, residual};
+  return launched(oasis::launch_quantize(a, stream));
+}
+
+int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
+                   const uint32_t* idx_w, const float* w_scale, int d_out,
+                   const oasis_lut_block* lut, int b_a, int b_w, int algo, float* y,
+                   int accumulate, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (algo != OASIS_ALGO_LUT && algo != OASIS_ALGO_MFMA) return OASIS_ERR_MODE;
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!act_scale || !w_scale || !lut || !y || (d_in > 0 && (!idx_act || !idx_w)))
+    return OASIS_ERR_NULL;
+  if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
+      !aligned(act_scale, 4) || !aligned(w_scale, 4))
+    return OASIS_ERR_ALIGN;
+  if (d_in == 0) {  // empty reduction: Y* = 0
+    if (accumulate) return OASIS_OK;
+    return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
+  }
+  oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
+                    accumulate ? 1 : 0};
+  return launched(algo == OASIS_ALGO_LUT ? oasis::launch_gemm_lut(a, stream)
+                                         : oasis::launch_gemm_mfma(a, stream));
+}
+
+int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, const float* residual,
+                             int n, int k, const uint32_t* idx_w, const oasis_lut_block* lut,
+                             int b_w, const float* w_scale, int d_in, int d_out, float* y,
+                             int accumulate, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!lut || !w_scale || !y) return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual || !idx_w)) return OASIS_ERR_NULL;
+  if (!aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4) ||
+      !aligned(idx_w, 4) || !aligned(lut, 16) || !aligned(w_scale, 4) || !aligned(y, 4))
+    return OASIS_ERR_ALIGN;
+  oasis::CompArgs a{max_idx, min_idx, residual, n, k, idx_w, lut, b_w, w_scale, d_in, d_out, y,
+                    accumulate ? 1 : 0};
+  return launched(oasis::launch_compensate(a, stream));
+}
+
+int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out) {
+  if (!w_idx || !out) return OASIS_ERR_NULL;
+  if (d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  for (int b = 0; b < d_in / 8; ++b) {
+    uint32_t* row = out + (size_t)b * d_out;
+    for (int j = 0; j < d_out; ++j) row[j] = 0;
+    for (int e = 0; e < 8; ++e) {
+      const uint8_t* src = w_idx + (size_t)(8 * b + e) * d_out;
+      for (int j = 0; j < d_out; ++j) row[j] |= (uint32_t)(src[j] & 15u) << (4 * e);
+    }
+  }
+  return OASIS_OK;
+}
+
+}  // extern "C"

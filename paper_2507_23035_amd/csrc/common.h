@@ -1,0 +1,72 @@
+// Internal helpers shared by the OASIS HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "oasis.h"
+
+namespace oasis {
+
+constexpr int kWave = 64;
+
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t uint4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float h2f(uint16_t bits) {
+  return (float)__builtin_bit_cast(_Float16, bits);
+}
+
+// Everything the host launchers need; argument checking happens in api.cpp.
+struct QuantArgs {
+  const uint16_t* x;
+  int n, d_in, b_a, k, scale_mode;
+  const oasis_lut_block* lut;
+  uint8_t* idx_act;
+  float* act_scale;
+  int32_t* max_idx;
+  int32_t* min_idx;
+  float* residual;
+};
+
+struct GemmArgs {
+  const uint8_t* idx_act;
+  const float* act_scale;
+  int n, d_in;
+  const uint32_t* idx_w;
+  const float* w_scale;
+  int d_out;
+  const oasis_lut_block* lut;
+  int b_a, b_w;
+  float* y;
+  int accumulate;
+};
+
+struct CompArgs {
+  const int32_t* max_idx;
+  const int32_t* min_idx;
+  const float* residual;
+  int n, k;
+  const uint32_t* idx_w;
+  const oasis_lut_block* lut;
+  int b_w;
+  const float* w_scale;
+  int d_in, d_out;
+  float* y;
+  int accumulate;
+};
+
+// Bytes of dynamic LDS the quantize kernel needs for a token of d_in values
+// and k outliers per side.
+size_t quantize_lds_bytes(int d_in, int k);
+
+hipError_t launch_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                            oasis_lut_block* out, hipStream_t s);
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
+hipError_t launch_gemm_lut(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s);
+hipError_t launch_compensate(const CompArgs& a, hipStream_t s);
+hipError_t launch_fill_zero(float* y, size_t count, hipStream_t s);
+
+}  // namespace oasis

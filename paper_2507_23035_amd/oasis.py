@@ -1,0 +1,174 @@
+"""ctypes binding of liboasis.so, the C ABI of the OASIS hot path.
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+torch supplies device memory and the current HIP stream.  There is no
+fallback: if the library is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboasis.so")
+
+SCALE_ABSMAX = 0
+SCALE_NONE = 1
+ALGO_LUT = 0
+ALGO_MFMA = 1
+LUT_BLOCK_BYTES = 256 * 4 + 16 * 2 + 16 * 2
+
+EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quantize_act",
+           "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_pack_weight_indices")
+
+
+class OasisError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load liboasis.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with paper_2507_23035_amd.build.build()")
+    lib = ctypes.CDLL(path)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.oasis_status_str.restype = ctypes.c_char_p
+    lib.oasis_status_str.argtypes = [I]
+    lib.oasis_version.restype = ctypes.c_char_p
+    lib.oasis_version.argtypes = []
+    lib.oasis_build_lut.restype = I
+    lib.oasis_build_lut.argtypes = [P, I, P, I, P, P]
+    lib.oasis_quantize_act.restype = I
+    lib.oasis_quantize_act.argtypes = [P, I, I, P, I, I, I, P, P, P, P, P, P]
+    lib.oasis_lut_gemm.restype = I
+    lib.oasis_lut_gemm.argtypes = [P, P, I, I, P, P, I, P, I, I, I, P, I, P]
+    lib.oasis_outlier_compensate.restype = I
+    lib.oasis_outlier_compensate.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
+    lib.oasis_pack_weight_indices.restype = I
+    lib.oasis_pack_weight_indices.argtypes = [P, I, I, P]
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise OasisError(fn, status, load().oasis_status_str(status).decode())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _fp16_bits(cb) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(cb, dtype=np.float16)).view(np.uint16)
+
+
+# ----------------------------------------------------------------------------
+def pack_weight_indices(w_idx: np.ndarray) -> np.ndarray:
+    """uint8 [d_in][d_out] codes -> uint32 [d_in/8][d_out] words (host)."""
+    w = np.ascontiguousarray(w_idx, dtype=np.uint8)
+    d_in, d_out = w.shape
+    out = np.empty((d_in // 8, d_out), dtype=np.uint32)
+    _check("oasis_pack_weight_indices",
+           load().oasis_pack_weight_indices(w.ctypes.data, d_in, d_out, out.ctypes.data))
+    return out
+
+
+def build_lut(cb_act, b_a: int, cb_wgt, b_w: int, out=None, stream=None):
+    """Cartesian product LUT block (device uint8 tensor of 1088 bytes)."""
+    import torch
+    if out is None:
+        out = torch.empty(LUT_BLOCK_BYTES, dtype=torch.uint8, device="cuda")
+    ca = _fp16_bits(cb_act)
+    cw = _fp16_bits(cb_wgt)
+    _check("oasis_build_lut", load().oasis_build_lut(ca.ctypes.data, b_a, cw.ctypes.data, b_w,
+                                                     _ptr(out), _stream(stream)))
+    return out
+
+
+def quantize_act(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
+                 out: Optional[Dict] = None, stream=None) -> Dict:
+    """Scale, activation codes, outlier lists and residuals of every token."""
+    import torch
+    n, d_in = x.shape
+    dev = x.device
+    if out is None:
+        out = {
+            "idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=dev),
+            "act_scale": torch.empty(n, dtype=torch.float32, device=dev),
+            "max_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "min_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
+        }
+    _check("oasis_quantize_act", load().oasis_quantize_act(
+        _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode, _ptr(out["idx_act"]),
+        _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
+        _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
+        _stream(stream)))
+    return out
+
+
+def lut_gemm(idx_act, act_scale, idx_w, w_scale, lut, b_a: int, b_w: int, algo: int = ALGO_MFMA,
+             y=None, accumulate: bool = False, stream=None):
+    """Main branch Y* (y = Y*, or y += Y* with accumulate)."""
+    import torch
+    n = idx_act.shape[0]
+    d_in = idx_act.shape[1] * 2
+    d_out = idx_w.shape[1]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
+    _check("oasis_lut_gemm", load().oasis_lut_gemm(
+        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
+        b_a, b_w, algo, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def outlier_compensate(max_idx, min_idx, residual, idx_w, lut, b_w: int, w_scale, d_in: int,
+                       y=None, accumulate: bool = True, stream=None):
+    """Outlier branch Y' (y += Y' with accumulate, else y = Y')."""
+    import torch
+    n, k = max_idx.shape
+    d_out = idx_w.shape[1]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=max_idx.device)
+    _check("oasis_outlier_compensate", load().oasis_outlier_compensate(
+        _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
+        _ptr(residual) if k else None, n, k, _ptr(idx_w), _ptr(lut), b_w, _ptr(w_scale), d_in,
+        d_out, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def forward(x, lut, idx_w, w_scale, b_a: int, b_w: int, k: int, scale_mode: int = SCALE_ABSMAX,
+            algo: int = ALGO_MFMA, out: Optional[Dict] = None, y=None, stream=None) -> Dict:
+    """Whole hot path of one layer: Y = Y* + Y'.
+
+    The compensation term is written first and the main branch is merged into
+    it, so the split-reduction GEMM needs no separate clearing pass.
+    """
+    q = quantize_act(x, lut, b_a, k, scale_mode, out=out, stream=stream)
+    y = outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w, w_scale,
+                           x.shape[1], y=y, accumulate=False, stream=stream)
+    lut_gemm(q["idx_act"], q["act_scale"], idx_w, w_scale, lut, b_a, b_w, algo, y=y,
+             accumulate=True, stream=stream)
+    q["y"] = y
+    return q

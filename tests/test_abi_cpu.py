@@ -1,0 +1,126 @@
+"""The C-ABI library without a GPU: it loads, exports every declared symbol,
+and rejects bad arguments on the host before launching anything."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2507_23035_amd import oasis
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oasis.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(oasis.LIB_PATH):
+        from paper_2507_23035_amd import build
+        build.build()
+    return oasis.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(oasis_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for fn in ("oasis_build_lut", "oasis_quantize_act", "oasis_lut_gemm",
+               "oasis_outlier_compensate"):
+        assert fn in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", oasis.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(l.split()[-1] for l in out.splitlines() if l.strip())
+    for fn in declared_functions():
+        assert fn in exported, fn
+        assert hasattr(lib, fn)
+    assert set(oasis.EXPORTS) <= exported
+
+
+def test_status_strings(lib):
+    assert lib.oasis_status_str(0) == b"ok"
+    for s in range(-9, 0):
+        assert lib.oasis_status_str(s) != b"unknown status"
+    assert lib.oasis_version().startswith(b"oasis")
+
+
+# Host buffers stand in for device pointers: every call below fails its
+# argument check before anything touches them.
+BUF = np.zeros(1 << 16, dtype=np.uint8)
+P = BUF.ctypes.data          # 16-byte aligned by numpy for this size
+MIS = P + 2                  # misaligned
+
+
+def _cb(vals):
+    return np.asarray(vals, dtype=np.float16).view(np.uint16)
+
+
+def test_build_lut_errors(lib):
+    asc = _cb(np.linspace(-1, 1, 16))
+    cw = _cb(np.linspace(-1, 1, 16))
+    assert lib.oasis_build_lut(None, 4, cw.ctypes.data, 4, P, None) == -1
+    assert lib.oasis_build_lut(asc.ctypes.data, 5, cw.ctypes.data, 4, P, None) == -3
+    assert lib.oasis_build_lut(asc.ctypes.data, 4, cw.ctypes.data, 0, P, None) == -3
+    desc = _cb(np.linspace(1, -1, 16))
+    assert lib.oasis_build_lut(desc.ctypes.data, 4, cw.ctypes.data, 4, P, None) == -5
+    dup = _cb([0.0, 0.5, 0.5, 1.0])
+    assert lib.oasis_build_lut(dup.ctypes.data, 2, cw.ctypes.data, 4, P, None) == -5
+    bad = _cb([0.0, np.inf])
+    assert lib.oasis_build_lut(bad.ctypes.data, 1, cw.ctypes.data, 4, P, None) == -5
+    nanw = _cb([0.0, np.nan])
+    assert lib.oasis_build_lut(asc.ctypes.data, 4, nanw.ctypes.data, 1, P, None) == -5
+    assert lib.oasis_build_lut(asc.ctypes.data, 4, cw.ctypes.data, 4, MIS, None) == -6
+
+
+def test_quantize_errors(lib):
+    q = lib.oasis_quantize_act
+    assert q(P, 4, 12, P, 4, 1, 0, P, P, P, P, P, None) == -2        # d_in % 8
+    assert q(P, -1, 16, P, 4, 1, 0, P, P, P, P, P, None) == -2
+    assert q(P, 4, 16, P, 0, 1, 0, P, P, P, P, P, None) == -3
+    assert q(P, 4, 16, P, 4, 17, 0, P, P, P, P, P, None) == -4
+    assert q(P, 4, 16, P, 4, -1, 0, P, P, P, P, P, None) == -4
+    assert q(P, 4, 16, P, 4, 1, 2, P, P, P, P, P, None) == -7
+    assert q(P, 4, 65544, P, 4, 1, 0, P, P, P, P, P, None) == -9
+    assert q(P, 4, 32768, P, 4, 32768, 0, P, P, P, P, P, None) == -9   # LDS budget
+    assert q(None, 4, 16, P, 4, 1, 0, P, P, P, P, P, None) == -1
+    assert q(P, 4, 16, P, 4, 1, 0, P, P, None, P, P, None) == -1
+    assert q(MIS, 4, 16, P, 4, 1, 0, P, P, P, P, P, None) == -6
+    assert q(P, 0, 16, None, 4, 1, 0, None, None, None, None, None, None) == 0   # empty
+
+
+def test_gemm_errors(lib):
+    g = lib.oasis_lut_gemm
+    assert g(P, P, 4, 20, P, P, 8, P, 4, 4, 1, P, 0, None) == -2
+    assert g(P, P, 4, 16, P, P, -8, P, 4, 4, 1, P, 0, None) == -2
+    assert g(P, P, 4, 16, P, P, 8, P, 4, 9, 1, P, 0, None) == -3
+    assert g(P, P, 4, 16, P, P, 8, P, 4, 4, 2, P, 0, None) == -7
+    assert g(None, P, 4, 16, P, P, 8, P, 4, 4, 1, P, 0, None) == -1
+    assert g(P, P, 4, 16, MIS, P, 8, P, 4, 4, 1, P, 0, None) == -6
+    assert g(P, P, 0, 16, P, P, 8, P, 4, 4, 1, P, 0, None) == 0      # empty
+
+
+def test_compensate_errors(lib):
+    c = lib.oasis_outlier_compensate
+    assert c(P, P, P, 4, 3, P, P, 4, P, 20, 8, P, 1, None) == -2
+    assert c(P, P, P, 4, 17, P, P, 4, P, 16, 8, P, 1, None) == -4
+    assert c(P, P, P, 4, 3, P, P, 5, P, 16, 8, P, 1, None) == -3
+    assert c(None, P, P, 4, 3, P, P, 4, P, 16, 8, P, 1, None) == -1
+    assert c(P, P, P, 4, 3, P, P, 4, P, 16, 8, MIS, 1, None) == -6
+    assert c(P, P, P, 0, 3, P, P, 4, P, 16, 8, P, 1, None) == 0
+
+
+def test_pack_weight_indices_matches_oracle_packing():
+    from oracle import oasis_oracle as O
+    rng = np.random.default_rng(5)
+    w = rng.integers(0, 16, (24, 13)).astype(np.uint8)
+    assert np.array_equal(oasis.pack_weight_indices(w), O.pack_weight_indices(w))
+    with pytest.raises(oasis.OasisError):
+        oasis.pack_weight_indices(np.zeros((12, 4), dtype=np.uint8))

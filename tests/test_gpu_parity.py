@@ -1,0 +1,205 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integer outputs (activation codes, per-token scale, outlier lists, LUT block)
+and the residuals (one fp32 rounding on both sides) must match bit for bit.
+fp32 outputs must satisfy |y - y_ref| <= max(1e-3 * |y_ref|, 1e-2) for every
+entry, y_ref being the oracle's fp64 result.
+"""
+import numpy as np
+import pytest
+
+from oracle import oasis_oracle as O
+from paper_2507_23035_amd import oasis, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+RTOL, ATOL = 1e-3, 1e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oasis.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def upload(L):
+    x = torch.from_numpy(L.x.view(np.int16).copy()).to(dev())
+    idx_w = torch.from_numpy(oasis.pack_weight_indices(L.w_idx).view(np.int32)).to(dev())
+    s_w = torch.from_numpy(L.s_w).to(dev())
+    lut = oasis.build_lut(L.cb_a, L.spec.b_a, L.cb_w, L.spec.b_w)
+    return x, idx_w, s_w, lut
+
+
+def assert_close(y, ref, what):
+    y = np.asarray(y, dtype=np.float64)
+    err = np.abs(y - ref)
+    bound = np.maximum(RTOL * np.abs(ref), ATOL)
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {bad.sum()} of {bad.size} entries out of tolerance, "
+                           f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}")
+
+
+def check_quant(q, ref, k):
+    torch.cuda.synchronize()
+    assert np.array_equal(q["act_scale"].cpu().numpy().view(np.uint32),
+                          ref["t"].view(np.uint32)), "act_scale"
+    assert np.array_equal(q["idx_act"].cpu().numpy(), O.pack_act_indices(ref["a"])), "idx_act"
+    if k:
+        assert np.array_equal(q["max_idx"].cpu().numpy(), ref["max_idx"]), "max_idx"
+        assert np.array_equal(q["min_idx"].cpu().numpy(), ref["min_idx"]), "min_idx"
+        assert np.array_equal(q["residual"].cpu().numpy().view(np.uint32),
+                              ref["residual"].view(np.uint32)), "residual"
+
+
+def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_ABSMAX,
+             tokens=None):
+    """Run every entry point and compare with the oracle (all or some tokens)."""
+    b_a, b_w, k = L.spec.b_a, L.spec.b_w, L.spec.k
+    print(f"case {L.spec.name} n={L.spec.n} d_in={L.spec.d_in} d_out={L.spec.d_out} k={k} "
+          f"bits=({b_a},{b_w}) mode={scale_mode} tokens={tokens}", flush=True)
+    x, idx_w, s_w, lut = upload(L)
+    ref = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, b_a, b_w, k, mode=scale_mode,
+                    tokens=tokens)
+    q = oasis.quantize_act(x, lut, b_a, k, scale_mode)
+    check_quant(q, ref, k)
+    rows = slice(None) if tokens is None else list(tokens)
+    for algo in algos:
+        ys = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algo)
+        torch.cuda.synchronize()
+        assert_close(ys.cpu().numpy()[rows], ref["y_star"], f"Y* algo={algo}")
+    yc = oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w,
+                                  s_w, L.spec.d_in, accumulate=False)
+    torch.cuda.synchronize()
+    assert_close(yc.cpu().numpy()[rows], ref["y_comp"], "Y'")
+    for algo in algos:
+        r = oasis.forward(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode, algo)
+        torch.cuda.synchronize()
+        assert_close(r["y"].cpu().numpy()[rows], ref["y"], f"Y algo={algo}")
+    # the other merge order: main branch first, compensation merged into it
+    y = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
+    oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w, s_w,
+                             L.spec.d_in, y=y, accumulate=True)
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy()[rows], ref["y"], "Y (gemm then compensate)")
+    return ref
+
+
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("b_a,b_w", [(4, 4), (3, 4), (2, 3), (1, 1), (4, 2)])
+def test_lut_block_bitexact(b_a, b_w):
+    rng = np.random.default_rng(b_a * 10 + b_w)
+    ca = np.unique(rng.standard_normal(1 << b_a).astype(np.float16))
+    cw = rng.standard_normal(1 << b_w).astype(np.float16)
+    assert ca.size == 1 << b_a
+    lut = oasis.build_lut(ca, b_a, cw, b_w)
+    torch.cuda.synchronize()
+    raw = lut.cpu().numpy()
+    got = raw[:1024].view(np.float32)
+    want = np.zeros(256, dtype=np.float32)
+    want[: 1 << (b_a + b_w)] = O.build_lut(ca, cw, b_a, b_w)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    cba = np.zeros(16, dtype=np.uint16)
+    cba[: ca.size] = ca.view(np.uint16)
+    cbw = np.zeros(16, dtype=np.uint16)
+    cbw[: cw.size] = cw.view(np.uint16)
+    assert np.array_equal(raw[1024:1056].view(np.uint16), cba)
+    assert np.array_equal(raw[1056:1088].view(np.uint16), cbw)
+
+
+def test_tiny_layer():
+    run_full(synth.make_layer(synth.config("tiny_4x256x256")))
+
+
+def test_decode_layer():
+    run_full(synth.make_layer(synth.config("decode_8x4096x4096")))
+
+
+RAGGED = [
+    # n, d_in, d_out, k, b_a, b_w, seed
+    (1, 64, 1, 1, 4, 4, 0),
+    (3, 264, 100, 4, 4, 4, 1),
+    (5, 1032, 130, 0, 4, 4, 2),
+    (17, 512, 257, 8, 3, 4, 3),
+    (16, 256, 64, 128, 4, 4, 4),     # k = d_in / 2
+    (2, 128, 96, 128, 4, 4, 5),      # k = d_in: every channel in both lists
+    (33, 264, 300, 3, 2, 3, 6),      # prefill tiling, ragged everywhere
+    (130, 136, 129, 5, 4, 4, 7),
+    (40, 4096, 200, 32, 1, 1, 8),
+    (64, 520, 512, 16, 4, 2, 9),
+]
+
+
+@pytest.mark.parametrize("n,d_in,d_out,k,b_a,b_w,seed", RAGGED)
+def test_ragged_shapes(n, d_in, d_out, k, b_a, b_w, seed):
+    run_full(synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed, b_a=b_a, b_w=b_w)))
+
+
+def test_scale_mode_none():
+    spec = synth.custom(6, 256, 80, 4, seed=11, dist="normal", outlier_count=2,
+                        outlier_scale=4.0)
+    run_full(synth.make_layer(spec), scale_mode=oasis.SCALE_NONE)
+
+
+def test_degenerate_tokens():
+    """Constant tokens, an all-zero token, signed zeros and heavy ties."""
+    L = synth.make_layer(synth.custom(6, 128, 72, 6, seed=12))
+    x = L.x.copy()
+    x[0, :] = np.float16(1.5)                                  # constant: lists overlap
+    x[1, :] = np.float16(0.0)                                  # all zero: t = 0
+    x[2, ::2] = np.float16(-0.0)
+    x[2, 1::2] = np.float16(0.0)
+    x[3, :] = np.float16(np.round(np.linspace(-2, 2, 128)))    # five distinct values
+    x[4, :] = np.float16(-7.0)
+    x[4, 77] = np.float16(7.0)
+    L.x = x
+    run_full(L)
+
+
+def test_empty_batch():
+    L = synth.make_layer(synth.custom(2, 64, 32, 2, seed=13))
+    x, idx_w, s_w, lut = upload(L)
+    x0 = x[:0]
+    q = oasis.quantize_act(x0, lut, 4, 2)
+    y = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, 4, 4)
+    assert y.shape == (0, 32)
+
+
+def test_repeated_calls_are_stable():
+    """Same inputs, 5 calls: integer outputs identical every time."""
+    L = synth.make_layer(synth.config("decode_8x4096x4096"))
+    x, idx_w, s_w, lut = upload(L)
+    first = None
+    for _ in range(5):
+        q = oasis.forward(x, lut, idx_w, s_w, 4, 4, 32)
+        torch.cuda.synchronize()
+        cur = {kk: v.cpu().numpy().copy() for kk, v in q.items()}
+        if first is None:
+            first = cur
+        for kk in ("idx_act", "act_scale", "max_idx", "min_idx", "residual"):
+            assert np.array_equal(cur[kk], first[kk])
+        assert_close(cur["y"], first["y"].astype(np.float64), "repeat")
+
+
+# ----------------------------------------------------------------------------
+# Full-size layers: every token's quantization, sampled rows of the outputs
+# ----------------------------------------------------------------------------
+FULL = ["prefill_up_2048x4096x11008", "prefill_down_2048x11008x4096",
+        "large_decode_16x8192x28672", "large_prefill_4096x8192x28672"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_layers(name):
+    L = synth.make_layer(synth.config(name))
+    n = L.spec.n
+    rng = np.random.default_rng(3)
+    tokens = sorted({0, n - 1, *rng.choice(n, 2, replace=False).tolist()})
+    algos = (oasis.ALGO_MFMA, oasis.ALGO_LUT) if n <= 2048 else (oasis.ALGO_MFMA,)
+    run_full(L, algos=algos, tokens=tokens)
