@@ -1,0 +1,235 @@
+"""Benchmark of the OASIS hot path on one MI355X.
+
+A step is one pass of the whole path over one synthetic layer: build the LUT
+block, quantize the activations (scale, codes, top-k outliers, residuals),
+compensate the outliers, and run the LUT-GEMM merged into the compensation.
+Inputs are resident in HBM when timing starts; the weight codes are rotated
+over enough copies (> 512 MiB in total) that the 256 MiB last-level cache
+cannot serve them.  The timed steps are captured once into one HIP graph and
+replayed (no host launch gaps); per-kernel durations come from HIP events
+around each kernel in a second pass of the same steps, launched eagerly
+behind a spin kernel so that every launch is queued before the GPU gets to
+it.
+
+Prints ONE JSON line (rank 0).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective TOPS (2*n*d_in*d_out/s) + HBM GB/s, % of roofline, at decode & prefill"
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+
+
+def gemm_bytes(n, d_in, d_out):
+    """Algorithmic HBM bytes of one main-branch launch: weight codes (0.5 B
+    each), activation codes (0.5 B each), both scale vectors, and Y read and
+    written once (the GEMM merges into the compensation term)."""
+    return d_in * d_out // 2 + n * d_in // 2 + 4 * n + 4 * d_out + 8 * n * d_out
+
+
+def step_bytes(n, d_in, d_out, k):
+    """Algorithmic HBM bytes of one whole step."""
+    quant = 2 * n * d_in + n * d_in // 2 + 4 * n + 16 * n * k       # x in; codes, t, lists out
+    comp = 12 * n * k + 2 * n * k * d_out // 2 + 4 * d_out + 4 * n * d_out
+    return quant + comp + gemm_bytes(n, d_in, d_out)
+
+
+def cpu_baseline(layer, budget_s=12.0):
+    """Time the oracle's whole-layer forward on the host (single-threaded numpy)."""
+    from oracle import oasis_oracle as O
+    s = layer.spec
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w, s.k)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 50:
+            break
+    per = el / reps
+    return {"value": 2.0 * s.n * s.d_in * s.d_out / per / 1e12,
+            "unit": "effective TOPS", "cores": 1, "kind": "oracle",
+            "sample": f"whole {s.name} layer ({s.n} tokens, k={s.k}), {reps} forward passes, "
+                      f"{per * 1e3:.1f} ms each, numpy single thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="decode_8x4096x4096")
+    ap.add_argument("--algo", default="mfma", choices=["mfma", "lut"])
+    ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
+    ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--verbose", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2507_23035_amd import oasis, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU", file=sys.stderr)
+        sys.exit(1)
+    oasis.load()
+    dev = torch.device("cuda:0")
+    layer = synth.make_layer(synth.config(args.config))
+    s = layer.spec
+    n, d_in, d_out, k, b_a, b_w = s.n, s.d_in, s.d_out, s.k, s.b_a, s.b_w
+    algo = oasis.ALGO_MFMA if args.algo == "mfma" else oasis.ALGO_LUT
+
+    wbytes = d_in * d_out // 2
+    copies = args.copies or max(1, min(64, (512 << 20) // wbytes + 1))
+    packed = oasis.pack_weight_indices(layer.w_idx).view(np.int32)
+    idx_w = [torch.from_numpy(packed).to(dev) for _ in range(copies)]
+    x = torch.from_numpy(layer.x.view(np.int16).copy()).to(dev)
+    s_w = torch.from_numpy(layer.s_w).to(dev)
+    cb_a, cb_w = layer.cb_a, layer.cb_w
+    lut = torch.empty(oasis.LUT_BLOCK_BYTES, dtype=torch.uint8, device=dev)
+    q = {
+        "idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=dev),
+        "act_scale": torch.empty(n, dtype=torch.float32, device=dev),
+        "max_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+        "min_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+        "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
+    }
+    y = torch.empty((n, d_out), dtype=torch.float32, device=dev)
+    names = ["build_lut", "quantize_act", "outlier_compensate", "lut_gemm"]
+
+    def step(c, evs=None):
+        if evs is not None:
+            evs[0].record()
+        oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
+        if evs is not None:
+            evs[1].record()
+        oasis.quantize_act(x, lut, b_a, k, out=q)
+        if evs is not None:
+            evs[2].record()
+        oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut, b_w,
+                                 s_w, d_in, y=y, accumulate=False)
+        if evs is not None:
+            evs[3].record()
+        oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, algo, y=y,
+                       accumulate=True)
+        if evs is not None:
+            evs[4].record()
+
+    nsteps = args.steps
+
+    def capture(count, first):
+        """One HIP graph holding `count` consecutive steps (rotating weight copies)."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(first, first + count):
+                step(i % copies)
+        return g
+
+    # prime the library and the allocator outside capture
+    for c in range(min(copies, 2)):
+        step(c)
+    torch.cuda.synchronize()
+    mode = "graph"
+    try:
+        g_warm = capture(args.warmup, 0) if args.warmup else None
+        g_timed = capture(nsteps, args.warmup)
+    except Exception as e:
+        if args.verbose:
+            print(f"graph capture failed ({e}); timing eager launches", file=sys.stderr)
+        mode = "eager"
+        torch.cuda.synchronize()
+    if args.eager:
+        mode = "eager"
+
+    # ---- timed region: exactly `nsteps` steps, wall clock, synchronized on both sides
+    if mode == "graph":
+        if g_warm is not None:
+            g_warm.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g_timed.replay()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    else:
+        for i in range(args.warmup):
+            step(i % copies)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.warmup, args.warmup + nsteps):
+            step(i % copies)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+
+    # ---- per-kernel durations: the same steps launched eagerly behind a spin
+    # kernel, so every launch is queued before the GPU reaches it and the HIP
+    # events around each kernel see no host gaps.
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(nsteps)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2.4e9 * (0.002 + nsteps * 60e-6)))   # ~2 ms + 60 us per step
+    for i in range(nsteps):
+        step((args.warmup + i) % copies, events[i])
+    torch.cuda.synchronize()
+
+    per_kernel = np.array([[events[i][j].elapsed_time(events[i][j + 1])
+                            for j in range(4)] for i in range(nsteps)]) * 1e3   # us
+    kern_us = {nm: float(np.mean(per_kernel[:, j])) for j, nm in enumerate(names)}
+    ms_per_step = elapsed * 1e3 / nsteps
+    ops = 2.0 * n * d_in * d_out
+    value = ops / (ms_per_step * 1e-3) / 1e12
+
+    gemm_us = kern_us["lut_gemm"]
+    gb = gemm_bytes(n, d_in, d_out)
+    achieved = gb / (gemm_us * 1e-6) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "lut_gemm (k_gemm_mfma_decode)" if algo == oasis.ALGO_MFMA and n <= 32
+                else "lut_gemm", "kernel_us": round(gemm_us, 3), "bytes_per_launch": gb}
+    if n > 32:
+        tflops = ops / (gemm_us * 1e-6) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),
+                    "traffic": None, "kernel": "lut_gemm", "kernel_us": round(gemm_us, 3),
+                    "flops_per_launch": ops}
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "effective TOPS",
+        "n_gpus": 1,
+        "steps": nsteps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": s.name, "n": n, "d_in": d_in, "d_out": d_out, "k_per_side": k,
+                   "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
+                   "weight_copies": copies},
+        "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k) / (ms_per_step * 1e-3) / 1e9, 1),
+        "kernel_us": {kk: round(v, 3) for kk, v in kern_us.items()},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layer)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

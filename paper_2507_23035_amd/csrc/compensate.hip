@@ -5,39 +5,64 @@
 // are dequantized with the weight codebook (the Dequant Unit) and multiplied
 // by the residual (the MAC units), then merged into the main-branch output.
 //
-// One workgroup per (token, 256 output columns); the token's channel ids and
-// residuals are wave-uniform, so they travel through scalar loads, and
-// zero residuals (channels compensated through the max list already) are
-// skipped.
+// One workgroup per (token, 64 output columns); its 4 waves split the token's
+// 2k listed channels and are summed through LDS.  A lane owns one column and
+// issues the word loads of 16 listed channels before using any of them, so
+// the outlier stream costs a few memory latencies rather than one per
+// outlier.  Channel ids and residuals are wave-uniform (scalar loads); zero
+// residuals (channels already compensated through the max list) are skipped.
 #include "common.h"
 
 namespace oasis {
 
-constexpr int CT = 256;
+constexpr int CMP_COLS = 64;
+constexpr int CMP_BATCH = 16;
 
-__global__ void __launch_bounds__(CT) k_compensate(CompArgs A) {
+__global__ void __launch_bounds__(256) k_compensate(CompArgs A) {
   __shared__ float cw[16];
-  const int tid = threadIdx.x;
+  __shared__ float red[4][CMP_COLS];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   if (tid < 16) cw[tid] = h2f(A.lut->cb_wgt[tid]);
-  __syncthreads();
-  const int j = blockIdx.y * CT + tid;
   const int i = blockIdx.x;
-  const int k = A.k;
-  const int d_out = A.d_out;
+  const int j = blockIdx.y * CMP_COLS + lane;
+  const int k = A.k, E = 2 * k;
+  const int d_out = A.d_out, d_in = A.d_in;
   const size_t kr = (size_t)i * k;
-  const float* res = A.residual + (size_t)i * 2 * k;
+  const float* res = A.residual + (size_t)i * E;
+  // this wave's share of the listed channels
+  const int per = (E + 3) / 4;
+  const int e_beg = min(E, wave * per), e_end = min(E, e_beg + per);
+  const bool col_ok = j < d_out;
+  __syncthreads();
+
   float acc = 0.0f;
-  if (j < d_out) {
-    for (int e = 0; e < 2 * k; ++e) {
-      const float r = res[e];
-      const int p = e < k ? A.max_idx[kr + e] : A.min_idx[kr + (e - k)];
-      if (r == 0.0f || p < 0 || p >= A.d_in) continue;  // uniform branch
-      const uint32_t w = A.idx_w[(size_t)(p >> 3) * d_out + j];
-      const uint32_t code = (w >> (4 * (p & 7))) & 15u;
-      acc += r * cw[code];
+  for (int e0 = e_beg; e0 < e_end; e0 += CMP_BATCH) {
+    int sh[CMP_BATCH];
+    float r[CMP_BATCH];
+    uint32_t w[CMP_BATCH];
+#pragma unroll
+    for (int u = 0; u < CMP_BATCH; ++u) {
+      const int e = e0 + u;
+      int p = -1;
+      r[u] = 0.0f;
+      if (e < e_end) {
+        p = e < k ? A.max_idx[kr + e] : A.min_idx[kr + (e - k)];
+        r[u] = res[e];
+      }
+      const bool live = p >= 0 && p < d_in && r[u] != 0.0f;  // wave-uniform
+      if (!live) r[u] = 0.0f;
+      sh[u] = live ? 4 * (p & 7) : 0;
+      w[u] = 0u;
+      if (live && col_ok) w[u] = A.idx_w[(size_t)(p >> 3) * d_out + j];
     }
+#pragma unroll
+    for (int u = 0; u < CMP_BATCH; ++u) acc += r[u] * cw[(w[u] >> sh[u]) & 15u];
+  }
+  red[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0 && col_ok) {
+    const float v = A.w_scale[j] * (red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane]);
     float* dst = A.y + (size_t)i * d_out + j;
-    const float v = A.w_scale[j] * acc;
     if (A.accumulate)
       *dst += v;
     else
@@ -51,8 +76,8 @@ hipError_t launch_compensate(const CompArgs& a, hipStream_t s) {
     if (a.accumulate) return hipSuccess;
     return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
   }
-  dim3 grid(a.n, (a.d_out + CT - 1) / CT);
-  hipLaunchKernelGGL(k_compensate, grid, dim3(CT), 0, s, a);
+  dim3 grid(a.n, (a.d_out + CMP_COLS - 1) / CMP_COLS);
+  hipLaunchKernelGGL(k_compensate, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -31,13 +31,26 @@ namespace oasis {
 // ----------------------------------------------------------------------------
 constexpr int DEC_R = 8;  // replication of the byte -> fp16 pair tables
 
-// byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes
+// byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes.
+// `cb` is the 16-entry codebook already staged in LDS.
 __device__ __forceinline__ void build_pair_table(uint32_t* tab, const uint16_t* cb, int tid,
                                                  int nthreads) {
   for (int e = tid; e < 256 * DEC_R; e += nthreads) {
     const int b = e / DEC_R;
     tab[e] = (uint32_t)cb[b & 15] | ((uint32_t)cb[b >> 4] << 16);
   }
+}
+
+// Stage both codebooks of the LUT block in LDS, then build both pair tables.
+__device__ __forceinline__ void build_tables(const oasis_lut_block* lut, uint16_t (&cbs)[2][16],
+                                             uint32_t* tabW, uint32_t* tabA, int tid,
+                                             int nthreads) {
+  if (tid < 16) cbs[0][tid] = lut->cb_wgt[tid];
+  else if (tid < 32) cbs[1][tid - 16] = lut->cb_act[tid - 16];
+  __syncthreads();
+  build_pair_table(tabW, cbs[0], tid, nthreads);
+  build_pair_table(tabA, cbs[1], tid, nthreads);
+  __syncthreads();
 }
 
 __device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, int lane_off) {
@@ -64,155 +77,208 @@ __device__ __forceinline__ uint4_t load_w4(const uint32_t* __restrict__ idx_w, s
   return v;
 }
 
-// The 16-column x 16-token MFMA tiles of one wave: CG groups of 64 columns
-// (4 tiles each) by TF groups of 16 tokens.  Runs the blocks of 16 words in
-// [blk_begin, blk_end) with a stride, accumulating into acc.
-template <int CG, int TF>
-__device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0, int blk_begin,
-                                            int blk_end, int blk_stride, const uint32_t* tabW,
-                                            const uint32_t* tabA,
-                                            float4_t (&acc)[CG * 4][TF]) {
+// Raw codes of one block of 16 words for one wave: the activation words of
+// its tokens (4 consecutive words per lane) and, for each of the 4 steps, CW
+// consecutive weight words (CW output columns) per lane.
+template <int CW, int TF>
+struct BlockCodes {
+  uint4_t av[TF];
+  uint32_t wv[4][CW];
+};
+
+template <int CW>
+__device__ __forceinline__ void load_words(const uint32_t* __restrict__ row, int j, int d_out,
+                                           uint32_t (&out)[CW]) {
+  if (CW == 4 && (d_out & 3) == 0 && j + 3 < d_out) {
+    const uint4_t v = *reinterpret_cast<const uint4_t*>(row + j);
+#pragma unroll
+    for (int c = 0; c < CW; ++c) out[c] = v[c];
+  } else if (CW == 2 && (d_out & 1) == 0 && j + 1 < d_out) {
+    const uint2 v = *reinterpret_cast<const uint2*>(row + j);
+    out[0] = v.x;
+    out[CW - 1] = v.y;
+  } else {
+#pragma unroll
+    for (int c = 0; c < CW; ++c) out[c] = (j + c < d_out) ? row[j + c] : 0u;
+  }
+}
+
+template <int CW, int TF>
+__device__ __forceinline__ void load_block(const GemmArgs& A, int blk, int j0, int tok0,
+                                           BlockCodes<CW, TF>& bc) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, m = lane & 15;
-  const int lane_off = lane & (DEC_R - 1);
   const int KB = A.d_in >> 3;
   const int d_out = A.d_out;
-  const bool vec_ok = (d_out & 3) == 0;
-  const size_t arow_words = (size_t)(A.d_in >> 3);
+  const size_t arow_words = (size_t)KB;
   const uint32_t* aw = reinterpret_cast<const uint32_t*>(A.idx_act);
-
-  for (int blk = blk_begin; blk < blk_end; blk += blk_stride) {
-    const int kw0 = blk * 16 + 4 * g;  // this lane group's first word in the block
-    // activation words of this lane's tokens: 4 consecutive words, one per step
-    uint4_t av[TF];
+  const int kw0 = blk * 16 + 4 * g;  // this lane group's first word in the block
 #pragma unroll
-    for (int f = 0; f < TF; ++f) {
-      const int tok = tok0 + 16 * f + m;
-      av[f] = uint4_t{0u, 0u, 0u, 0u};
-      if (tok < A.n) {
-        const uint32_t* src = aw + (size_t)tok * arow_words + kw0;
-        if (kw0 + 3 < KB && (arow_words & 3) == 0) {
-          av[f] = *reinterpret_cast<const uint4_t*>(src);
-        } else {
+  for (int f = 0; f < TF; ++f) {
+    const int tok = tok0 + 16 * f + m;
+    bc.av[f] = uint4_t{0u, 0u, 0u, 0u};
+    if (tok < A.n) {
+      const uint32_t* src = aw + (size_t)tok * arow_words + kw0;
+      if (kw0 + 3 < KB && (arow_words & 3) == 0) {
+        bc.av[f] = *reinterpret_cast<const uint4_t*>(src);
+      } else {
 #pragma unroll
-          for (int s = 0; s < 4; ++s)
-            if (kw0 + s < KB) av[f][s] = src[s];
-        }
+        for (int s = 0; s < 4; ++s)
+          if (kw0 + s < KB) bc.av[f][s] = src[s];
       }
     }
-    // weight words: 4 rows (steps) x CG*4 columns for this lane
-    uint4_t wv[4][CG];
+  }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int kw = kw0 + s;
+  for (int s = 0; s < 4; ++s) {
+    const int kw = kw0 + s;
+    if (kw < KB) {
+      load_words<CW>(A.idx_w + (size_t)kw * d_out, j0 + CW * m, d_out, bc.wv[s]);
+    } else {
 #pragma unroll
-      for (int h = 0; h < CG; ++h) {
-        if (kw < KB)
-          wv[s][h] = load_w4(A.idx_w, (size_t)kw * d_out, j0 + 64 * h + 4 * m, d_out, vec_ok);
-        else
-          wv[s][h] = uint4_t{0u, 0u, 0u, 0u};
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const bool live = (kw0 + s) < KB;  // words past the end contribute nothing
-      half8_t bf[TF];
-#pragma unroll
-      for (int f = 0; f < TF; ++f) {
-        bf[f] = expand_word(av[f][s], tabA, lane_off);
-        const bool tok_ok = (tok0 + 16 * f + m) < A.n;
-        if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int h = 0; h < CG; ++h) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const half8_t af = expand_word(wv[s][h][c], tabW, lane_off);
-#pragma unroll
-          for (int f = 0; f < TF; ++f)
-            acc[4 * h + c][f] =
-                __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[f], acc[4 * h + c][f], 0, 0, 0);
-        }
-      }
+      for (int c = 0; c < CW; ++c) bc.wv[s][c] = 0u;
     }
   }
 }
 
-// Output of tile (4h + c, f): lane (g, tc) holds rows m = 4g + r, i.e. output
-// columns j0 + 64h + 16g + 4r + c of token tok0 + 16f + tc.
-__device__ __forceinline__ void store_out(const GemmArgs& A, int tok, int j, float v, bool atomic) {
+// Expand the codes of one block to fp16 centroid values and run its MFMAs:
+// CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
+template <int CW, int TF>
+__device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
+                                          const BlockCodes<CW, TF>& bc, const uint32_t* tabW,
+                                          const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, m = lane & 15;
+  const int lane_off = lane & (DEC_R - 1);
+  const int KB = A.d_in >> 3;
+  const int kw0 = blk * 16 + 4 * g;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const bool live = (kw0 + s) < KB;  // words past the end contribute nothing
+    half8_t bf[TF];
+#pragma unroll
+    for (int f = 0; f < TF; ++f) {
+      bf[f] = expand_word(bc.av[f][s], tabA, lane_off);
+      const bool tok_ok = (tok0 + 16 * f + m) < A.n;
+      if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int c = 0; c < CW; ++c) {
+      const half8_t af = expand_word(bc.wv[s][c], tabW, lane_off);
+#pragma unroll
+      for (int f = 0; f < TF; ++f)
+        acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[f], acc[c][f], 0, 0, 0);
+    }
+  }
+}
+
+// Blocks blk_begin, blk_begin + stride, ... < blk_end of one wave, the next
+// block's codes loaded while the current one is expanded and multiplied.
+// `first` holds the codes of blk_begin (loaded by the caller before the
+// decode tables were built).
+template <int CW, int TF>
+__device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0, int blk_begin,
+                                            int blk_end, int blk_stride,
+                                            BlockCodes<CW, TF>& first, const uint32_t* tabW,
+                                            const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
+  BlockCodes<CW, TF> cur = first;
+  for (int blk = blk_begin; blk < blk_end; blk += blk_stride) {
+    BlockCodes<CW, TF> nxt;
+    const int nb = blk + blk_stride;
+    if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, nxt);
+    mma_block<CW, TF>(A, blk, tok0, cur, tabW, tabA, acc);
+    if (nb < blk_end) cur = nxt;
+  }
+}
+
+// Output of tile (c, f): lane (g, tc) holds rows m = 4g + r, i.e. output
+// column j0 + CW*(4g + r) + c of token tok0 + 16f + tc.
+__device__ __forceinline__ void store_out(const GemmArgs& A, int tok, int j, float v) {
   if (tok >= A.n || j >= A.d_out) return;
   float* dst = A.y + (size_t)tok * A.d_out + j;
   const float val = A.act_scale[tok] * A.w_scale[j] * v;
-  if (atomic)
-    atomicAdd(dst, val);
-  else if (A.accumulate)
+  if (A.accumulate)
     *dst += val;
   else
     *dst = val;
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin (id mod 8).  Map ids so that
+// each XCD gets a contiguous range of tiles and neighbouring tiles share its
+// L2.  A bijection on [0, T).
+__device__ __forceinline__ int xcd_tile(int b, int T) {
+  const int per = T >> 3;
+  return b < 8 * per ? (b & 7) * per + (b >> 3) : b;
+}
+
 // ----------------------------------------------------------------------------
-// MFMA kernel, decode tiling: 4 waves share 64 columns and split the words of
-// the WG's input-channel slice; gridDim.z slices are merged with atomics.
+// MFMA kernel, few tokens (GEMV-like): one workgroup per 16*CW output
+// columns, its NW waves interleave the K blocks and are summed through LDS,
+// so every output is written once, without atomics.
 // ----------------------------------------------------------------------------
-template <int TF>
-__global__ void __launch_bounds__(256) k_gemm_mfma_decode(GemmArgs A, int blk_per_split) {
+template <int CW, int TF, int NW>
+__global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
   __shared__ uint32_t tabW[256 * DEC_R];
   __shared__ uint32_t tabA[256 * DEC_R];
-  __shared__ float4_t red[4][4 * TF][64];
+  __shared__ float4_t red[NW][CW * TF][64];
+  __shared__ uint16_t cbs[2][16];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  build_pair_table(tabW, A.lut->cb_wgt, tid, 256);
-  build_pair_table(tabA, A.lut->cb_act, tid, 256);
-  __syncthreads();
 
-  const int j0 = blockIdx.x * 64;
+  const int j0 = xcd_tile(blockIdx.x, ntiles) * 16 * CW;
   const int nblk = (A.d_in / 8 + 15) / 16;
-  const int b0 = blockIdx.z * blk_per_split;
-  const int b1 = min(nblk, b0 + blk_per_split);
 
-  float4_t acc[4][TF];
+  // issue the first block's loads, then build the tables while they fly
+  BlockCodes<CW, TF> first;
+  if (wave < nblk) load_block<CW, TF>(A, wave, j0, 0, first);
+  build_tables(A.lut, cbs, tabW, tabA, tid, NW * 64);
+
+  float4_t acc[CW][TF];
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
+  for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  mfma_blocks<1, TF>(A, j0, 0, b0 + wave, b1, 4, tabW, tabA, acc);
+  if (wave < nblk) mfma_blocks<CW, TF>(A, j0, 0, wave, nblk, NW, first, tabW, tabA, acc);
 
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
+  for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) red[wave][c * TF + f][lane] = acc[c][f];
   __syncthreads();
 
-  const bool atomic = gridDim.z > 1;
   const int g = lane >> 4, tc = lane & 15;
-  for (int t = wave; t < 4 * TF; t += 4) {
-    float4_t v = red[0][t][lane] + red[1][t][lane] + red[2][t][lane] + red[3][t][lane];
-    const int c = t / TF, f = t % TF;
-    const int tok = 16 * f + tc;
+  for (int t = wave; t < CW * TF; t += NW) {
+    float4_t v = red[0][t][lane];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) store_out(A, tok, j0 + 16 * g + 4 * r + c, v[r], atomic);
+    for (int w = 1; w < NW; ++w) v += red[w][t][lane];
+    const int c = t / TF, f = t % TF;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) store_out(A, 16 * f + tc, j0 + CW * (4 * g + r) + c, v[r]);
   }
 }
 
 // ----------------------------------------------------------------------------
 // MFMA kernel, prefill tiling: 2 x 2 waves, each 64 columns x 64 tokens, over
-// the whole reduction; WG tile 128 columns x 128 tokens.
+// the whole reduction; WG tile 128 columns x 128 tokens.  Tiles are ordered
+// column-major over the XCDs so that one XCD's L2 holds few weight columns.
 // ----------------------------------------------------------------------------
 constexpr int PF_TF = 4;
 
-__global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A) {
+__global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A, int ncx, int nty) {
   __shared__ uint32_t tabW[256 * DEC_R];
   __shared__ uint32_t tabA[256 * DEC_R];
+  __shared__ uint16_t cbs[2][16];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  build_pair_table(tabW, A.lut->cb_wgt, tid, 256);
-  build_pair_table(tabA, A.lut->cb_act, tid, 256);
-  __syncthreads();
 
-  const int j0 = blockIdx.x * 128 + (wave & 1) * 64;
-  const int tok0 = blockIdx.y * 128 + (wave >> 1) * 64;
+  const int r = xcd_tile(blockIdx.x, ncx * nty);
+  const int cx = r / nty, ty = r % nty;
+  const int j0 = cx * 128 + (wave & 1) * 64;
+  const int tok0 = ty * 128 + (wave >> 1) * 64;
   const int nblk = (A.d_in / 8 + 15) / 16;
+  const bool active = j0 < A.d_out && tok0 < A.n;
+
+  BlockCodes<4, PF_TF> first;
+  if (active) load_block<4, PF_TF>(A, 0, j0, tok0, first);
+  build_tables(A.lut, cbs, tabW, tabA, tid, 256);
 
   float4_t acc[4][PF_TF];
 #pragma unroll
@@ -220,8 +286,7 @@ __global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A) {
 #pragma unroll
     for (int f = 0; f < PF_TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (j0 < A.d_out && tok0 < A.n)
-    mfma_blocks<1, PF_TF>(A, j0, tok0, 0, nblk, 1, tabW, tabA, acc);
+  if (active) mfma_blocks<4, PF_TF>(A, j0, tok0, 0, nblk, 1, first, tabW, tabA, acc);
 
   const int g = lane >> 4, tc = lane & 15;
 #pragma unroll
@@ -229,32 +294,40 @@ __global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A) {
 #pragma unroll
     for (int f = 0; f < PF_TF; ++f)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        store_out(A, tok0 + 16 * f + tc, j0 + 16 * g + 4 * r + c, acc[c][f][r], false);
+      for (int q = 0; q < 4; ++q)
+        store_out(A, tok0 + 16 * f + tc, j0 + 4 * (4 * g + q) + c, acc[c][f][q]);
+}
+
+template <int CW, int TF, int NW>
+static void launch_gemv(const GemmArgs& a, hipStream_t s) {
+  const int ntiles = (a.d_out + 16 * CW - 1) / (16 * CW);
+  hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW>), dim3(ntiles), dim3(NW * 64), 0, s, a,
+                     ntiles);
+}
+
+template <int TF>
+static void launch_gemv_tf(const GemmArgs& a, hipStream_t s) {
+  // widest column tile that still gives >= 256 workgroups; LDS reduction
+  // buffer NW * CW * TF KiB kept <= 32 KiB
+  if ((a.d_out + 63) / 64 >= 256) {
+    if (TF == 1) launch_gemv<4, TF, 8>(a, s);
+    else launch_gemv<4, TF, 4>(a, s);
+  } else if ((a.d_out + 31) / 32 >= 256) {
+    if (TF == 1) launch_gemv<2, TF, 16>(a, s);
+    else launch_gemv<2, TF, 8>(a, s);
+  } else {
+    launch_gemv<1, TF, 16>(a, s);
+  }
 }
 
 hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s) {
-  const int KB = a.d_in / 8;
-  const int nblk = (KB + 15) / 16;
-  if (a.n <= 32) {
-    const int ct = (a.d_out + 63) / 64;
-    int split = (2048 + ct - 1) / ct;
-    split = min(split, max(1, nblk / 4));
-    split = max(1, split);
-    int bps = (nblk + split - 1) / split;
-    split = (nblk + bps - 1) / bps;
-    if (split > 1 && !a.accumulate) {
-      hipError_t e = launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
-      if (e != hipSuccess) return e;
-    }
-    dim3 grid(ct, 1, max(1, split));
-    if (a.n <= 16)
-      hipLaunchKernelGGL(k_gemm_mfma_decode<1>, grid, dim3(256), 0, s, a, max(1, bps));
-    else
-      hipLaunchKernelGGL(k_gemm_mfma_decode<2>, grid, dim3(256), 0, s, a, max(1, bps));
+  if (a.n <= 16) {
+    launch_gemv_tf<1>(a, s);
+  } else if (a.n <= 32) {
+    launch_gemv_tf<2>(a, s);
   } else {
-    dim3 grid((a.d_out + 127) / 128, (a.n + 127) / 128, 1);
-    hipLaunchKernelGGL(k_gemm_mfma_prefill, grid, dim3(256), 0, s, a);
+    const int ncx = (a.d_out + 127) / 128, nty = (a.n + 127) / 128;
+    hipLaunchKernelGGL(k_gemm_mfma_prefill, dim3(ncx * nty), dim3(256), 0, s, a, ncx, nty);
   }
   return hipGetLastError();
 }
@@ -270,8 +343,11 @@ constexpr int LUT_TN = 8;   // tokens per WG
 __global__ void __launch_bounds__(256) k_gemm_lut(GemmArgs A, int words_per_split) {
   __shared__ float lut_s[256 * LUT_R];
   __shared__ float red[4][LUT_TN][64];
+  __shared__ float lut1[256];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  for (int e = tid; e < 256 * LUT_R; e += 256) lut_s[e] = A.lut->lut[e / LUT_R];
+  lut1[tid] = A.lut->lut[tid];  // one coalesced load, then replicate from LDS
+  __syncthreads();
+  for (int e = tid; e < 256 * LUT_R; e += 256) lut_s[e] = lut1[e / LUT_R];
   __syncthreads();
 
   const int j = blockIdx.x * 64 + lane;
@@ -314,7 +390,17 @@ __global__ void __launch_bounds__(256) k_gemm_lut(GemmArgs A, int words_per_spli
   const bool atomic = gridDim.z > 1;
   for (int t = wave; t < LUT_TN; t += 4) {
     const float v = red[0][t][lane] + red[1][t][lane] + red[2][t][lane] + red[3][t][lane];
-    if (t < ntok) store_out(A, tok0 + t, j, v, atomic);
+    if (t < ntok && j < A.d_out) {
+      const int tok = tok0 + t;
+      float* dst = A.y + (size_t)tok * A.d_out + j;
+      const float val = A.act_scale[tok] * A.w_scale[j] * v;
+      if (atomic)
+        unsafeAtomicAdd(dst, val);
+      else if (A.accumulate)
+        *dst += val;
+      else
+        *dst = val;
+    }
   }
 }
 
