@@ -32,17 +32,22 @@ HBM_PEAK_GBS = 8000.0
 MFMA_F16_PEAK_TFLOPS = 2500.0
 
 
-def gemm_bytes(n, d_in, d_out):
+def gemm_bytes(n, d_in, d_out, k=0, merge=True):
     """Algorithmic HBM bytes of one main-branch launch: weight codes (0.5 B
-    each), activation codes (0.5 B each), both scale vectors, and Y read and
-    written once (the GEMM merges into the compensation term)."""
-    return d_in * d_out // 2 + n * d_in // 2 + 4 * n + 4 * d_out + 8 * n * d_out
+    each), activation codes (0.5 B each), both scale vectors, Y written once
+    (read too when the GEMM merges into a compensation term written before
+    it), and with k > 0 the outlier lists and residuals it compensates from
+    (the weight rows those need are rows the same launch streams anyway)."""
+    y = (8 if merge else 4) * n * d_out
+    return d_in * d_out // 2 + n * d_in // 2 + 4 * n + 4 * d_out + y + 16 * n * k
 
 
-def step_bytes(n, d_in, d_out, k):
-    """Algorithmic HBM bytes of one whole step."""
+def step_bytes(n, d_in, d_out, k, fused):
+    """Algorithmic HBM bytes of one whole step (LUT block ignored: 1 KiB)."""
     quant = 2 * n * d_in + n * d_in // 2 + 4 * n + 16 * n * k       # x in; codes, t, lists out
-    comp = 12 * n * k + 2 * n * k * d_out // 2 + 4 * d_out + 4 * n * d_out
+    if fused:
+        return quant + gemm_bytes(n, d_in, d_out, k, merge=False)
+    comp = 16 * n * k + 2 * n * k * d_out // 2 + 4 * d_out + 4 * n * d_out
     return quant + comp + gemm_bytes(n, d_in, d_out)
 
 
@@ -73,6 +78,8 @@ def main():
     ap.add_argument("--algo", default="mfma", choices=["mfma", "lut"])
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
+    ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate"],
+                    help="fused: one call for Y* + Y' (default for <= 32 tokens)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--verbose", action="store_true")
     args = ap.parse_args()
@@ -110,25 +117,32 @@ def main():
         "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
     }
     y = torch.empty((n, d_out), dtype=torch.float32, device=dev)
-    names = ["build_lut", "quantize_act", "outlier_compensate", "lut_gemm"]
+    fused = args.path == "fused" or (args.path == "auto" and n <= 32 and algo == oasis.ALGO_MFMA)
+    if fused:
+        names = ["build_lut", "quantize_act", "lut_gemm_compensated"]
+    else:
+        names = ["build_lut", "quantize_act", "outlier_compensate", "lut_gemm"]
 
     def step(c, evs=None):
-        if evs is not None:
-            evs[0].record()
+        def mark(i):
+            if evs is not None:
+                evs[i].record()
+        mark(0)
         oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
-        if evs is not None:
-            evs[1].record()
+        mark(1)
         oasis.quantize_act(x, lut, b_a, k, out=q)
-        if evs is not None:
-            evs[2].record()
-        oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut, b_w,
-                                 s_w, d_in, y=y, accumulate=False)
-        if evs is not None:
-            evs[3].record()
-        oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, algo, y=y,
-                       accumulate=True)
-        if evs is not None:
-            evs[4].record()
+        mark(2)
+        if fused:
+            oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w,
+                                       q["max_idx"], q["min_idx"], q["residual"], y=y)
+            mark(3)
+        else:
+            oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut,
+                                     b_w, s_w, d_in, y=y, accumulate=False)
+            mark(3)
+            oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, algo, y=y,
+                           accumulate=True)
+            mark(4)
 
     nsteps = args.steps
 
@@ -178,32 +192,33 @@ def main():
     # ---- per-kernel durations: the same steps launched eagerly behind a spin
     # kernel, so every launch is queued before the GPU reaches it and the HIP
     # events around each kernel see no host gaps.
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(nsteps)]
+    nev = len(names) + 1
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(nsteps)]
     torch.cuda.synchronize()
-    torch.cuda._sleep(int(2.4e9 * (0.002 + nsteps * 60e-6)))   # ~2 ms + 60 us per step
+    torch.cuda._sleep(int(2.4e9 * (0.003 + nsteps * 200e-6)))  # longer than the host needs
     for i in range(nsteps):
         step((args.warmup + i) % copies, events[i])
     torch.cuda.synchronize()
 
     per_kernel = np.array([[events[i][j].elapsed_time(events[i][j + 1])
-                            for j in range(4)] for i in range(nsteps)]) * 1e3   # us
+                            for j in range(len(names))] for i in range(nsteps)]) * 1e3   # us
     kern_us = {nm: float(np.mean(per_kernel[:, j])) for j, nm in enumerate(names)}
     ms_per_step = elapsed * 1e3 / nsteps
     ops = 2.0 * n * d_in * d_out
     value = ops / (ms_per_step * 1e-3) / 1e12
 
-    gemm_us = kern_us["lut_gemm"]
-    gb = gemm_bytes(n, d_in, d_out)
+    gemm_name = names[-1]
+    gemm_us = kern_us[gemm_name]
+    gb = gemm_bytes(n, d_in, d_out, k if fused else 0, merge=not fused)
     achieved = gb / (gemm_us * 1e-6) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": "lut_gemm (k_gemm_mfma_decode)" if algo == oasis.ALGO_MFMA and n <= 32
-                else "lut_gemm", "kernel_us": round(gemm_us, 3), "bytes_per_launch": gb}
+                "kernel": gemm_name, "kernel_us": round(gemm_us, 3), "bytes_per_launch": gb}
     if n > 32:
         tflops = ops / (gemm_us * 1e-6) / 1e12
         roofline = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),
-                    "traffic": None, "kernel": "lut_gemm", "kernel_us": round(gemm_us, 3),
+                    "traffic": None, "kernel": gemm_name, "kernel_us": round(gemm_us, 3),
                     "flops_per_launch": ops}
 
     out = {
@@ -221,8 +236,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "n": n, "d_in": d_in, "d_out": d_out, "k_per_side": k,
                    "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
+                   "path": "fused" if fused else "separate",
                    "weight_copies": copies},
-        "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k) / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),
         "kernel_us": {kk: round(v, 3) for kk, v in kern_us.items()},
         "roofline": roofline,
     }

@@ -163,6 +163,25 @@ int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, con
                              int accumulate, hipStream_t stream);
 
 /*
+ * oasis_lut_gemm_compensated - main branch and outlier branch in one call
+ * (look-ahead computation with error compensation, Sec. III-C):
+ *   y (+)= Y* + Y', with Y* as in oasis_lut_gemm and Y' as in
+ *   oasis_outlier_compensate (same arguments, same layouts).
+ *   For n <= 32 tokens both terms come from one kernel: every workgroup
+ *   adds the compensation of its output columns while it streams the
+ *   weights, so the outlier branch costs no extra pass.  For larger n the
+ *   call runs the MFMA GEMM and then the compensation kernel.
+ *   k == 0 (lists may be NULL) gives Y* alone.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, LAUNCH.
+ */
+int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
+                               const uint32_t* idx_w, const float* w_scale, int d_out,
+                               const oasis_lut_block* lut, int b_a, int b_w,
+                               const int32_t* max_idx, const int32_t* min_idx,
+                               const float* residual, int k, float* y, int accumulate,
+                               hipStream_t stream);
+
+/*
  * oasis_pack_weight_indices - HOST helper: pack w_idx uint8 [d_in][d_out]
  * (codes 0..15, row-major, host memory) into the idx_w layout above
  * (host memory, d_in/8 * d_out words).  Errors: NULL, SHAPE.

@@ -112,7 +112,7 @@ int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_
     return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
   }
   oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
-                    accumulate ? 1 : 0};
+                    accumulate ? 1 : 0, nullptr, nullptr, nullptr, 0};
   return launched(algo == OASIS_ALGO_LUT ? oasis::launch_gemm_lut(a, stream)
                                          : oasis::launch_gemm_mfma(a, stream));
 }
@@ -133,6 +133,41 @@ int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, con
   oasis::CompArgs a{max_idx, min_idx, residual, n, k, idx_w, lut, b_w, w_scale, d_in, d_out, y,
                     accumulate ? 1 : 0};
   return launched(oasis::launch_compensate(a, stream));
+}
+
+int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
+                               const uint32_t* idx_w, const float* w_scale, int d_out,
+                               const oasis_lut_block* lut, int b_a, int b_w,
+                               const int32_t* max_idx, const int32_t* min_idx,
+                               const float* residual, int k, float* y, int accumulate,
+                               hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!act_scale || !w_scale || !lut || !y || (d_in > 0 && (!idx_act || !idx_w)))
+    return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
+  if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
+      !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
+      !aligned(min_idx, 4) || !aligned(residual, 4))
+    return OASIS_ERR_ALIGN;
+  if (d_in == 0) {  // no channels: Y* = Y' = 0
+    if (accumulate) return OASIS_OK;
+    return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
+  }
+  if (n <= oasis::kFusedMaxTokens) {
+    oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
+                      accumulate ? 1 : 0, max_idx, min_idx, residual, k};
+    return launched(oasis::launch_gemm_mfma(a, stream));
+  }
+  // many tokens: main branch into y, then the compensation merged into it
+  oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
+                    accumulate ? 1 : 0, nullptr, nullptr, nullptr, 0};
+  hipError_t e = oasis::launch_gemm_mfma(a, stream);
+  if (e != hipSuccess || k == 0) return launched(e);
+  oasis::CompArgs c{max_idx, min_idx, residual, n, k, idx_w, lut, b_w, w_scale, d_in, d_out, y, 1};
+  return launched(oasis::launch_compensate(c, stream));
 }
 
 int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out) {

@@ -41,6 +41,11 @@ struct GemmArgs {
   int b_a, b_w;
   float* y;
   int accumulate;
+  // optional outlier lists: when k > 0 the GEMM also adds the compensation
+  const int32_t* max_idx;
+  const int32_t* min_idx;
+  const float* residual;
+  int k;
 };
 
 struct CompArgs {
@@ -66,6 +71,8 @@ hipError_t launch_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
 hipError_t launch_gemm_lut(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s);
+// Y (+)= Y* + Y' in one launch when a.n <= kFusedMaxTokens.
+constexpr int kFusedMaxTokens = 32;
 hipError_t launch_compensate(const CompArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* y, size_t count, hipStream_t s);
 

@@ -210,26 +210,100 @@ __device__ __forceinline__ int xcd_tile(int b, int T) {
   return b < 8 * per ? (b & 7) * per + (b >> 3) : b;
 }
 
+// Outlier compensation of one column tile (fused variant).  Every listed
+// outlier (token i, channel p, residual r) reads the words of input channel p
+// for the tile's columns - rows this workgroup has just streamed, so they are
+// L2 hits - and adds r * C_W[code] per column.  Thread t owns token
+// t / T (T = threads per token), four consecutive columns and a slice of the
+// token's entries; the slices' register sums are added through LDS in a fixed
+// order.  Returns nothing: part[i][slice][c] holds the partial sums.
+template <int COLS>
+__device__ __forceinline__ void tile_compensation(const GemmArgs& A, int j0, const float* cwf,
+                                                  float* part, int nslices, int tid,
+                                                  int nthreads, int slots) {
+  constexpr int QUADS = COLS / 4;
+  const int T = nthreads / slots;  // threads per token, a multiple of QUADS
+  const int i = tid / T, u = tid - i * T;
+  const int quad = u % QUADS, slice = u / QUADS;
+  const int k = A.k, E = 2 * k;
+  const int d_out = A.d_out;
+  const int j = j0 + 4 * quad;
+  const bool vec_ok = (d_out & 3) == 0 && j + 3 < d_out;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (i < A.n) {
+    const float* res = A.residual + (size_t)i * E;
+    const int32_t* mx = A.max_idx + (size_t)i * k;
+    const int32_t* mn = A.min_idx + (size_t)i * k;
+    constexpr int B = 8;
+    for (int e0 = slice; e0 < E; e0 += B * nslices) {
+      float r[B];
+      int sh[B];
+      uint32_t w[B][4];
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        const int e = e0 + b * nslices;
+        int p = -1;
+        r[b] = 0.0f;
+        if (e < E) {
+          p = e < k ? mx[e] : mn[e - k];
+          r[b] = res[e];
+        }
+        const bool live = p >= 0 && p < A.d_in && r[b] != 0.0f;
+        if (!live) r[b] = 0.0f;
+        sh[b] = live ? 4 * (p & 7) : 0;
+        w[b][0] = w[b][1] = w[b][2] = w[b][3] = 0u;
+        if (live) {
+          const uint32_t* row = A.idx_w + (size_t)(p >> 3) * d_out + j;
+          if (vec_ok) {
+            const uint4_t v = *reinterpret_cast<const uint4_t*>(row);
+            w[b][0] = v[0]; w[b][1] = v[1]; w[b][2] = v[2]; w[b][3] = v[3];
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              if (j + c < d_out) w[b][c] = row[c];
+          }
+        }
+      }
+#pragma unroll
+      for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] += r[b] * cwf[(w[b][c] >> sh[b]) & 15u];
+    }
+  }
+  if (i < slots) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) part[(i * nslices + slice) * COLS + 4 * quad + c] = acc[c];
+  }
+}
+
 // ----------------------------------------------------------------------------
 // MFMA kernel, few tokens (GEMV-like): one workgroup per 16*CW output
 // columns, its NW waves interleave the K blocks and are summed through LDS,
-// so every output is written once, without atomics.
+// so every output is written once, without atomics.  With outlier lists
+// (A.k > 0) the workgroup also adds the compensation of its columns.
 // ----------------------------------------------------------------------------
 template <int CW, int TF, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
   __shared__ uint32_t tabW[256 * DEC_R];
   __shared__ uint32_t tabA[256 * DEC_R];
+  constexpr int SLOTS = 16 * TF, COLS = 16 * CW;
+  constexpr int NSLICES = (NW * 64 / SLOTS) / (COLS / 4) > 0 ? (NW * 64 / SLOTS) / (COLS / 4) : 1;
+  static_assert((NW * 64 / SLOTS) % (COLS / 4) == 0, "threads per token must cover the columns");
   __shared__ float4_t red[NW][CW * TF][64];
+  __shared__ float part[SLOTS * NSLICES * COLS];
+  __shared__ float cwf[16];
   __shared__ uint16_t cbs[2][16];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
 
   const int j0 = xcd_tile(blockIdx.x, ntiles) * 16 * CW;
   const int nblk = (A.d_in / 8 + 15) / 16;
+  const bool fused = A.k > 0;
 
   // issue the first block's loads, then build the tables while they fly
   BlockCodes<CW, TF> first;
   if (wave < nblk) load_block<CW, TF>(A, wave, j0, 0, first);
-  build_tables(A.lut, cbs, tabW, tabA, tid, NW * 64);
+  if (fused && tid < 16) cwf[tid] = h2f(A.lut->cb_wgt[tid]);
+  build_tables(A.lut, cbs, tabW, tabA, tid, NW * 64);  // barriers: cwf ready
 
   float4_t acc[CW][TF];
 #pragma unroll
@@ -243,6 +317,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) red[wave][c * TF + f][lane] = acc[c][f];
+  // outlier branch, after the main loop so its weight rows are warm in L2
+  if (fused) tile_compensation<COLS>(A, j0, cwf, part, NSLICES, tid, NW * 64, SLOTS);
   __syncthreads();
 
   const int g = lane >> 4, tc = lane & 15;
@@ -251,8 +327,21 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 #pragma unroll
     for (int w = 1; w < NW; ++w) v += red[w][t][lane];
     const int c = t / TF, f = t % TF;
+    const int tok = 16 * f + tc;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) store_out(A, 16 * f + tc, j0 + CW * (4 * g + r) + c, v[r]);
+    for (int r = 0; r < 4; ++r) {
+      const int jl = CW * (4 * g + r) + c;
+      const int j = j0 + jl;
+      if (tok >= A.n || j >= A.d_out) continue;
+      float* dst = A.y + (size_t)tok * A.d_out + j;
+      float val = A.act_scale[tok] * A.w_scale[j] * v[r];
+      if (fused) {
+        float cs = 0.0f;
+        for (int sl = 0; sl < NSLICES; ++sl) cs += part[(tok * NSLICES + sl) * COLS + jl];
+        val += A.w_scale[j] * cs;
+      }
+      *dst = A.accumulate ? *dst + val : val;
+    }
   }
 }
 
@@ -307,16 +396,16 @@ static void launch_gemv(const GemmArgs& a, hipStream_t s) {
 
 template <int TF>
 static void launch_gemv_tf(const GemmArgs& a, hipStream_t s) {
-  // widest column tile that still gives >= 256 workgroups; LDS reduction
-  // buffer NW * CW * TF KiB kept <= 32 KiB
-  if ((a.d_out + 63) / 64 >= 256) {
-    if (TF == 1) launch_gemv<4, TF, 8>(a, s);
-    else launch_gemv<4, TF, 4>(a, s);
-  } else if ((a.d_out + 31) / 32 >= 256) {
-    if (TF == 1) launch_gemv<2, TF, 16>(a, s);
-    else launch_gemv<2, TF, 8>(a, s);
+  // widest column tile that still gives >= 256 workgroups.  LDS: reduction
+  // buffer NW * CW * TF KiB <= 32 KiB; the fused compensation needs the
+  // threads per token (NW * 64 / (16 * TF)) to be a multiple of CW * 4.
+  if constexpr (TF == 1) {
+    if ((a.d_out + 63) / 64 >= 256) launch_gemv<4, 1, 8>(a, s);
+    else if ((a.d_out + 31) / 32 >= 256) launch_gemv<2, 1, 16>(a, s);
+    else launch_gemv<1, 1, 16>(a, s);
   } else {
-    launch_gemv<1, TF, 16>(a, s);
+    if ((a.d_out + 31) / 32 >= 256) launch_gemv<2, TF, 8>(a, s);
+    else launch_gemv<1, TF, 16>(a, s);
   }
 }
 

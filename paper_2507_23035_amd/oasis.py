@@ -22,7 +22,8 @@ ALGO_MFMA = 1
 LUT_BLOCK_BYTES = 256 * 4 + 16 * 2 + 16 * 2
 
 EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quantize_act",
-           "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_pack_weight_indices")
+           "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_lut_gemm_compensated",
+           "oasis_pack_weight_indices")
 
 
 class OasisError(RuntimeError):
@@ -55,6 +56,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_lut_gemm.argtypes = [P, P, I, I, P, P, I, P, I, I, I, P, I, P]
     lib.oasis_outlier_compensate.restype = I
     lib.oasis_outlier_compensate.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
+    lib.oasis_lut_gemm_compensated.restype = I
+    lib.oasis_lut_gemm_compensated.argtypes = [P, P, I, I, P, P, I, P, I, I, P, P, P, I, P, I, P]
     lib.oasis_pack_weight_indices.restype = I
     lib.oasis_pack_weight_indices.argtypes = [P, I, I, P]
     _lib = lib
@@ -158,17 +161,41 @@ def outlier_compensate(max_idx, min_idx, residual, idx_w, lut, b_w: int, w_scale
     return y
 
 
+def lut_gemm_compensated(idx_act, act_scale, idx_w, w_scale, lut, b_a: int, b_w: int, max_idx,
+                         min_idx, residual, y=None, accumulate: bool = False, stream=None):
+    """Main branch plus outlier compensation in one call: y (+)= Y* + Y'."""
+    import torch
+    n = idx_act.shape[0]
+    d_in = idx_act.shape[1] * 2
+    d_out = idx_w.shape[1]
+    k = max_idx.shape[1]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
+    _check("oasis_lut_gemm_compensated", load().oasis_lut_gemm_compensated(
+        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
+        b_a, b_w, _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
+        _ptr(residual) if k else None, k, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+    return y
+
+
 def forward(x, lut, idx_w, w_scale, b_a: int, b_w: int, k: int, scale_mode: int = SCALE_ABSMAX,
-            algo: int = ALGO_MFMA, out: Optional[Dict] = None, y=None, stream=None) -> Dict:
+            algo: int = ALGO_MFMA, out: Optional[Dict] = None, y=None, fused: bool = False,
+            stream=None) -> Dict:
     """Whole hot path of one layer: Y = Y* + Y'.
 
-    The compensation term is written first and the main branch is merged into
-    it, so the split-reduction GEMM needs no separate clearing pass.
+    fused=False: quantize, compensation (y = Y'), then the main branch merged
+    into it (y += Y*).  fused=True: quantize, then one call that produces both
+    terms (matrix-core path only).
     """
     q = quantize_act(x, lut, b_a, k, scale_mode, out=out, stream=stream)
-    y = outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w, w_scale,
-                           x.shape[1], y=y, accumulate=False, stream=stream)
-    lut_gemm(q["idx_act"], q["act_scale"], idx_w, w_scale, lut, b_a, b_w, algo, y=y,
-             accumulate=True, stream=stream)
+    if fused:
+        y = lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w, w_scale, lut, b_a, b_w,
+                                 q["max_idx"], q["min_idx"], q["residual"], y=y,
+                                 accumulate=False, stream=stream)
+    else:
+        y = outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w,
+                               w_scale, x.shape[1], y=y, accumulate=False, stream=stream)
+        lut_gemm(q["idx_act"], q["act_scale"], idx_w, w_scale, lut, b_a, b_w, algo, y=y,
+                 accumulate=True, stream=stream)
     q["y"] = y
     return q

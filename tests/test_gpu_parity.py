@@ -83,6 +83,14 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
         r = oasis.forward(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode, algo)
         torch.cuda.synchronize()
         assert_close(r["y"].cpu().numpy()[rows], ref["y"], f"Y algo={algo}")
+    r = oasis.forward(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode, fused=True)
+    torch.cuda.synchronize()
+    assert_close(r["y"].cpu().numpy()[rows], ref["y"], "Y fused")
+    yf = torch.full_like(r["y"], 0.5)
+    oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w,
+                               q["max_idx"], q["min_idx"], q["residual"], y=yf, accumulate=True)
+    torch.cuda.synchronize()
+    assert_close(yf.cpu().numpy()[rows] - 0.5, ref["y"], "Y fused, accumulate")
     # the other merge order: main branch first, compensation merged into it
     y = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
     oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w, s_w,
