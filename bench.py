@@ -2,14 +2,14 @@
 
 A step is one pass of the whole path over one synthetic layer: build the LUT
 block, quantize the activations (scale, codes, top-k outliers, residuals),
-compensate the outliers, and run the LUT-GEMM merged into the compensation.
+then the LUT-GEMM and the outlier compensation (one fused call for few
+tokens; --path selects the schedule).
 Inputs are resident in HBM when timing starts; the weight codes are rotated
 over enough copies (> 512 MiB in total) that the 256 MiB last-level cache
 cannot serve them.  The timed steps are captured once into one HIP graph and
-replayed (no host launch gaps); per-kernel durations come from HIP events
-around each kernel in a second pass of the same steps, launched eagerly
-behind a spin kernel so that every launch is queued before the GPU gets to
-it.
+replayed (no host launch gaps); per-call durations come from HIP events
+around back-to-back launches of each call, queued behind a spin kernel so
+that every launch is waiting before the GPU gets to it.
 
 Prints ONE JSON line (rank 0).
 """
@@ -78,8 +78,9 @@ def main():
     ap.add_argument("--algo", default="mfma", choices=["mfma", "lut"])
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
-    ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate"],
-                    help="fused: one call for Y* + Y' (default for <= 32 tokens)")
+    ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate", "lookahead"],
+                    help="fused: one call for Y* + Y' (default for <= 32 tokens); lookahead: "
+                         "outlier detection on a second stream beside the main-branch GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--verbose", action="store_true")
     args = ap.parse_args()
@@ -117,32 +118,57 @@ def main():
         "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
     }
     y = torch.empty((n, d_out), dtype=torch.float32, device=dev)
-    fused = args.path == "fused" or (args.path == "auto" and n <= 32 and algo == oasis.ALGO_MFMA)
-    if fused:
+    path = args.path
+    if path == "auto":
+        path = "fused" if (n <= 32 and algo == oasis.ALGO_MFMA) else "separate"
+    side = torch.cuda.Stream()
+
+    # Every call of the path, with the arguments the step uses (c = weight copy).
+    calls = {
+        "build_lut": lambda c: oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut),
+        "quantize_act": lambda c: oasis.quantize_act(x, lut, b_a, k, out=q),
+        "cluster_act": lambda c: oasis.cluster_act(x, lut, b_a, out=q),
+        "detect_outliers": lambda c: oasis.detect_outliers(x, lut, b_a, k, out=q),
+        "outlier_compensate": lambda c: oasis.outlier_compensate(
+            q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut, b_w, s_w, d_in, y=y,
+            accumulate=False),
+        "lut_gemm": lambda c: oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut,
+                                             b_a, b_w, algo, y=y, accumulate=True),
+        "lut_gemm_compensated": lambda c: oasis.lut_gemm_compensated(
+            q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, q["max_idx"],
+            q["min_idx"], q["residual"], y=y),
+    }
+    if path == "fused":
         names = ["build_lut", "quantize_act", "lut_gemm_compensated"]
+        gemm_name = "lut_gemm_compensated"
+    elif path == "lookahead":
+        names = ["build_lut", "cluster_act", "detect_outliers", "lut_gemm", "outlier_compensate"]
+        gemm_name = "lut_gemm"
     else:
         names = ["build_lut", "quantize_act", "outlier_compensate", "lut_gemm"]
+        gemm_name = "lut_gemm"
 
-    def step(c, evs=None):
-        def mark(i):
-            if evs is not None:
-                evs[i].record()
-        mark(0)
-        oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
-        mark(1)
-        oasis.quantize_act(x, lut, b_a, k, out=q)
-        mark(2)
-        if fused:
-            oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w,
-                                       q["max_idx"], q["min_idx"], q["residual"], y=y)
-            mark(3)
-        else:
+    def step(c):
+        main = torch.cuda.current_stream()
+        calls["build_lut"](c)
+        if path == "fused":
+            calls["quantize_act"](c)
+            calls["lut_gemm_compensated"](c)
+        elif path == "lookahead":
+            # main branch and outlier detection run concurrently (Sec. III-C)
+            side.wait_stream(main)
+            with torch.cuda.stream(side):
+                oasis.detect_outliers(x, lut, b_a, k, out=q, stream=side)
+            calls["cluster_act"](c)
+            oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, algo,
+                           y=y, accumulate=False)
+            main.wait_stream(side)
             oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut,
-                                     b_w, s_w, d_in, y=y, accumulate=False)
-            mark(3)
-            oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, algo, y=y,
-                           accumulate=True)
-            mark(4)
+                                     b_w, s_w, d_in, y=y, accumulate=True)
+        else:
+            calls["quantize_act"](c)
+            calls["outlier_compensate"](c)
+            calls["lut_gemm"](c)
 
     nsteps = args.steps
 
@@ -158,17 +184,16 @@ def main():
     for c in range(min(copies, 2)):
         step(c)
     torch.cuda.synchronize()
-    mode = "graph"
-    try:
-        g_warm = capture(args.warmup, 0) if args.warmup else None
-        g_timed = capture(nsteps, args.warmup)
-    except Exception as e:
-        if args.verbose:
-            print(f"graph capture failed ({e}); timing eager launches", file=sys.stderr)
-        mode = "eager"
-        torch.cuda.synchronize()
-    if args.eager:
-        mode = "eager"
+    mode = "eager" if args.eager else "graph"
+    if mode == "graph":
+        try:
+            g_warm = capture(args.warmup, 0) if args.warmup else None
+            g_timed = capture(nsteps, args.warmup)
+        except Exception as e:
+            if args.verbose:
+                print(f"graph capture failed ({e}); timing eager launches", file=sys.stderr)
+            mode = "eager"
+            torch.cuda.synchronize()
 
     # ---- timed region: exactly `nsteps` steps, wall clock, synchronized on both sides
     if mode == "graph":
@@ -189,27 +214,29 @@ def main():
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
 
-    # ---- per-kernel durations: the same steps launched eagerly behind a spin
-    # kernel, so every launch is queued before the GPU reaches it and the HIP
-    # events around each kernel see no host gaps.
-    nev = len(names) + 1
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(nsteps)]
-    torch.cuda.synchronize()
-    torch.cuda._sleep(int(2.4e9 * (0.003 + nsteps * 200e-6)))  # longer than the host needs
-    for i in range(nsteps):
-        step((args.warmup + i) % copies, events[i])
-    torch.cuda.synchronize()
-
-    per_kernel = np.array([[events[i][j].elapsed_time(events[i][j + 1])
-                            for j in range(len(names))] for i in range(nsteps)]) * 1e3   # us
-    kern_us = {nm: float(np.mean(per_kernel[:, j])) for j, nm in enumerate(names)}
+    # ---- per-call durations: `nsteps` back-to-back launches of one call (same
+    # arguments, rotating weight copies) queued behind a spin kernel, so the
+    # GPU never waits for the host; one HIP event pair around the batch on the
+    # stream the calls launch on.
+    kern_us = {}
+    for nm in names:
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(int(2.4e9 * (0.002 + nsteps * 60e-6)))  # longer than the host needs
+        e0.record()
+        for i in range(nsteps):
+            calls[nm]((args.warmup + i) % copies)
+        e1.record()
+        torch.cuda.synchronize()
+        kern_us[nm] = e0.elapsed_time(e1) * 1e3 / nsteps
+    fused = path == "fused"
     ms_per_step = elapsed * 1e3 / nsteps
     ops = 2.0 * n * d_in * d_out
     value = ops / (ms_per_step * 1e-3) / 1e12
 
-    gemm_name = names[-1]
     gemm_us = kern_us[gemm_name]
-    gb = gemm_bytes(n, d_in, d_out, k if fused else 0, merge=not fused)
+    gb = gemm_bytes(n, d_in, d_out, k if fused else 0, merge=path == "separate")
     achieved = gb / (gemm_us * 1e-6) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
@@ -236,7 +263,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "n": n, "d_in": d_in, "d_out": d_out, "k_per_side": k,
                    "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
-                   "path": "fused" if fused else "separate",
+                   "path": path,
                    "weight_copies": copies},
         "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),
         "kernel_us": {kk: round(v, 3) for kk, v in kern_us.items()},

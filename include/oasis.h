@@ -121,6 +121,30 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
                        int32_t* max_idx, int32_t* min_idx, float* residual, hipStream_t stream);
 
 /*
+ * oasis_cluster_act - the main branch's share of oasis_quantize_act: scale
+ * and cluster index of every channel (Sec. III-C1: the whole token is
+ * clustered, outliers included), without outlier detection.  Same arguments
+ * and outputs as oasis_quantize_act restricted to idx_act and act_scale.
+ * With oasis_detect_outliers on a second stream this is the GPU form of the
+ * look-ahead schedule: the main-branch GEMM needs only these outputs, so it
+ * does not wait for outlier detection (Sec. II-C, III-C).
+ * Errors: NULL, SHAPE, BITS, ALIGN, MODE, TOO_LARGE, LAUNCH.
+ */
+int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
+                      int scale_mode, uint8_t* idx_act, float* act_scale, hipStream_t stream);
+
+/*
+ * oasis_detect_outliers - the outlier branch's share of oasis_quantize_act
+ * (Orizuru and the Error Calculation Unit, Sec. IV-A, IV-D): max_idx,
+ * min_idx and residual exactly as oasis_quantize_act writes them (the scale
+ * and the cluster index of each outlier are recomputed from x).  k == 0 is a
+ * no-op.  Errors: NULL, SHAPE, BITS, K, ALIGN, MODE, TOO_LARGE, LAUNCH.
+ */
+int oasis_detect_outliers(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
+                          int k, int scale_mode, int32_t* max_idx, int32_t* min_idx,
+                          float* residual, hipStream_t stream);
+
+/*
  * oasis_lut_gemm - look-ahead WAQ LUT-GEMM, the main branch (Sec. III-B,
  * III-C1): Y*[i][j] = t_i * s_j * sum_p LUT[(a_ip << b_w) | w_pj].
  *   idx_act, act_scale : from oasis_quantize_act (n tokens, d_in channels);

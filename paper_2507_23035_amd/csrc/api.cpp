@@ -94,6 +94,40 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
   return launched(oasis::launch_quantize(a, stream));
 }
 
+int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
+                      int scale_mode, uint8_t* idx_act, float* act_scale, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a)) return OASIS_ERR_BITS;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
+  if (n == 0) return OASIS_OK;
+  if (!x || !lut || !act_scale || (d_in > 0 && !idx_act)) return OASIS_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(lut, 16) || !aligned(idx_act, 16) || !aligned(act_scale, 4))
+    return OASIS_ERR_ALIGN;
+  oasis::QuantArgs a{x, n, d_in, b_a, 0, scale_mode, lut, idx_act, act_scale,
+                     nullptr, nullptr, nullptr};
+  return launched(oasis::launch_cluster(a, stream));
+}
+
+int oasis_detect_outliers(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
+                          int k, int scale_mode, int32_t* max_idx, int32_t* min_idx,
+                          float* residual, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
+  if (oasis::quantize_lds_bytes(d_in, k) > kMaxLds) return OASIS_ERR_TOO_LARGE;
+  if (n == 0 || k == 0) return OASIS_OK;
+  if (!x || !lut || !max_idx || !min_idx || !residual) return OASIS_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(lut, 16) || !aligned(max_idx, 4) || !aligned(min_idx, 4) ||
+      !aligned(residual, 4))
+    return OASIS_ERR_ALIGN;
+  oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, nullptr, nullptr,
+                     max_idx, min_idx, residual};
+  return launched(oasis::launch_outliers(a, stream));
+}
+
 int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
                    const uint32_t* idx_w, const float* w_scale, int d_out,
                    const oasis_lut_block* lut, int b_a, int b_w, int algo, float* y,

@@ -69,6 +69,8 @@ size_t quantize_lds_bytes(int d_in, int k);
 hipError_t launch_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
                             oasis_lut_block* out, hipStream_t s);
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
+hipError_t launch_cluster(const QuantArgs& a, hipStream_t s);   // scale + codes only
+hipError_t launch_outliers(const QuantArgs& a, hipStream_t s);  // lists + residuals only
 hipError_t launch_gemm_lut(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s);
 // Y (+)= Y* + Y' in one launch when a.n <= kFusedMaxTokens.

@@ -11,8 +11,8 @@
 // (-0 folded into +0) shared by the max and min lists: pass 1 histograms the
 // high byte, pass 2 the low byte inside the boundary bucket, which fixes the
 // threshold key T and the count G of keys strictly beyond it.  Keys beyond T
-// (G < k of them) are ranked among themselves with wave ballots; keys equal
-// to T are taken in channel order, which one block-wide scan provides.  The
+// (G < k of them) are ranked among themselves, one lane per candidate; keys
+// equal to T are taken in channel order, which one block-wide scan provides.  The
 // paper's tree pops in exactly this order; the select needs two histogram
 // passes instead of k pops.
 //
@@ -33,7 +33,6 @@ struct QuantSmem {
   uint64_t scan_tmp[NT / 64];
   uint32_t red_tmp[NT / 64];
   uint32_t ctl[8];    // B1/G1 of the max and min lists, then T/G of both
-  uint32_t slots[2];  // candidate counters
 };
 
 // Dynamic LDS after the fixed part: token (2 B per channel, 16-byte padded),
@@ -85,7 +84,8 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* tmp) {
   return r;
 }
 
-template <int NT>
+// CLUSTER: write scale and codes.  TOPK: write outlier lists and residuals.
+template <int NT, bool CLUSTER, bool TOPK>
 __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
 #pragma clang fp contract(off)
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -98,7 +98,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   uint32_t* cand_min = cand_max + k;
   uint32_t* cand_dup = cand_min + k;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x;
   const int i = blockIdx.x;
   const uint16_t* xrow = A.x + (size_t)i * d_in;
   const uint4* xs4 = reinterpret_cast<const uint4*>(xs);
@@ -120,11 +120,10 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   }
   if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
   if (tid < 8) S.ctl[tid] = 0;
-  if (tid < 2) S.slots[tid] = 0;
   amax = block_max<NT>(amax, S.red_tmp);  // barrier: xs, ca, hist visible
 
   const float t = (A.scale_mode == OASIS_SCALE_NONE) ? 1.0f : h2f((uint16_t)amax);
-  if (tid == 0) A.act_scale[i] = t;
+  if (CLUSTER && tid == 0) A.act_scale[i] = t;
 
   // ---- scaled cluster boundaries P_c = fp32(t * b_c), b_c = (c_c + c_{c+1}) * 0.5
   const int nb = (1 << A.b_a) - 1;
@@ -143,7 +142,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
 
   // ---- cluster index of every channel, packed 8 per word (coalesced stores)
   uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
-  for (int v = tid; v < nvec; v += NT) {
+  for (int v = tid; CLUSTER && v < nvec; v += NT) {
     const uint4 q = xs4[v];
     const uint32_t w[4] = {q.x, q.y, q.z, q.w};
     uint32_t packed = 0;
@@ -152,7 +151,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       packed |= cluster(h2f((uint16_t)(w[h >> 1] >> (16 * (h & 1))))) << (4 * h);
     arow[v] = packed;
   }
-  if (k == 0) return;  // uniform across the block
+  if (!TOPK || k == 0) return;  // uniform across the block
 
   // contiguous run of channels owned by this thread, in 8-channel vectors
   const int vpt = (nvec + NT - 1) / NT;
@@ -226,19 +225,24 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   const uint32_t Gmin = min(S.ctl[7], (uint32_t)k - 1u);
   const uint32_t need_max = (uint32_t)k - Gmax, need_min = (uint32_t)k - Gmin;
 
-  // ---- ties in channel order: one scan of (min ties << 32 | max ties)
-  uint64_t ties = 0;
+  // ---- per-thread counts, in channel order, of (max-list ties, min-list ties,
+  // keys above Tmax, keys below Tmin), 16 bits each: one 64-bit block scan
+  // gives every thread its tie ranks and its candidate slots.  (Exclusive
+  // prefixes stay below 2^16 because d_in <= 65536.)
+  uint64_t cnt = 0;
   for (int v = v0; v < v1; ++v) {
     const uint4 q = xs4[v];
     const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
     for (int h = 0; h < 8; ++h) {
       const uint32_t key = ord_key((w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu);
-      ties += (key == Tmax ? 1ull : 0ull) + (key == Tmin ? (1ull << 32) : 0ull);
+      cnt += (uint64_t)(key == Tmax) | ((uint64_t)(key == Tmin) << 16) |
+             ((uint64_t)(key > Tmax) << 32) | ((uint64_t)(key < Tmin) << 48);
     }
   }
-  const uint64_t tie_excl = block_scan64<NT>(ties, S.scan_tmp) - ties;
-  uint32_t rank_max = (uint32_t)tie_excl, rank_min = (uint32_t)(tie_excl >> 32);
+  const uint64_t excl = block_scan64<NT>(cnt, S.scan_tmp) - cnt;
+  uint32_t rank_max = (uint32_t)(excl & 0xFFFFu), rank_min = (uint32_t)((excl >> 16) & 0xFFFFu);
+  uint32_t slot_max = (uint32_t)((excl >> 32) & 0xFFFFu), slot_min = (uint32_t)(excl >> 48);
 
   const size_t krow = (size_t)i * k;
   const size_t rrow = (size_t)i * 2 * k;
@@ -247,7 +251,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     return x - xhat;
   };
 
-  // ---- collect: direct output for threshold ties, candidates for the rest
+  // ---- collect: direct output for threshold ties, candidate slots for the rest
   for (int v = v0; v < v1; ++v) {
     const uint4 q = xs4[v];
     const uint32_t w[4] = {q.x, q.y, q.z, q.w};
@@ -266,8 +270,8 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
         }
         ++rank_max;
       } else if (in_max) {
-        const uint32_t slot = atomicAdd(&S.slots[0], 1u);
-        if (slot < Gmax) cand_max[slot] = (key << 16) | (0xFFFFu - (uint32_t)p);
+        if (slot_max < Gmax) cand_max[slot_max] = (key << 16) | (0xFFFFu - (uint32_t)p);
+        ++slot_max;
       }
       if (key == Tmin) {
         if (rank_min < need_min) {
@@ -277,62 +281,64 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
         }
         ++rank_min;
       } else if (key < Tmin) {
-        const uint32_t slot = atomicAdd(&S.slots[1], 1u);
-        if (slot < Gmin) {
-          cand_min[slot] = (key << 16) | (uint32_t)p;
-          cand_dup[slot] = in_max ? 1u : 0u;
+        if (slot_min < Gmin) {
+          cand_min[slot_min] = (key << 16) | (uint32_t)p;
+          cand_dup[slot_min] = in_max ? 1u : 0u;
         }
+        ++slot_min;
       }
     }
   }
   __syncthreads();
 
-  // ---- rank the candidates: one wave per candidate, ballot counts
-  constexpr int NW = NT / 64;
-  for (uint32_t c = wave; c < Gmax; c += NW) {
-    const uint32_t key = cand_max[c];
-    uint32_t rank = 0;
-    for (uint32_t q0 = 0; q0 < Gmax; q0 += 64) {
-      const uint32_t q = q0 + lane;
-      rank += __popcll(__ballot(q < Gmax && cand_max[q] > key));
-    }
-    if (lane == 0) {
+  // ---- rank the candidates: one lane per candidate, counting the
+  // candidates that pop before it (broadcast LDS reads, no serial chain)
+  for (uint32_t c = tid; c < Gmax + Gmin; c += NT) {
+    if (c < Gmax) {
+      const uint32_t key = cand_max[c];
+      uint32_t rank = 0;
+#pragma unroll 4
+      for (uint32_t q = 0; q < Gmax; ++q) rank += cand_max[q] > key ? 1u : 0u;
       const int p = (int)(0xFFFFu - (key & 0xFFFFu));
       A.max_idx[krow + rank] = p;
       A.residual[rrow + rank] = residual_of(h2f(xs[p]));
-    }
-  }
-  for (uint32_t c = wave; c < Gmin; c += NW) {
-    const uint32_t key = cand_min[c];
-    uint32_t rank = 0;
-    for (uint32_t q0 = 0; q0 < Gmin; q0 += 64) {
-      const uint32_t q = q0 + lane;
-      rank += __popcll(__ballot(q < Gmin && cand_min[q] < key));
-    }
-    if (lane == 0) {
+    } else {
+      const uint32_t cm = c - Gmax;
+      const uint32_t key = cand_min[cm];
+      uint32_t rank = 0;
+#pragma unroll 4
+      for (uint32_t q = 0; q < Gmin; ++q) rank += cand_min[q] < key ? 1u : 0u;
       const int p = (int)(key & 0xFFFFu);
       A.min_idx[krow + rank] = p;
-      A.residual[rrow + k + rank] = cand_dup[c] ? 0.0f : residual_of(h2f(xs[p]));
+      A.residual[rrow + k + rank] = cand_dup[cm] ? 0.0f : residual_of(h2f(xs[p]));
     }
   }
 }
 
-template <int NT>
+template <int NT, bool CL, bool TK>
 static hipError_t launch_nt(const QuantArgs& a, hipStream_t s) {
-  const size_t lds = sizeof(QuantSmem<NT>) + dyn_bytes(a.d_in, a.k);
+  const size_t lds = sizeof(QuantSmem<NT>) + dyn_bytes(a.d_in, TK ? a.k : 0);
   if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_quantize<NT>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_quantize<NT, CL, TK>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_quantize<NT>, dim3(a.n), dim3(NT), lds, s, a);
+  hipLaunchKernelGGL((k_quantize<NT, CL, TK>), dim3(a.n), dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_quantize(const QuantArgs& a, hipStream_t s) {
+template <bool CL, bool TK>
+static hipError_t launch_parts(const QuantArgs& a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   // few tokens: wide workgroups keep each token's serial phases short
-  return a.n <= 64 ? launch_nt<1024>(a, s) : launch_nt<256>(a, s);
+  return a.n <= 64 ? launch_nt<1024, CL, TK>(a, s) : launch_nt<256, CL, TK>(a, s);
+}
+
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t s) { return launch_parts<true, true>(a, s); }
+hipError_t launch_cluster(const QuantArgs& a, hipStream_t s) { return launch_parts<true, false>(a, s); }
+hipError_t launch_outliers(const QuantArgs& a, hipStream_t s) {
+  if (a.k == 0) return hipSuccess;
+  return launch_parts<false, true>(a, s);
 }
 
 }  // namespace oasis

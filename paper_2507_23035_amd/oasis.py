@@ -22,6 +22,7 @@ ALGO_MFMA = 1
 LUT_BLOCK_BYTES = 256 * 4 + 16 * 2 + 16 * 2
 
 EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quantize_act",
+           "oasis_cluster_act", "oasis_detect_outliers",
            "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_lut_gemm_compensated",
            "oasis_pack_weight_indices")
 
@@ -52,6 +53,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_build_lut.argtypes = [P, I, P, I, P, P]
     lib.oasis_quantize_act.restype = I
     lib.oasis_quantize_act.argtypes = [P, I, I, P, I, I, I, P, P, P, P, P, P]
+    lib.oasis_cluster_act.restype = I
+    lib.oasis_cluster_act.argtypes = [P, I, I, P, I, I, P, P, P]
+    lib.oasis_detect_outliers.restype = I
+    lib.oasis_detect_outliers.argtypes = [P, I, I, P, I, I, I, P, P, P, P]
     lib.oasis_lut_gemm.restype = I
     lib.oasis_lut_gemm.argtypes = [P, P, I, I, P, P, I, P, I, I, I, P, I, P]
     lib.oasis_outlier_compensate.restype = I
@@ -131,6 +136,36 @@ def quantize_act(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
     return out
 
 
+def cluster_act(x, lut, b_a: int, scale_mode: int = SCALE_ABSMAX, out: Optional[Dict] = None,
+                stream=None) -> Dict:
+    """Scale and activation codes only (the main branch's inputs)."""
+    import torch
+    n, d_in = x.shape
+    if out is None:
+        out = {"idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=x.device),
+               "act_scale": torch.empty(n, dtype=torch.float32, device=x.device)}
+    _check("oasis_cluster_act", load().oasis_cluster_act(
+        _ptr(x), n, d_in, _ptr(lut), b_a, scale_mode, _ptr(out["idx_act"]),
+        _ptr(out["act_scale"]), _stream(stream)))
+    return out
+
+
+def detect_outliers(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
+                    out: Optional[Dict] = None, stream=None) -> Dict:
+    """Outlier lists and residuals only (the outlier branch's inputs)."""
+    import torch
+    n, d_in = x.shape
+    if out is None:
+        out = {"max_idx": torch.empty((n, k), dtype=torch.int32, device=x.device),
+               "min_idx": torch.empty((n, k), dtype=torch.int32, device=x.device),
+               "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=x.device)}
+    _check("oasis_detect_outliers", load().oasis_detect_outliers(
+        _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode,
+        _ptr(out["max_idx"]) if k else None, _ptr(out["min_idx"]) if k else None,
+        _ptr(out["residual"]) if k else None, _stream(stream)))
+    return out
+
+
 def lut_gemm(idx_act, act_scale, idx_w, w_scale, lut, b_a: int, b_w: int, algo: int = ALGO_MFMA,
              y=None, accumulate: bool = False, stream=None):
     """Main branch Y* (y = Y*, or y += Y* with accumulate)."""
@@ -199,3 +234,45 @@ def forward(x, lut, idx_w, w_scale, b_a: int, b_w: int, k: int, scale_mode: int 
                  accumulate=True, stream=stream)
     q["y"] = y
     return q
+
+
+_side_streams: Dict = {}
+
+
+def forward_lookahead(x, lut, idx_w, w_scale, b_a: int, b_w: int, k: int,
+                      scale_mode: int = SCALE_ABSMAX, algo: int = ALGO_MFMA,
+                      out: Optional[Dict] = None, y=None, side_stream=None) -> Dict:
+    """Whole hot path with the look-ahead schedule of Sec. III-C on two streams.
+
+    Main stream: cluster the whole token, then the LUT-GEMM (y = Y*).  Side
+    stream, concurrently: outlier detection and residuals.  The main stream
+    then waits for the side stream and merges the compensation (y += Y').
+    """
+    import torch
+    main = torch.cuda.current_stream()
+    if side_stream is None:
+        side_stream = _side_streams.setdefault(main.device, torch.cuda.Stream(device=main.device))
+    n, d_in = x.shape
+    if out is None:
+        out = {
+            "idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=x.device),
+            "act_scale": torch.empty(n, dtype=torch.float32, device=x.device),
+            "max_idx": torch.empty((n, k), dtype=torch.int32, device=x.device),
+            "min_idx": torch.empty((n, k), dtype=torch.int32, device=x.device),
+            "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=x.device),
+        }
+    side_stream.wait_stream(main)                      # x and lut are ready
+    with torch.cuda.stream(side_stream):
+        detect_outliers(x, lut, b_a, k, scale_mode, out=out, stream=side_stream)
+    cluster_act(x, lut, b_a, scale_mode, out=out, stream=main)
+    y = lut_gemm(out["idx_act"], out["act_scale"], idx_w, w_scale, lut, b_a, b_w, algo, y=y,
+                 accumulate=False, stream=main)
+    main.wait_stream(side_stream)                      # outlier branch done
+    for key in ("max_idx", "min_idx", "residual"):
+        out[key].record_stream(side_stream)
+    x.record_stream(side_stream)
+    outlier_compensate(out["max_idx"], out["min_idx"], out["residual"], idx_w, lut, b_w, w_scale,
+                       d_in, y=y, accumulate=True, stream=main)
+    out["y"] = y
+    return out
+

@@ -96,6 +96,28 @@ def test_quantize_errors(lib):
     assert q(P, 0, 16, None, 4, 1, 0, None, None, None, None, None, None) == 0   # empty
 
 
+def test_cluster_and_detect_errors(lib):
+    c = lib.oasis_cluster_act
+    assert c(P, 4, 12, P, 4, 0, P, P, None) == -2
+    assert c(P, 4, 16, P, 5, 0, P, P, None) == -3
+    assert c(P, 4, 16, P, 4, 3, P, P, None) == -7
+    assert c(None, 4, 16, P, 4, 0, P, P, None) == -1
+    assert c(P, 4, 16, P, 4, 0, MIS, P, None) == -6
+    d = lib.oasis_detect_outliers
+    assert d(P, 4, 16, P, 4, 17, 0, P, P, P, None) == -4
+    assert d(P, 4, 16, P, 4, 2, 0, None, P, P, None) == -1
+    assert d(P, 4, 16, P, 4, 0, 0, None, None, None, None) == 0   # k = 0: nothing to do
+    assert d(P, 4, 65544, P, 4, 1, 0, P, P, P, None) == -9
+
+
+def test_fused_gemm_errors(lib):
+    f = lib.oasis_lut_gemm_compensated
+    assert f(P, P, 4, 20, P, P, 8, P, 4, 4, P, P, P, 1, P, 0, None) == -2
+    assert f(P, P, 4, 16, P, P, 8, P, 4, 4, P, P, P, 17, P, 0, None) == -4
+    assert f(P, P, 4, 16, P, P, 8, P, 4, 4, None, P, P, 1, P, 0, None) == -1
+    assert f(P, P, 4, 16, P, P, 8, P, 4, 4, P, P, MIS, 1, P, 0, None) == -6
+
+
 def test_gemm_errors(lib):
     g = lib.oasis_lut_gemm
     assert g(P, P, 4, 20, P, P, 8, P, 4, 4, 1, P, 0, None) == -2

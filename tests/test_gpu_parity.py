@@ -91,6 +91,13 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
                                q["max_idx"], q["min_idx"], q["residual"], y=yf, accumulate=True)
     torch.cuda.synchronize()
     assert_close(yf.cpu().numpy()[rows] - 0.5, ref["y"], "Y fused, accumulate")
+    c = oasis.cluster_act(x, lut, b_a, scale_mode)
+    d = oasis.detect_outliers(x, lut, b_a, k, scale_mode)
+    check_quant({**c, **d}, ref, k)
+    r = oasis.forward_lookahead(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode)
+    torch.cuda.synchronize()
+    check_quant(r, ref, k)
+    assert_close(r["y"].cpu().numpy()[rows], ref["y"], "Y look-ahead")
     # the other merge order: main branch first, compensation merged into it
     y = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
     oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w, s_w,
