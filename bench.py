@@ -51,6 +51,131 @@ def step_bytes(n, d_in, d_out, k, fused):
     return quant + comp + gemm_bytes(n, d_in, d_out)
 
 
+def call_bytes(n, d_in, d_out, k, path):
+    """Algorithmic HBM bytes per launch of every call of the path."""
+    x, codes = 2 * n * d_in, n * d_in // 2
+    lists = 16 * n * k                       # two int32 lists + 2k fp32 residuals
+    # outlier branch: one input channel of the index matrix (d_out/2 bytes) per
+    # listed outlier, the lists, the scales, y written (read too if merging)
+    comp_y = (8 if path == "lookahead" else 4) * n * d_out
+    comp = 2 * n * k * d_out // 2 + lists + 4 * d_out + comp_y
+    return {
+        "build_lut": 2 * 32 + 1088,
+        "quantize_act": x + codes + 4 * n + lists,
+        "cluster_act": x + codes + 4 * n,
+        "detect_outliers": x + lists,
+        "outlier_compensate": comp,
+        "lut_gemm": gemm_bytes(n, d_in, d_out, merge=path == "separate"),
+        "lut_gemm_compensated": gemm_bytes(n, d_in, d_out, k, merge=False),
+    }
+
+
+KERNEL_SOURCES = {
+    "build_lut": ["lut.hip"],
+    "quantize_act": ["quantize.hip"], "cluster_act": ["quantize.hip"],
+    "detect_outliers": ["quantize.hip"],
+    "outlier_compensate": ["compensate.hip"],
+    "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
+}
+
+
+def source_digest(call):
+    """sha256 of the HIP sources a call's kernels are built from (+ common.h)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[call] + ["common.h"]:
+        with open(os.path.join(ROOT, "paper_2507_23035_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(call, workload):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary, scaled by the copy-kernel calibration; None if there is none or
+    the kernel source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(f"{call}|{workload}")
+    if not rec or rec.get("source_sha256") != source_digest(call):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+CALL_SYMBOLS = {   # kernel symbol fragment of each call's dominant kernel
+    "build_lut": "k_build_lut", "quantize_act": "k_quantize<", "cluster_act": "k_quantize<",
+    "detect_outliers": "k_quantize<", "outlier_compensate": "k_compensate",
+    "lut_gemm": "k_gemm_mfma", "lut_gemm_compensated": "k_gemm_mfma",
+}
+
+
+def _pmc_rows(d, counter):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        rows += [r for r in csv.DictReader(open(f)) if r.get("Counter_Name") == counter]
+    return rows
+
+
+def summarize_pmc(root, workload, path):
+    """Turn four rocprofv3 --pmc runs (subdirectories fetch/, write/ of the
+    bench, cal_fetch/, cal_write/ of --calibrate-copy) into per-launch HBM
+    bytes for every call of the path, written to profiles/traffic.json."""
+    cal = {}
+    for c, sub in (("FETCH_SIZE", "cal_fetch"), ("WRITE_SIZE", "cal_write")):
+        vals = [float(r["Counter_Value"]) for r in _pmc_rows(os.path.join(root, sub), c)]
+        cal[c] = max(vals) / float(256 << 20)      # counter units per byte (copy of 256 MiB)
+    out_path = os.path.join(ROOT, "profiles", "traffic.json")
+    db = json.load(open(out_path)) if os.path.exists(out_path) else {}
+    lines = [f"| call | kernel | dispatches | FETCH_SIZE | WRITE_SIZE | HBM bytes/launch |",
+             "|---|---|---|---|---|---|"]
+    names = {"fused": ["quantize_act", "lut_gemm_compensated"],
+             "separate": ["quantize_act", "outlier_compensate", "lut_gemm"],
+             "lookahead": ["cluster_act", "detect_outliers", "lut_gemm",
+                           "outlier_compensate"]}[path]
+    for call in names:
+        sym = CALL_SYMBOLS[call]
+        vals = {}
+        for c, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+            rs = [r for r in _pmc_rows(os.path.join(root, sub), c) if sym in r["Kernel_Name"]]
+            if call in ("cluster_act", "detect_outliers", "quantize_act"):
+                want = {"cluster_act": "true, false", "detect_outliers": "false, true",
+                        "quantize_act": "true, true"}[call]
+                rs = [r for r in rs if want in r["Kernel_Name"]]
+            vals[c] = (len(rs), sum(float(r["Counter_Value"]) for r in rs) / max(1, len(rs)))
+        if not vals["FETCH_SIZE"][0]:
+            continue
+        hbm = vals["FETCH_SIZE"][1] / cal["FETCH_SIZE"] + vals["WRITE_SIZE"][1] / cal["WRITE_SIZE"]
+        db[f"{call}|{workload}"] = {"source_sha256": source_digest(call),
+                                    "fetch_counter": vals["FETCH_SIZE"][1],
+                                    "write_counter": vals["WRITE_SIZE"][1],
+                                    "copy_factor_fetch": cal["FETCH_SIZE"],
+                                    "copy_factor_write": cal["WRITE_SIZE"],
+                                    "hbm_bytes_per_launch": round(hbm)}
+        lines.append(f"| {call} | {sym} | {vals['FETCH_SIZE'][0]} | {vals['FETCH_SIZE'][1]:.1f} "
+                     f"| {vals['WRITE_SIZE'][1]:.1f} | {hbm:.0f} |")
+    with open(out_path, "w") as fh:
+        json.dump(db, fh, indent=1, sort_keys=True)
+    print(f"copy calibration: FETCH_SIZE {cal['FETCH_SIZE']:.6g} and WRITE_SIZE "
+          f"{cal['WRITE_SIZE']:.6g} counter units per byte")
+    print("\n".join(lines))
+
+
+def calibrate_copy(mib):
+    """A plain device copy of known size (the counter calibration run)."""
+    import torch
+    nbytes = mib << 20
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "copy", "bytes_read_per_copy": nbytes,
+                      "bytes_written_per_copy": nbytes, "copies": 10}), flush=True)
+
+
 def cpu_baseline(layer, budget_s=12.0):
     """Time the oracle's whole-layer forward on the host (single-threaded numpy)."""
     from oracle import oasis_oracle as O
@@ -83,7 +208,15 @@ def main():
                          "outlier detection on a second stream beside the main-branch GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--verbose", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--summarize-pmc", default="", metavar="DIR",
+                    help="only summarize rocprofv3 --pmc runs under DIR into profiles/")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc, args.config,
+                      "fused" if args.path == "auto" else args.path)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
@@ -95,6 +228,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU", file=sys.stderr)
         sys.exit(1)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     oasis.load()
     dev = torch.device("cuda:0")
     layer = synth.make_layer(synth.config(args.config))
@@ -235,18 +371,28 @@ def main():
     ops = 2.0 * n * d_in * d_out
     value = ops / (ms_per_step * 1e-3) / 1e12
 
-    gemm_us = kern_us[gemm_name]
-    gb = gemm_bytes(n, d_in, d_out, k if fused else 0, merge=path == "separate")
-    achieved = gb / (gemm_us * 1e-6) / 1e9
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": gemm_name, "kernel_us": round(gemm_us, 3), "bytes_per_launch": gb}
-    if n > 32:
-        tflops = ops / (gemm_us * 1e-6) / 1e12
-        roofline = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),
-                    "traffic": None, "kernel": gemm_name, "kernel_us": round(gemm_us, 3),
-                    "flops_per_launch": ops}
+    # ---- roofline of the dominant call (largest share of the step)
+    kbytes = call_bytes(n, d_in, d_out, k, path)
+    dom = max(names, key=lambda nm: kern_us[nm])
+
+    def roof(nm):
+        us = kern_us[nm]
+        if nm in ("lut_gemm", "lut_gemm_compensated") and n > 32:
+            tflops = ops / (us * 1e-6) / 1e12
+            r = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
+                 "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),
+                 "flops_per_launch": ops}
+        else:
+            gbs = kbytes[nm] / (us * 1e-6) / 1e9
+            r = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                 "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_per_launch": kbytes[nm]}
+        r["traffic"] = measured_traffic(nm, s.name)
+        r["kernel"] = nm
+        r["kernel_us"] = round(us, 3)
+        return r
+
+    roofline = roof(dom)
+    main_branch = roof(gemm_name)
 
     out = {
         "metric": METRIC,
@@ -268,6 +414,7 @@ def main():
         "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),
         "kernel_us": {kk: round(v, 3) for kk, v in kern_us.items()},
         "roofline": roofline,
+        "roofline_main_branch": main_branch,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layer)
