@@ -161,9 +161,10 @@ int oasis_detect_outliers(const uint16_t* x, int n, int d_in, const oasis_lut_bl
  *   y         : DEVICE fp32 [n][d_out], 4-byte aligned.
  *   accumulate != 0 : y += Y*  (merge into a compensation term written first);
  *   accumulate == 0 : y  = Y*.
- *   Partial sums over input-channel slices may be merged with fp32 atomics,
- *   so the summation order (not the set of products) can vary run to run.
- * Errors: NULL, SHAPE, BITS, ALIGN, MODE, LAUNCH.
+ *   The literal-LUT kernel may merge partial sums over input-channel slices
+ *   with fp32 atomics, so its summation order can vary run to run.
+ *   The weight codes and the activation codes must each be < 2 GiB.
+ * Errors: NULL, SHAPE, BITS, ALIGN, MODE, TOO_LARGE, LAUNCH.
  */
 int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
                    const uint32_t* idx_w, const float* w_scale, int d_out,
@@ -196,7 +197,7 @@ int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, con
  *   weights, so the outlier branch costs no extra pass.  For larger n the
  *   call runs the MFMA GEMM and then the compensation kernel.
  *   k == 0 (lists may be NULL) gives Y* alone.
- * Errors: NULL, SHAPE, BITS, K, ALIGN, LAUNCH.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, TOO_LARGE, LAUNCH.
  */
 int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
                                const uint32_t* idx_w, const float* w_scale, int d_out,

@@ -141,6 +141,8 @@ int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_
   if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
       !aligned(act_scale, 4) || !aligned(w_scale, 4))
     return OASIS_ERR_ALIGN;
+  if ((size_t)(d_in / 8) * d_out * 4 >= (1ull << 31) || (size_t)n * d_in / 2 >= (1ull << 31))
+    return OASIS_ERR_TOO_LARGE;  // 32-bit buffer offsets
   if (d_in == 0) {  // empty reduction: Y* = 0
     if (accumulate) return OASIS_OK;
     return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
@@ -186,6 +188,8 @@ int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, i
       !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
       !aligned(min_idx, 4) || !aligned(residual, 4))
     return OASIS_ERR_ALIGN;
+  if ((size_t)(d_in / 8) * d_out * 4 >= (1ull << 31) || (size_t)n * d_in / 2 >= (1ull << 31))
+    return OASIS_ERR_TOO_LARGE;  // 32-bit buffer offsets
   if (d_in == 0) {  // no channels: Y* = Y' = 0
     if (accumulate) return OASIS_OK;
     return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));

@@ -29,52 +29,55 @@ namespace oasis {
 // ----------------------------------------------------------------------------
 // shared helpers
 // ----------------------------------------------------------------------------
-constexpr int DEC_R = 8;  // replication of the byte -> fp16 pair tables
+constexpr int DEC_R = 8;   // replication of the byte -> fp16 pair tables
+constexpr int WIDE_R = 64;  // one copy per lane: lane l always reads bank l
 
-// byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes.
-// `cb` is the 16-entry codebook already staged in LDS.
+// byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes,
+// replicated R times (entry b * R + r).  `cb` is the codebook staged in LDS.
+template <int R>
 __device__ __forceinline__ void build_pair_table(uint32_t* tab, const uint16_t* cb, int tid,
                                                  int nthreads) {
-  for (int e = tid; e < 256 * DEC_R; e += nthreads) {
-    const int b = e / DEC_R;
+  for (int e = tid; e < 256 * R; e += nthreads) {
+    const int b = e / R;
     tab[e] = (uint32_t)cb[b & 15] | ((uint32_t)cb[b >> 4] << 16);
   }
 }
 
 // Stage both codebooks of the LUT block in LDS, then build both pair tables.
+template <int RW, int RA>
 __device__ __forceinline__ void build_tables(const oasis_lut_block* lut, uint16_t (&cbs)[2][16],
                                              uint32_t* tabW, uint32_t* tabA, int tid,
                                              int nthreads) {
   if (tid < 16) cbs[0][tid] = lut->cb_wgt[tid];
   else if (tid < 32) cbs[1][tid - 16] = lut->cb_act[tid - 16];
   __syncthreads();
-  build_pair_table(tabW, cbs[0], tid, nthreads);
-  build_pair_table(tabA, cbs[1], tid, nthreads);
+  build_pair_table<RW>(tabW, cbs[0], tid, nthreads);
+  build_pair_table<RA>(tabA, cbs[1], tid, nthreads);
   __syncthreads();
 }
 
-__device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, int lane_off) {
+// Eight codes -> eight fp16 centroid values (channel order kept: VGPR v holds
+// the two channels of byte v).  R == WIDE_R: the byte offset of entry
+// (byte, lane) is byte * 256 + lane * 4, assembled by one v_perm_b32 from the
+// code word and the lane's offset (bank = lane, no conflicts).  Otherwise
+// entry byte * R + (lane mod R).
+template <int R>
+__device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, uint32_t lane) {
   uint4_t r;
-  r[0] = tab[((w >> 0) & 0xFFu) * DEC_R + lane_off];
-  r[1] = tab[((w >> 8) & 0xFFu) * DEC_R + lane_off];
-  r[2] = tab[((w >> 16) & 0xFFu) * DEC_R + lane_off];
-  r[3] = tab[((w >> 24) & 0xFFu) * DEC_R + lane_off];
-  return __builtin_bit_cast(half8_t, r);
-}
-
-__device__ __forceinline__ uint4_t load_w4(const uint32_t* __restrict__ idx_w, size_t row_off,
-                                           int j, int d_out, bool vec_ok) {
-  uint4_t v = {0u, 0u, 0u, 0u};
-  const uint32_t* p = idx_w + row_off + j;
-  if (vec_ok && j + 3 < d_out) {
-    v = *reinterpret_cast<const uint4_t*>(p);
+  if constexpr (R == WIDE_R) {
+    const char* base = reinterpret_cast<const char*>(tab);
+    const uint32_t lane4 = lane * 4u;  // < 256: fits the low byte
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
+      r[b] = *reinterpret_cast<const uint32_t*>(base + off);
+    }
   } else {
-    if (j + 0 < d_out) v[0] = p[0];
-    if (j + 1 < d_out) v[1] = p[1];
-    if (j + 2 < d_out) v[2] = p[2];
-    if (j + 3 < d_out) v[3] = p[3];
+    const uint32_t lo = lane & (R - 1);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) r[b] = tab[((w >> (8 * b)) & 0xFFu) * R + lo];
   }
-  return v;
+  return __builtin_bit_cast(half8_t, r);
 }
 
 // Raw codes of one block of 16 words for one wave: the activation words of
@@ -140,15 +143,72 @@ __device__ __forceinline__ void load_block(const GemmArgs& A, int blk, int j0, i
   }
 }
 
+// Buffer-load form of load_block for the GEMV kernel.  Per-lane byte offsets
+// are computed once; the block's offset travels in an SGPR.  The buffer
+// descriptors carry the tensors' sizes, so a read past the end returns 0
+// instead of faulting: columns past d_out or tokens past n only feed outputs
+// that are never stored, and the words of a last, partial K block are masked
+// in mma_block.
+struct GemvAddr {
+  __amdgpu_buffer_rsrc_t rw, ra;
+  uint32_t woff[4];  // byte offset of (row 4g + s, column j0 + CW*m) in block 0
+  uint32_t aoff;     // byte offset of (token m, word 4g) in block 0
+  uint32_t wblk;     // bytes per block of 16 weight rows
+  uint32_t astride;  // bytes between token tiles (16 tokens)
+};
+
+template <int CW>
+__device__ __forceinline__ GemvAddr gemv_addr(const GemmArgs& A, int j0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, m = lane & 15;
+  const uint32_t KB = (uint32_t)(A.d_in >> 3);
+  GemvAddr ad;
+  ad.rw = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(A.idx_w), 0,
+                                            (int)(KB * (uint32_t)A.d_out * 4u), 0x00020000);
+  ad.ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(A.idx_act), 0,
+                                            (int)((uint32_t)A.n * KB * 4u), 0x00020000);
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    ad.woff[s] = ((uint32_t)(4 * g + s) * (uint32_t)A.d_out + (uint32_t)(j0 + CW * m)) * 4u;
+  ad.aoff = ((uint32_t)m * KB + 4u * g) * 4u;
+  ad.wblk = 16u * (uint32_t)A.d_out * 4u;
+  ad.astride = 16u * KB * 4u;
+  return ad;
+}
+
+template <int CW, int TF>
+__device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
+                                               BlockCodes<CW, TF>& bc) {
+  const int sw = (int)((uint32_t)blk * ad.wblk);
+  const int sa = blk * 64;
+#pragma unroll
+  for (int f = 0; f < TF; ++f)
+    bc.av[f] = __builtin_bit_cast(
+        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.ra, (int)(ad.aoff + f * ad.astride), sa, 0));
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if constexpr (CW == 4) {
+      const uint4_t v = __builtin_bit_cast(
+          uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)ad.woff[s], sw, 0));
+      bc.wv[s][0] = v[0]; bc.wv[s][1] = v[1]; bc.wv[s][2] = v[2]; bc.wv[s][3] = v[3];
+    } else if constexpr (CW == 2) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(ad.rw, (int)ad.woff[s], sw, 0);
+      bc.wv[s][0] = v[0]; bc.wv[s][CW - 1] = v[1];
+    } else {
+      bc.wv[s][0] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)ad.woff[s], sw, 0);
+    }
+  }
+}
+
 // Expand the codes of one block to fp16 centroid values and run its MFMAs:
 // CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
-template <int CW, int TF>
+// MASK: zero the activation operand of words past d_in and of tokens past n
+// (needed when those words hold codes that are not 0 contributions).
+template <int CW, int TF, int RW, bool MASK = true>
 __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
                                           const BlockCodes<CW, TF>& bc, const uint32_t* tabW,
                                           const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, m = lane & 15;
-  const int lane_off = lane & (DEC_R - 1);
   const int KB = A.d_in >> 3;
   const int kw0 = blk * 16 + 4 * g;
 #pragma unroll
@@ -157,13 +217,15 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
     half8_t bf[TF];
 #pragma unroll
     for (int f = 0; f < TF; ++f) {
-      bf[f] = expand_word(bc.av[f][s], tabA, lane_off);
-      const bool tok_ok = (tok0 + 16 * f + m) < A.n;
-      if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      bf[f] = expand_word<DEC_R>(bc.av[f][s], tabA, lane);
+      if constexpr (MASK) {
+        const bool tok_ok = (tok0 + 16 * f + m) < A.n;
+        if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      }
     }
 #pragma unroll
     for (int c = 0; c < CW; ++c) {
-      const half8_t af = expand_word(bc.wv[s][c], tabW, lane_off);
+      const half8_t af = expand_word<RW>(bc.wv[s][c], tabW, lane);
 #pragma unroll
       for (int f = 0; f < TF; ++f)
         acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[f], acc[c][f], 0, 0, 0);
@@ -171,22 +233,69 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
   }
 }
 
-// Blocks blk_begin, blk_begin + stride, ... < blk_end of one wave, the next
-// block's codes loaded while the current one is expanded and multiplied.
-// `first` holds the codes of blk_begin (loaded by the caller before the
-// decode tables were built).
-template <int CW, int TF>
+// Blocks blk_begin, blk_begin + stride, ... < blk_end of one wave with PF
+// blocks' codes in flight: after a block is expanded and multiplied its
+// registers are refilled with the block PF strides ahead.  `first` holds the
+// codes of blk_begin (loaded by the caller before the decode tables were
+// built).
+template <int CW, int TF, int RW, int PF = 1>
 __device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0, int blk_begin,
                                             int blk_end, int blk_stride,
                                             BlockCodes<CW, TF>& first, const uint32_t* tabW,
                                             const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
-  BlockCodes<CW, TF> cur = first;
-  for (int blk = blk_begin; blk < blk_end; blk += blk_stride) {
-    BlockCodes<CW, TF> nxt;
-    const int nb = blk + blk_stride;
-    if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, nxt);
-    mma_block<CW, TF>(A, blk, tok0, cur, tabW, tabA, acc);
-    if (nb < blk_end) cur = nxt;
+  if constexpr (PF == 1) {
+    BlockCodes<CW, TF> cur = first;
+    for (int blk = blk_begin; blk < blk_end; blk += blk_stride) {
+      BlockCodes<CW, TF> nxt;
+      const int nb = blk + blk_stride;
+      if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, nxt);
+      mma_block<CW, TF, RW>(A, blk, tok0, cur, tabW, tabA, acc);
+      if (nb < blk_end) cur = nxt;
+    }
+  } else {
+    BlockCodes<CW, TF> buf[PF];
+    buf[0] = first;
+#pragma unroll
+    for (int d = 1; d < PF; ++d)
+      if (blk_begin + d * blk_stride < blk_end)
+        load_block<CW, TF>(A, blk_begin + d * blk_stride, j0, tok0, buf[d]);
+    for (int blk = blk_begin; blk < blk_end; blk += PF * blk_stride) {
+#pragma unroll
+      for (int d = 0; d < PF; ++d) {
+        const int b = blk + d * blk_stride;
+        if (b < blk_end) {
+          mma_block<CW, TF, RW>(A, b, tok0, buf[d], tabW, tabA, acc);
+          const int nb = b + PF * blk_stride;
+          if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, buf[d]);
+        }
+      }
+    }
+  }
+}
+
+// mfma_blocks for the GEMV kernel: buffer loads, PF blocks in flight,
+// activation masking only for a partial last K block.
+template <int CW, int TF, int PF, bool FULLK>
+__device__ __forceinline__ void gemv_blocks(const GemmArgs& A, const GemvAddr& ad, int blk_begin,
+                                            int blk_end, int blk_stride,
+                                            BlockCodes<CW, TF>& first, const uint32_t* tabW,
+                                            const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
+  BlockCodes<CW, TF> buf[PF];
+  buf[0] = first;
+#pragma unroll
+  for (int d = 1; d < PF; ++d)
+    if (blk_begin + d * blk_stride < blk_end)
+      load_block_buf<CW, TF>(ad, blk_begin + d * blk_stride, buf[d]);
+  for (int blk = blk_begin; blk < blk_end; blk += PF * blk_stride) {
+#pragma unroll
+    for (int d = 0; d < PF; ++d) {
+      const int b = blk + d * blk_stride;
+      if (b < blk_end) {
+        mma_block<CW, TF, WIDE_R, !FULLK>(A, b, 0, buf[d], tabW, tabA, acc);
+        const int nb = b + PF * blk_stride;
+        if (nb < blk_end) load_block_buf<CW, TF>(ad, nb, buf[d]);
+      }
+    }
   }
 }
 
@@ -215,59 +324,51 @@ __device__ __forceinline__ int xcd_tile(int b, int T) {
 // for the tile's columns - rows this workgroup has just streamed, so they are
 // L2 hits - and adds r * C_W[code] per column.  Thread t owns token
 // t / T (T = threads per token), four consecutive columns and a slice of the
-// token's entries; the slices' register sums are added through LDS in a fixed
-// order.  Returns nothing: part[i][slice][c] holds the partial sums.
-template <int COLS>
-__device__ __forceinline__ void tile_compensation(const GemmArgs& A, int j0, const float* cwf,
-                                                  float* part, int nslices, int tid,
-                                                  int nthreads, int slots) {
+// token's entries; 16 entries' row loads are issued before any is used.  The
+// slices' register sums are added through LDS in a fixed order (part).
+// `cwtab` is C_W replicated once per lane: entry (code, lane) at byte offset
+// code * 256 + lane * 4, so the 64 lanes of a wave never share a bank.
+template <int COLS, int B>
+__device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvAddr& ad, int j0,
+                                                  const float* cwtab, float* part, int nslices,
+                                                  int tid, int nthreads, int slots) {
   constexpr int QUADS = COLS / 4;
   const int T = nthreads / slots;  // threads per token, a multiple of QUADS
   const int i = tid / T, u = tid - i * T;
   const int quad = u % QUADS, slice = u / QUADS;
   const int k = A.k, E = 2 * k;
-  const int d_out = A.d_out;
-  const int j = j0 + 4 * quad;
-  const bool vec_ok = (d_out & 3) == 0 && j + 3 < d_out;
+  const uint32_t d_out = (uint32_t)A.d_out;
+  const uint32_t col4 = (uint32_t)(j0 + 4 * quad) * 4u;
+  const uint32_t lane4 = (uint32_t)(threadIdx.x & 63) * 4u;
+  const char* ctab = reinterpret_cast<const char*>(cwtab);
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   if (i < A.n) {
     const float* res = A.residual + (size_t)i * E;
     const int32_t* mx = A.max_idx + (size_t)i * k;
     const int32_t* mn = A.min_idx + (size_t)i * k;
-    constexpr int B = 8;
     for (int e0 = slice; e0 < E; e0 += B * nslices) {
       float r[B];
-      int sh[B];
-      uint32_t w[B][4];
+      uint32_t sh[B];
+      uint4_t w[B];
 #pragma unroll
       for (int b = 0; b < B; ++b) {
-        const int e = e0 + b * nslices;
-        int p = -1;
-        r[b] = 0.0f;
-        if (e < E) {
-          p = e < k ? mx[e] : mn[e - k];
-          r[b] = res[e];
-        }
-        const bool live = p >= 0 && p < A.d_in && r[b] != 0.0f;
-        if (!live) r[b] = 0.0f;
-        sh[b] = live ? 4 * (p & 7) : 0;
-        w[b][0] = w[b][1] = w[b][2] = w[b][3] = 0u;
-        if (live) {
-          const uint32_t* row = A.idx_w + (size_t)(p >> 3) * d_out + j;
-          if (vec_ok) {
-            const uint4_t v = *reinterpret_cast<const uint4_t*>(row);
-            w[b][0] = v[0]; w[b][1] = v[1]; w[b][2] = v[2]; w[b][3] = v[3];
-          } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-              if (j + c < d_out) w[b][c] = row[c];
-          }
-        }
+        const int e = min(e0 + b * nslices, E - 1);
+        const int p = e < k ? mx[e] : mn[e - k];
+        const bool live = (e0 + b * nslices) < E && p >= 0 && p < A.d_in;
+        r[b] = live ? res[e] : 0.0f;
+        const uint32_t pp = live ? (uint32_t)p : 0u;
+        sh[b] = 4u * (pp & 7u);
+        w[b] = __builtin_bit_cast(
+            uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)((pp >> 3) * d_out * 4u + col4),
+                                                           0, 0));
       }
 #pragma unroll
       for (int b = 0; b < B; ++b)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[c] += r[b] * cwf[(w[b][c] >> sh[b]) & 15u];
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t code = (w[b][c] >> sh[b]) & 15u;
+          acc[c] += r[b] * *reinterpret_cast<const float*>(ctab + ((code << 8) | lane4));
+        }
     }
   }
   if (i < slots) {
@@ -282,16 +383,19 @@ __device__ __forceinline__ void tile_compensation(const GemmArgs& A, int j0, con
 // so every output is written once, without atomics.  With outlier lists
 // (A.k > 0) the workgroup also adds the compensation of its columns.
 // ----------------------------------------------------------------------------
-template <int CW, int TF, int NW>
+template <int CW, int TF, int NW, int PF, bool FULLK>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
-  __shared__ uint32_t tabW[256 * DEC_R];
-  __shared__ uint32_t tabA[256 * DEC_R];
   constexpr int SLOTS = 16 * TF, COLS = 16 * CW;
   constexpr int NSLICES = (NW * 64 / SLOTS) / (COLS / 4) > 0 ? (NW * 64 / SLOTS) / (COLS / 4) : 1;
   static_assert((NW * 64 / SLOTS) % (COLS / 4) == 0, "threads per token must cover the columns");
-  __shared__ float4_t red[NW][CW * TF][64];
-  __shared__ float part[SLOTS * NSLICES * COLS];
-  __shared__ float cwf[16];
+  constexpr int RED_FLOATS = 4 * NW * CW * TF * 64;
+  constexpr int PART_FLOATS = SLOTS * NSLICES * COLS;
+  static_assert(4 * (RED_FLOATS + PART_FLOATS + 16 * 64) <= 256 * WIDE_R * 4,
+                "reduction buffers fit in tabW");
+  // 64 KiB; after the main loop it holds the wave reduction and the
+  // compensation partials
+  __shared__ uint32_t tabW[256 * WIDE_R];
+  __shared__ uint32_t tabA[256 * DEC_R];
   __shared__ uint16_t cbs[2][16];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
 
@@ -300,10 +404,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   const bool fused = A.k > 0;
 
   // issue the first block's loads, then build the tables while they fly
+  const GemvAddr ad = gemv_addr<CW>(A, j0);
   BlockCodes<CW, TF> first;
-  if (wave < nblk) load_block<CW, TF>(A, wave, j0, 0, first);
-  if (fused && tid < 16) cwf[tid] = h2f(A.lut->cb_wgt[tid]);
-  build_tables(A.lut, cbs, tabW, tabA, tid, NW * 64);  // barriers: cwf ready
+  if (wave < nblk) load_block_buf<CW, TF>(ad, wave, first);
+  build_tables<WIDE_R, DEC_R>(A.lut, cbs, tabW, tabA, tid, NW * 64);
 
   float4_t acc[CW][TF];
 #pragma unroll
@@ -311,14 +415,26 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 #pragma unroll
     for (int f = 0; f < TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (wave < nblk) mfma_blocks<CW, TF>(A, j0, 0, wave, nblk, NW, first, tabW, tabA, acc);
-
+  if (wave < nblk)
+    gemv_blocks<CW, TF, PF, FULLK>(A, ad, wave, nblk, NW, first, tabW, tabA, acc);
+  __syncthreads();  // every wave is done with tabW: reuse it for the reduction
+  float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tabW);
+  float* part = reinterpret_cast<float*>(tabW) + RED_FLOATS;  // compensation partials
+  float* cwtab = part + PART_FLOATS;                           // C_W, one copy per lane
 #pragma unroll
   for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) red[wave][c * TF + f][lane] = acc[c][f];
   // outlier branch, after the main loop so its weight rows are warm in L2
-  if (fused) tile_compensation<COLS>(A, j0, cwf, part, NSLICES, tid, NW * 64, SLOTS);
+  if (fused) {
+    for (int q = tid; q < 16 * 64; q += NW * 64) cwtab[q] = h2f(cbs[0][q >> 6]);
+    __syncthreads();
+    // entries in flight per thread: about a token's share per slice, <= 16
+    if (2 * A.k <= 4 * NSLICES)
+      tile_compensation<COLS, 4>(A, ad, j0, cwtab, part, NSLICES, tid, NW * 64, SLOTS);
+    else
+      tile_compensation<COLS, 16>(A, ad, j0, cwtab, part, NSLICES, tid, NW * 64, SLOTS);
+  }
   __syncthreads();
 
   const int g = lane >> 4, tc = lane & 15;
@@ -367,7 +483,7 @@ __global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A, int ncx, 
 
   BlockCodes<4, PF_TF> first;
   if (active) load_block<4, PF_TF>(A, 0, j0, tok0, first);
-  build_tables(A.lut, cbs, tabW, tabA, tid, 256);
+  build_tables<DEC_R, DEC_R>(A.lut, cbs, tabW, tabA, tid, 256);
 
   float4_t acc[4][PF_TF];
 #pragma unroll
@@ -375,7 +491,7 @@ __global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A, int ncx, 
 #pragma unroll
     for (int f = 0; f < PF_TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (active) mfma_blocks<4, PF_TF>(A, j0, tok0, 0, nblk, 1, first, tabW, tabA, acc);
+  if (active) mfma_blocks<4, PF_TF, DEC_R>(A, j0, tok0, 0, nblk, 1, first, tabW, tabA, acc);
 
   const int g = lane >> 4, tc = lane & 15;
 #pragma unroll
@@ -390,8 +506,13 @@ __global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A, int ncx, 
 template <int CW, int TF, int NW>
 static void launch_gemv(const GemmArgs& a, hipStream_t s) {
   const int ntiles = (a.d_out + 16 * CW - 1) / (16 * CW);
-  hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW>), dim3(ntiles), dim3(NW * 64), 0, s, a,
-                     ntiles);
+  constexpr int PF = 2;  // blocks in flight per wave
+  if ((a.d_in / 8) % 16 == 0)
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true>), dim3(ntiles), dim3(NW * 64), 0,
+                       s, a, ntiles);
+  else
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false>), dim3(ntiles), dim3(NW * 64),
+                       0, s, a, ntiles);
 }
 
 template <int TF>
