@@ -18,7 +18,7 @@
 //
 // Each thread owns a contiguous run of channels (a multiple of 8, read from
 // LDS as 16-byte vectors), so channel order inside a tie is the order of the
-// block scan.  Small batches use 1024-thread workgroups (short runs, latency
+// block scan.  Small batches use 512-thread workgroups (short runs, latency
 // bound), large batches 256-thread ones (many tokens per CU).
 #include "common.h"
 
@@ -27,6 +27,8 @@ namespace oasis {
 template <int NT>
 struct QuantSmem {
   uint32_t hist1[256];
+  uint16_t bucket[256];  // per high byte of the key: first | last cluster index << 8
+  float P[16];           // scaled boundaries
   uint32_t hist2_max[256];
   uint32_t hist2_min[256];
   float ca[16];
@@ -140,16 +142,42 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     return a;
   };
 
-  // ---- cluster index of every channel, packed 8 per word (coalesced stores)
-  uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
-  for (int v = tid; CLUSTER && v < nvec; v += NT) {
-    const uint4 q = xs4[v];
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-    uint32_t packed = 0;
+  // ---- cluster index of every channel, packed 8 per word (coalesced stores).
+  // The index is monotone in the order-preserving key, so the keys sharing a
+  // high byte span a range [first, last] of indices; only the few buckets a
+  // boundary crosses need compares: a = first + #{first <= c < last : x >= P_c}.
+  if constexpr (CLUSTER) {
+    if (tid < 16) S.P[tid] = tid < nb ? P[tid < 15 ? tid : 14] : 0.0f;
+    if (tid < 256) {
+      auto bits_of = [](uint32_t key) -> uint16_t {  // inverse of ord_key
+        return (uint16_t)((key & 0x8000u) ? (key & 0x7FFFu) : (~key & 0xFFFFu));
+      };
+      const uint32_t lo = cluster(h2f(bits_of((uint32_t)tid << 8)));
+      const uint32_t hi = cluster(h2f(bits_of(((uint32_t)tid << 8) | 0xFFu)));
+      S.bucket[tid] = (uint16_t)(lo | (hi << 8));
+    }
+    __syncthreads();
+    uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
+    for (int v = tid; v < nvec; v += NT) {
+      const uint4 q = xs4[v];
+      const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+      uint32_t packed = 0;
 #pragma unroll
-    for (int h = 0; h < 8; ++h)
-      packed |= cluster(h2f((uint16_t)(w[h >> 1] >> (16 * (h & 1))))) << (4 * h);
-    arow[v] = packed;
+      for (int h = 0; h < 8; ++h) {
+        const uint32_t bits = (w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
+        const uint32_t e = S.bucket[ord_key(bits) >> 8];
+        uint32_t a = e & 0xFFu;
+        const uint32_t last = e >> 8;
+        if (a < last) {  // a boundary lies inside this bucket
+          const float x = h2f((uint16_t)bits);
+          uint32_t add = 0;
+          for (uint32_t c = a; c < last; ++c) add += x >= S.P[c] ? 1u : 0u;
+          a += add;
+        }
+        packed |= a << (4 * h);
+      }
+      arow[v] = packed;
+    }
   }
   if (!TOPK || k == 0) return;  // uniform across the block
 
@@ -331,7 +359,7 @@ template <bool CL, bool TK>
 static hipError_t launch_parts(const QuantArgs& a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   // few tokens: wide workgroups keep each token's serial phases short
-  return a.n <= 64 ? launch_nt<1024, CL, TK>(a, s) : launch_nt<256, CL, TK>(a, s);
+  return a.n <= 64 ? launch_nt<512, CL, TK>(a, s) : launch_nt<256, CL, TK>(a, s);
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s) { return launch_parts<true, true>(a, s); }
