@@ -18,6 +18,32 @@ __device__ __forceinline__ float h2f(uint16_t bits) {
   return (float)__builtin_bit_cast(_Float16, bits);
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin (id mod 8).  Map ids so that
+// each XCD gets a contiguous range of tiles and neighbouring tiles share its
+// L2.  A bijection on [0, T).
+__device__ __forceinline__ int xcd_tile(int b, int T) {
+  const int per = T >> 3;
+  return b < 8 * per ? (b & 7) * per + (b >> 3) : b;
+}
+
+// Inclusive scan of one 64-bit value per thread over the block (NT threads).
+// Each call needs its own `tmp` (NT / 64 words): there is no trailing barrier.
+template <int NT>
+__device__ __forceinline__ uint64_t block_scan64(uint64_t v, uint64_t* tmp) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    uint64_t u = __shfl_up(v, off, 64);
+    if (lane >= off) v += u;
+  }
+  if (lane == 63) tmp[wid] = v;
+  __syncthreads();
+  uint64_t base = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w)
+    if (w < wid) base += tmp[w];
+  return v + base;
+}
 // Everything the host launchers need; argument checking happens in api.cpp.
 struct QuantArgs {
   const uint16_t* x;

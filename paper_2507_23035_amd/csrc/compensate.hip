@@ -5,12 +5,18 @@
 // are dequantized with the weight codebook (the Dequant Unit) and multiplied
 // by the residual (the MAC units), then merged into the main-branch output.
 //
-// One workgroup per (token, 64 or 256 output columns); its 4 waves split the
-// token's 2k listed channels and are summed through LDS.  A lane owns one or
-// four columns and issues the word loads of 16 listed channels before using
-// any of them, so the outlier stream costs a few memory latencies rather than
-// one per outlier.  Channel ids and residuals are wave-uniform (scalar loads); zero
-// residuals (channels already compensated through the max list) are skipped.
+// Two kernels.  k_compensate (few tokens): one workgroup per (token, 64 or
+// 256 output columns); its 4 waves split the token's 2k listed channels and
+// are summed through LDS.  A lane owns one or four columns and issues the word
+// loads of 16 listed channels before using any of them.  Channel ids and
+// residuals are wave-uniform; zero residuals (channels already compensated
+// through the max list) are skipped.
+//
+// k_compensate_rows (many tokens): a 32-bit word of the codes holds 8 input
+// channels, so fetching it for one outlier uses 4 of its 32 bits.  A workgroup
+// takes a tile of tokens, counting-sorts their listed outliers by word row in
+// LDS and fetches every touched row once for all the tile's outliers in it;
+// outlier channels recur across tokens, so rows are shared.
 #include "common.h"
 
 namespace oasis {
@@ -91,11 +97,301 @@ __global__ void __launch_bounds__(256) k_compensate(CompArgs A) {
   }
 }
 
+
+// ----------------------------------------------------------------------------
+// Row-grouped compensation.  Workgroup = (tile of up to TT tokens,
+// NW * 64 * CPL output columns); lane l of wave w owns CPL consecutive columns
+// and one register accumulator per (token, column).  The tile's live entries
+// (nonzero residual) are sorted by word row, then channel, then token: a run
+// of entries on one channel needs one codebook lookup per column for all its
+// tokens, and every sum is taken in a fixed order.  Every wave walks all
+// touched rows for its own columns.  A run's token mask drives an unrolled
+// loop over the tile's tokens, so each accumulator stays in a fixed register.
+//
+// Entry meta word: token (bits 0-4), channel within the row (5-7); the first
+// entry of a run also carries the run's token mask (8-15), bit 16 and the
+// run's length (17-29).
+// ----------------------------------------------------------------------------
+constexpr int ROW_TT = 4;       // tokens per tile, at most (<= 8: token mask)
+constexpr int ROW_EMAX = 4096;  // listed entries of a tile held in LDS
+constexpr int ROW_PF = 4;       // rows of codes in flight per wave
+
+// LDS bytes of one workgroup: codebook, per-row counters, entries (meta and
+// residual), touched-row list and row starts.
+static size_t rows_lds_bytes(int d_in, int tt, int k) {
+  const size_t R = (size_t)d_in / 8, emax = (size_t)tt * 2 * k;
+  const size_t rmax = R < emax ? R : emax;
+  return 64 + 4 * R + 8 * emax + 4 * rmax + 4 * (rmax + 1) + 16;
+}
+
+template <int TT, int CPL, int NW>
+__global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt, int ncol_tiles,
+                                                             int ntok_tiles) {
+  constexpr int NT = NW * 64;
+  static_assert(TT >= 1 && TT <= 8, "the run token mask has 8 bits");
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ uint64_t scan_tmp[NW];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int d_in = A.d_in, d_out = A.d_out, k = A.k, E2 = 2 * k;
+  const int R = d_in >> 3;
+  const int emax = tt * E2;
+  const int rmax = min(R, emax);
+  float* cwf = reinterpret_cast<float*>(smem);                    // 16
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + 64);         // R: count, then fill
+  uint32_t* meta = cnt + R;                                       // emax
+  float* rv = reinterpret_cast<float*>(meta + emax);              // emax
+  uint32_t* rowlist = reinterpret_cast<uint32_t*>(rv + emax);     // rmax
+  uint32_t* rowbeg = rowlist + rmax;                              // rmax + 1
+  uint32_t* nrow_s = rowbeg + rmax + 1;
+
+  // token tiles fastest, so one XCD sweeps every token tile of a column slab
+  // while the slab's rows sit in its L2
+  const int tile = xcd_tile(blockIdx.x, ncol_tiles * ntok_tiles);
+  const int tk = tile % ntok_tiles, ct = tile / ntok_tiles;
+  const int tok0 = tk * tt;
+  const int ntok = min(tt, A.n - tok0);
+  const int e_tot = ntok * E2;
+
+  if (tid < 16) cwf[tid] = h2f(A.lut->cb_wgt[tid]);
+  for (int r = tid; r < R; r += NT) cnt[r] = 0u;
+  __syncthreads();
+
+  // entry f of the tile: token tok0 + f / 2k, list position f % 2k
+  auto entry = [&](int f, int& t, int& e, int& p, float& r) -> bool {
+    t = f / E2;
+    e = f - t * E2;
+    const size_t i = (size_t)(tok0 + t);
+    p = e < k ? A.max_idx[i * k + e] : A.min_idx[i * k + (e - k)];
+    r = A.residual[i * E2 + e];
+    return r != 0.0f && p >= 0 && p < d_in;
+  };
+  for (int f = tid; f < e_tot; f += NT) {
+    int t, e, p;
+    float r;
+    if (entry(f, t, e, p, r)) atomicAdd(&cnt[p >> 3], 1u);
+  }
+  __syncthreads();
+
+  // exclusive scan over the rows (each thread a contiguous run): entry
+  // offsets, and the ascending list of touched rows
+  {
+    const int rpt = (R + NT - 1) / NT;
+    const int r0 = min(R, tid * rpt), r1 = min(R, r0 + rpt);
+    uint64_t loc = 0;
+    for (int r = r0; r < r1; ++r) loc += (uint64_t)cnt[r] | ((uint64_t)(cnt[r] != 0u) << 32);
+    const uint64_t excl = block_scan64<NT>(loc, scan_tmp) - loc;
+    uint32_t off = (uint32_t)excl, nr = (uint32_t)(excl >> 32);
+    for (int r = r0; r < r1; ++r) {
+      const uint32_t c = cnt[r];
+      if (c) {
+        rowlist[nr] = (uint32_t)r;
+        rowbeg[nr] = off;
+        ++nr;
+      }
+      cnt[r] = off;  // fill pointer
+      off += c;
+    }
+    if (tid == NT - 1) {
+      rowbeg[nr] = off;
+      *nrow_s = nr;
+    }
+  }
+  __syncthreads();
+  for (int f = tid; f < e_tot; f += NT) {
+    int t, e, p;
+    float r;
+    if (entry(f, t, e, p, r)) {
+      const uint32_t pos = atomicAdd(&cnt[p >> 3], 1u);
+      meta[pos] = ((uint32_t)(p & 7) << 5) | (uint32_t)t;
+      rv[pos] = r;
+    }
+  }
+  __syncthreads();
+  const uint32_t nrow = *nrow_s;
+  // each row: insertion sort by (channel, token) - atomics placed the entries
+  // in arbitrary order; a (channel, token) pair occurs once - then mark the
+  // runs of one channel with their token masks
+  for (uint32_t j = tid; j < nrow; j += NT) {
+    const uint32_t b = rowbeg[j], e_end = rowbeg[j + 1];
+    for (uint32_t q = b + 1; q < e_end; ++q) {
+      const uint32_t m = meta[q];
+      const float v = rv[q];
+      uint32_t z = q;
+      while (z > b && meta[z - 1] > m) {
+        meta[z] = meta[z - 1];
+        rv[z] = rv[z - 1];
+        --z;
+      }
+      meta[z] = m;
+      rv[z] = v;
+    }
+    for (uint32_t q = b; q < e_end;) {
+      const uint32_t ch = meta[q] >> 5;
+      uint32_t tm = 0, z = q, w = q;
+      for (; z < e_end && (meta[z] >> 5) == ch; ++z) {
+        const uint32_t t = meta[z] & 31u;
+        if (tm & (1u << t)) {
+          rv[w - 1] += rv[z];  // a token listing the channel twice: one entry
+        } else {
+          tm |= 1u << t;
+          meta[w] = meta[z];
+          rv[w] = rv[z];
+          ++w;
+        }
+      }
+      // live entries [q, w) in token order; [w, z) are never read
+      meta[q] |= (tm << 8) | (1u << 16) | ((z - q) << 17);
+      q = z;
+    }
+  }
+  __syncthreads();
+
+  // ---- accumulate: every wave walks all touched rows for its columns.
+  // Row data and entries are read 64 at a time into lanes (lane u holds
+  // item base + u) and handed out as scalars with readlane, so no LDS read
+  // sits on the per-row path.  A row's offset into the codes is the scalar
+  // offset of its buffer loads.
+  const int j0 = ct * (NW * 64 * CPL) + wave * 64 * CPL + lane * CPL;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(A.idx_w), 0, (int)((uint32_t)R * (uint32_t)d_out * 4u), 0x00020000);
+  const uint32_t voff = (uint32_t)j0 * 4u;
+  const uint32_t row_bytes = (uint32_t)d_out * 4u;
+  auto window = [&](const uint32_t* src, uint32_t first, uint32_t count, uint32_t fill) {
+    return first + lane < count ? src[first + lane] : fill;
+  };
+  // load stream: rows [lw0, lw0 + 64) of the list in lanes
+  uint32_t lw0 = 0, lw_row = window(rowlist, 0, nrow, 0u);
+  auto load_batch = [&](uint32_t base, uint32_t (&w)[ROW_PF][CPL]) {
+    if (base >= lw0 + 64) {  // batches are 64-aligned: slide the window
+      lw0 += 64;
+      lw_row = window(rowlist, lw0, nrow, 0u);
+    }
+#pragma unroll
+    for (int d = 0; d < ROW_PF; ++d) {
+      const uint32_t j = base + d;
+      const uint32_t row = (uint32_t)__builtin_amdgcn_readlane((int)lw_row, (int)(j - lw0));
+      // rows past the list read past the buffer: zeros, no branch
+      const int soff = j < nrow ? (int)(row * row_bytes) : (int)0x80000000u;
+      if constexpr (CPL % 4 == 0) {
+#pragma unroll
+        for (int h = 0; h < CPL / 4; ++h) {
+          const uint4_t v = __builtin_bit_cast(
+              uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(voff + 16u * h), soff, 0));
+          w[d][4 * h] = v[0]; w[d][4 * h + 1] = v[1]; w[d][4 * h + 2] = v[2]; w[d][4 * h + 3] = v[3];
+        }
+      } else {
+        w[d][0] = __builtin_amdgcn_raw_buffer_load_b32(rw, (int)voff, soff, 0);
+      }
+    }
+  };
+  float acc[TT][CPL];
+#pragma unroll
+  for (int t = 0; t < TT; ++t)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) acc[t][c] = 0.0f;
+
+  // processing stream: rows [pw0, pw0 + 64) and entries [ew0, ew0 + 64)
+  uint32_t pw0 = 0;
+  uint32_t pw_beg = window(rowbeg, 0, nrow + 1, 0u), pw_end = window(rowbeg, 1, nrow + 1, 0u);
+  uint32_t ew0 = 0;
+  uint32_t ew_m = window(meta, 0, emax, 0u);
+  float ew_r = __builtin_bit_cast(float, window(reinterpret_cast<const uint32_t*>(rv), 0, emax, 0u));
+
+  uint32_t wv[2][ROW_PF][CPL];
+  load_batch(0, wv[0]);
+  for (uint32_t jb = 0; jb < nrow; jb += 2 * ROW_PF) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t base = jb + h * ROW_PF;
+      load_batch(base + ROW_PF, wv[h ^ 1]);  // next batch in flight
+#pragma unroll
+      for (int d = 0; d < ROW_PF; ++d)  // wait for this batch only
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) asm volatile("" : "+v"(wv[h][d][c]));
+      if (base >= pw0 + 64) {
+        pw0 += 64;
+        pw_beg = window(rowbeg, pw0, nrow + 1, 0u);
+        pw_end = window(rowbeg, pw0 + 1, nrow + 1, 0u);
+      }
+#pragma unroll
+      for (int d = 0; d < ROW_PF; ++d) {
+        const uint32_t j = base + d;
+        // rows past the list: an empty range
+        const int u = (int)(j - pw0);
+        const uint32_t b = j < nrow ? (uint32_t)__builtin_amdgcn_readlane((int)pw_beg, u) : 0u;
+        const uint32_t e_end = j < nrow ? (uint32_t)__builtin_amdgcn_readlane((int)pw_end, u) : 0u;
+        for (uint32_t q = b; q < e_end;) {
+          // a run: one channel, at most TT entries, in token order
+          if (q + TT > ew0 + 64) {  // entries are consumed in order: slide
+            ew0 = q;
+            ew_m = window(meta, ew0, emax, 0u);
+            ew_r = __builtin_bit_cast(float, window(reinterpret_cast<const uint32_t*>(rv), ew0, emax, 0u));
+          }
+          const uint32_t m = (uint32_t)__builtin_amdgcn_readlane((int)ew_m, (int)(q - ew0));
+          const uint32_t tm = (m >> 8) & 0xFFu;
+          const uint32_t sh = ((m >> 5) & 7u) * 4u;
+          float cv[CPL];
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) cv[c] = cwf[(wv[h][d][c] >> sh) & 15u];
+          int pos = (int)(q - ew0);
+#pragma unroll
+          for (int T = 0; T < TT; ++T) {
+            if (tm & (1u << T)) {
+              const float r = __builtin_bit_cast(
+                  float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ew_r), pos));
+              ++pos;
+#pragma unroll
+              for (int c = 0; c < CPL; ++c) acc[T][c] = fmaf(r, cv[c], acc[T][c]);
+            }
+          }
+          q += max(1u, (m >> 17) & 0x1FFFu);  // the run's length (>= 1 always advances)
+        }
+      }
+    }
+  }
+
+  // ---- merge: y (+)= s_j * acc
+  float sw[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) sw[c] = (j0 + c < d_out) ? A.w_scale[j0 + c] : 0.0f;
+#pragma unroll
+  for (int t = 0; t < TT; ++t) {
+    float* dst = A.y + (size_t)(tok0 + t) * d_out + j0;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      if (t < ntok && j0 + c < d_out) {
+        const float v = sw[c] * acc[t][c];
+        dst[c] = A.accumulate ? dst[c] + v : v;
+      }
+    }
+  }
+}
+
 hipError_t launch_compensate(const CompArgs& a, hipStream_t s) {
   if (a.n == 0 || a.d_out == 0) return hipSuccess;
   if (a.k == 0) {
     if (a.accumulate) return hipSuccess;
     return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
+  }
+  // many tokens: row-grouped, as long as a tile's lists fit in LDS
+  const int tt = a.k <= ROW_EMAX / 2 ? min(ROW_TT, ROW_EMAX / (2 * a.k)) : 0;
+  if (a.n > 64 && tt >= 1) {
+    constexpr int NW = 4;
+    const size_t lds = rows_lds_bytes(a.d_in, tt, a.k);
+    const int ntok_tiles = (a.n + tt - 1) / tt;
+    auto go = [&](auto kern, int cols) -> hipError_t {
+      if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+      }
+      const int ncol_tiles = (a.d_out + cols - 1) / cols;
+      hipLaunchKernelGGL(kern, dim3(ncol_tiles * ntok_tiles), dim3(NW * 64), lds, s, a, tt,
+                         ncol_tiles, ntok_tiles);
+      return hipGetLastError();
+    };
+    if ((a.d_out & 3) == 0) return go(k_compensate_rows<ROW_TT, 8, NW>, NW * 64 * 8);
+    return go(k_compensate_rows<ROW_TT, 1, NW>, NW * 64);
   }
   // few tokens: one column per lane for more workgroups; many: 16-byte loads
   if (a.n <= 64) {

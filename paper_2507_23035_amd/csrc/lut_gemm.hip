@@ -311,14 +311,6 @@ __device__ __forceinline__ void store_out(const GemmArgs& A, int tok, int j, flo
     *dst = val;
 }
 
-// Workgroups are dealt to the 8 XCDs round-robin (id mod 8).  Map ids so that
-// each XCD gets a contiguous range of tiles and neighbouring tiles share its
-// L2.  A bijection on [0, T).
-__device__ __forceinline__ int xcd_tile(int b, int T) {
-  const int per = T >> 3;
-  return b < 8 * per ? (b & 7) * per + (b >> 3) : b;
-}
-
 // Outlier compensation of one column tile (fused variant).  Every listed
 // outlier (token i, channel p, residual r) reads the words of input channel p
 // for the tile's columns - rows this workgroup has just streamed, so they are

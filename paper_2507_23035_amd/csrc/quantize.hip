@@ -9,7 +9,8 @@
 //   * the residual of every listed outlier (Sec. III-C2).
 // The top-k is a two-pass radix select on order-preserving 16-bit keys
 // (-0 folded into +0) shared by the max and min lists: pass 1 histograms the
-// high byte, pass 2 the low byte inside the boundary bucket, which fixes the
+// high byte while the token is staged, pass 2 the low byte inside the boundary
+// bucket, which fixes the
 // threshold key T and the count G of keys strictly beyond it.  Keys beyond T
 // (G < k of them) are ranked among themselves, one lane per candidate; keys
 // equal to T are taken in channel order, which one block-wide scan provides.  The
@@ -18,7 +19,7 @@
 //
 // Each thread owns a contiguous run of channels (a multiple of 8, read from
 // LDS as 16-byte vectors), so channel order inside a tie is the order of the
-// block scan.  Small batches use 512-thread workgroups (short runs, latency
+// block scan; the pass that counts ties also writes the run's cluster codes.  Small batches use 512-thread workgroups (short runs, latency
 // bound), large batches 256-thread ones (many tokens per CU).
 #include "common.h"
 
@@ -32,7 +33,7 @@ struct QuantSmem {
   uint32_t hist2_max[256];
   uint32_t hist2_min[256];
   float ca[16];
-  uint64_t scan_tmp[NT / 64];
+  uint64_t scan_tmp[3][NT / 64];  // one per block scan: no barrier between reuses
   uint32_t red_tmp[NT / 64];
   uint32_t ctl[8];    // B1/G1 of the max and min lists, then T/G of both
 };
@@ -53,25 +54,6 @@ __device__ __forceinline__ uint32_t ord_key(uint32_t bits) {
   return (bits & 0x8000u) ? (~bits & 0xFFFFu) : (bits | 0x8000u);
 }
 
-// Inclusive scan of one 64-bit value per thread over the block.
-template <int NT>
-__device__ __forceinline__ uint64_t block_scan64(uint64_t v, uint64_t* tmp) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    uint64_t u = __shfl_up(v, off, 64);
-    if (lane >= off) v += u;
-  }
-  if (lane == 63) tmp[wid] = v;
-  __syncthreads();
-  uint64_t base = 0;
-#pragma unroll
-  for (int w = 0; w < NT / 64; ++w)
-    if (w < wid) base += tmp[w];
-  __syncthreads();
-  return v + base;
-}
-
 template <int NT>
 __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* tmp) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -82,8 +64,7 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* tmp) {
   uint32_t r = 0;
 #pragma unroll
   for (int w = 0; w < NT / 64; ++w) r = max(r, tmp[w]);
-  __syncthreads();
-  return r;
+  return r;  // `tmp` is not reused: no trailing barrier
 }
 
 // CLUSTER: write scale and codes.  TOPK: write outlier lists and residuals.
@@ -105,7 +86,19 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   const uint16_t* xrow = A.x + (size_t)i * d_in;
   const uint4* xs4 = reinterpret_cast<const uint4*>(xs);
 
-  // ---- stage the token in LDS (coalesced 16-byte loads) and find absmax
+  const bool topk = TOPK && k > 0;                 // uniform across the block
+  const bool fused_cluster = CLUSTER && topk;      // codes written by the count pass
+  if (tid < 256) {
+    S.hist1[tid] = 0;
+    S.hist2_max[tid] = 0;
+    S.hist2_min[tid] = 0;
+  }
+  if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
+  if (tid < 8) S.ctl[tid] = 0;
+  __syncthreads();  // histograms cleared
+
+  // ---- stage the token in LDS (coalesced 16-byte loads), find absmax and
+  // build the histogram of the key's high byte (pass 1 of the top-k select)
   uint32_t amax = 0;
   const int nvec = d_in / 8;
   for (int v = tid; v < nvec; v += NT) {
@@ -114,15 +107,13 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
     for (int h = 0; h < 4; ++h) amax = max(amax, max(w[h] & 0x7FFFu, (w[h] >> 16) & 0x7FFFu));
+    if (topk) {
+#pragma unroll
+      for (int h = 0; h < 8; ++h)
+        atomicAdd(&S.hist1[ord_key((w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu) >> 8], 1u);
+    }
   }
-  for (int b = tid; b < 256; b += NT) {
-    S.hist1[b] = 0;
-    S.hist2_max[b] = 0;
-    S.hist2_min[b] = 0;
-  }
-  if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
-  if (tid < 8) S.ctl[tid] = 0;
-  amax = block_max<NT>(amax, S.red_tmp);  // barrier: xs, ca, hist visible
+  amax = block_max<NT>(amax, S.red_tmp);  // barrier: xs and hist1 complete
 
   const float t = (A.scale_mode == OASIS_SCALE_NONE) ? 1.0f : h2f((uint16_t)amax);
   if (CLUSTER && tid == 0) A.act_scale[i] = t;
@@ -142,11 +133,12 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     return a;
   };
 
-  // ---- cluster index of every channel, packed 8 per word (coalesced stores).
-  // The index is monotone in the order-preserving key, so the keys sharing a
-  // high byte span a range [first, last] of indices; only the few buckets a
-  // boundary crosses need compares: a = first + #{first <= c < last : x >= P_c}.
-  if constexpr (CLUSTER) {
+  // ---- cluster index of every channel, packed 8 per word.  The index is
+  // monotone in the order-preserving key, so the keys sharing a high byte span
+  // a range [first, last] of indices; only the few buckets a boundary crosses
+  // need compares: a = first + #{first <= c < last : x >= P_c}.  The table is
+  // visible after the next barrier.
+  if (CLUSTER) {
     if (tid < 16) S.P[tid] = tid < nb ? P[tid < 15 ? tid : 14] : 0.0f;
     if (tid < 256) {
       auto bits_of = [](uint32_t key) -> uint16_t {  // inverse of ord_key
@@ -156,47 +148,44 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       const uint32_t hi = cluster(h2f(bits_of(((uint32_t)tid << 8) | 0xFFu)));
       S.bucket[tid] = (uint16_t)(lo | (hi << 8));
     }
-    __syncthreads();
-    uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
-    for (int v = tid; v < nvec; v += NT) {
-      const uint4 q = xs4[v];
-      const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-      uint32_t packed = 0;
-#pragma unroll
-      for (int h = 0; h < 8; ++h) {
-        const uint32_t bits = (w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
-        const uint32_t e = S.bucket[ord_key(bits) >> 8];
-        uint32_t a = e & 0xFFu;
-        const uint32_t last = e >> 8;
-        if (a < last) {  // a boundary lies inside this bucket
-          const float x = h2f((uint16_t)bits);
-          uint32_t add = 0;
-          for (uint32_t c = a; c < last; ++c) add += x >= S.P[c] ? 1u : 0u;
-          a += add;
-        }
-        packed |= a << (4 * h);
-      }
-      arow[v] = packed;
-    }
   }
-  if (!TOPK || k == 0) return;  // uniform across the block
+  auto code8 = [&](const uint4& q) -> uint32_t {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    uint32_t packed = 0;
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      const uint32_t bits = (w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
+      const uint32_t e = S.bucket[ord_key(bits) >> 8];
+      uint32_t a = e & 0xFFu;
+      const uint32_t last = e >> 8;
+      if (a < last) {  // a boundary lies inside this bucket
+        const float x = h2f((uint16_t)bits);
+        uint32_t add = 0;
+        for (uint32_t c = a; c < last; ++c) add += x >= S.P[c] ? 1u : 0u;
+        a += add;
+      }
+      packed |= a << (4 * h);
+    }
+    return packed;
+  };
+  uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
+  if (!topk) {
+    if (CLUSTER) {
+      __syncthreads();
+      for (int v = tid; v < nvec; v += NT) arow[v] = code8(xs4[v]);  // coalesced
+    }
+    return;
+  }
 
   // contiguous run of channels owned by this thread, in 8-channel vectors
   const int vpt = (nvec + NT - 1) / NT;
   const int v0 = min(nvec, tid * vpt), v1 = min(nvec, v0 + vpt);
 
-  // ---- pass 1: histogram of the key's high byte (shared by both lists)
-  for (int v = v0; v < v1; ++v) {
-    const uint4 q = xs4[v];
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int h = 0; h < 8; ++h)
-      atomicAdd(&S.hist1[ord_key((w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu) >> 8], 1u);
-  }
-  __syncthreads();
+  // ---- pass 1 (histogram built while staging): the high-byte buckets that
+  // hold the k-th largest and the k-th smallest key
   {
     const uint32_t h = tid < 256 ? S.hist1[tid] : 0u;
-    const uint32_t pre = (uint32_t)block_scan64<NT>(h, S.scan_tmp);  // keys with byte <= tid
+    const uint32_t pre = (uint32_t)block_scan64<NT>(h, S.scan_tmp[0]);  // keys with byte <= tid
     if (tid < 256) {
       const uint32_t suf_excl = (uint32_t)d_in - pre;  // keys with high byte > tid
       if (suf_excl < (uint32_t)k && (uint32_t)k <= suf_excl + h) {
@@ -228,7 +217,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   {
     const uint32_t hm = tid < 256 ? S.hist2_max[tid] : 0u;
     const uint32_t hn = tid < 256 ? S.hist2_min[tid] : 0u;
-    const uint64_t pre = block_scan64<NT>(((uint64_t)hn << 32) | hm, S.scan_tmp);
+    const uint64_t pre = block_scan64<NT>(((uint64_t)hn << 32) | hm, S.scan_tmp[1]);
     const uint32_t pre_m = (uint32_t)pre, pre_n = (uint32_t)(pre >> 32);
     if (tid < 256) {
       const uint32_t kk = (uint32_t)k - G1max;
@@ -256,7 +245,8 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   // ---- per-thread counts, in channel order, of (max-list ties, min-list ties,
   // keys above Tmax, keys below Tmin), 16 bits each: one 64-bit block scan
   // gives every thread its tie ranks and its candidate slots.  (Exclusive
-  // prefixes stay below 2^16 because d_in <= 65536.)
+  // prefixes stay below 2^16 because d_in <= 65536.)  The same pass writes the
+  // cluster codes of the thread's run.
   uint64_t cnt = 0;
   for (int v = v0; v < v1; ++v) {
     const uint4 q = xs4[v];
@@ -267,8 +257,9 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       cnt += (uint64_t)(key == Tmax) | ((uint64_t)(key == Tmin) << 16) |
              ((uint64_t)(key > Tmax) << 32) | ((uint64_t)(key < Tmin) << 48);
     }
+    if (fused_cluster) arow[v] = code8(q);
   }
-  const uint64_t excl = block_scan64<NT>(cnt, S.scan_tmp) - cnt;
+  const uint64_t excl = block_scan64<NT>(cnt, S.scan_tmp[2]) - cnt;
   uint32_t rank_max = (uint32_t)(excl & 0xFFFFu), rank_min = (uint32_t)((excl >> 16) & 0xFFFFu);
   uint32_t slot_max = (uint32_t)((excl >> 32) & 0xFFFFu), slot_min = (uint32_t)(excl >> 48);
 

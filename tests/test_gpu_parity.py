@@ -149,6 +149,9 @@ RAGGED = [
     (130, 136, 129, 5, 4, 4, 7),
     (40, 4096, 200, 32, 1, 1, 8),
     (64, 520, 512, 16, 4, 2, 9),
+    (72, 1032, 260, 300, 4, 4, 14),  # row-grouped compensation: 6 tokens per tile
+    (70, 4096, 96, 2048, 4, 4, 15),  # one token per tile
+    (66, 4104, 40, 2050, 4, 4, 16),  # lists too long for a tile: per-token kernel
 ]
 
 
