@@ -30,6 +30,7 @@ namespace oasis {
 // shared helpers
 // ----------------------------------------------------------------------------
 constexpr int DEC_R = 8;   // replication of the byte -> fp16 pair tables
+constexpr int HALF_R = 32;  // one copy per lane of a half-wave: conflict-free
 constexpr int WIDE_R = 64;  // one copy per lane: lane l always reads bank l
 
 // byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes,
@@ -59,8 +60,9 @@ __device__ __forceinline__ void build_tables(const oasis_lut_block* lut, uint16_
 // Eight codes -> eight fp16 centroid values (channel order kept: VGPR v holds
 // the two channels of byte v).  R == WIDE_R: the byte offset of entry
 // (byte, lane) is byte * 256 + lane * 4, assembled by one v_perm_b32 from the
-// code word and the lane's offset (bank = lane, no conflicts).  Otherwise
-// entry byte * R + (lane mod R).
+// code word and the lane's offset (bank = lane, no conflicts).  R == HALF_R:
+// byte * 128 + (lane mod 32) * 4, also conflict-free (a wave's LDS read is
+// served 32 lanes at a time).  Otherwise entry byte * R + (lane mod R).
 template <int R>
 __device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, uint32_t lane) {
   uint4_t r;
@@ -70,6 +72,15 @@ __device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, 
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
+      r[b] = *reinterpret_cast<const uint32_t*>(base + off);
+    }
+  } else if constexpr (R == HALF_R) {
+    // byte offset (byte << 7) | (lane mod 32) * 4: 32 lanes, 32 banks
+    const char* base = reinterpret_cast<const char*>(tab);
+    const uint32_t lane4 = (lane & 31u) * 4u;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const uint32_t off = (((w >> (8 * b)) & 0xFFu) << 7) | lane4;
       r[b] = *reinterpret_cast<const uint32_t*>(base + off);
     }
   } else {
@@ -92,10 +103,13 @@ struct BlockCodes {
 template <int CW>
 __device__ __forceinline__ void load_words(const uint32_t* __restrict__ row, int j, int d_out,
                                            uint32_t (&out)[CW]) {
-  if (CW == 4 && (d_out & 3) == 0 && j + 3 < d_out) {
-    const uint4_t v = *reinterpret_cast<const uint4_t*>(row + j);
+  if (CW % 4 == 0 && (d_out & 3) == 0 && j + CW - 1 < d_out) {
 #pragma unroll
-    for (int c = 0; c < CW; ++c) out[c] = v[c];
+    for (int h = 0; h < CW / 4; ++h) {
+      const uint4_t v = *reinterpret_cast<const uint4_t*>(row + j + 4 * h);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) out[4 * h + c] = v[c];
+    }
   } else if (CW == 2 && (d_out & 1) == 0 && j + 1 < d_out) {
     const uint2 v = *reinterpret_cast<const uint2*>(row + j);
     out[0] = v.x;
@@ -203,7 +217,7 @@ __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
 // CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
 // MASK: zero the activation operand of words past d_in and of tokens past n
 // (needed when those words hold codes that are not 0 contributions).
-template <int CW, int TF, int RW, bool MASK = true>
+template <int CW, int TF, int RW, bool MASK = true, int RA = DEC_R>
 __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
                                           const BlockCodes<CW, TF>& bc, const uint32_t* tabW,
                                           const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
@@ -217,7 +231,7 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
     half8_t bf[TF];
 #pragma unroll
     for (int f = 0; f < TF; ++f) {
-      bf[f] = expand_word<DEC_R>(bc.av[f][s], tabA, lane);
+      bf[f] = expand_word<RA>(bc.av[f][s], tabA, lane);
       if constexpr (MASK) {
         const bool tok_ok = (tok0 + 16 * f + m) < A.n;
         if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
@@ -238,7 +252,7 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
 // registers are refilled with the block PF strides ahead.  `first` holds the
 // codes of blk_begin (loaded by the caller before the decode tables were
 // built).
-template <int CW, int TF, int RW, int PF = 1>
+template <int CW, int TF, int RW, int PF = 1, int RA = DEC_R>
 __device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0, int blk_begin,
                                             int blk_end, int blk_stride,
                                             BlockCodes<CW, TF>& first, const uint32_t* tabW,
@@ -249,7 +263,7 @@ __device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0,
       BlockCodes<CW, TF> nxt;
       const int nb = blk + blk_stride;
       if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, nxt);
-      mma_block<CW, TF, RW>(A, blk, tok0, cur, tabW, tabA, acc);
+      mma_block<CW, TF, RW, true, RA>(A, blk, tok0, cur, tabW, tabA, acc);
       if (nb < blk_end) cur = nxt;
     }
   } else {
@@ -264,7 +278,7 @@ __device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0,
       for (int d = 0; d < PF; ++d) {
         const int b = blk + d * blk_stride;
         if (b < blk_end) {
-          mma_block<CW, TF, RW>(A, b, tok0, buf[d], tabW, tabA, acc);
+          mma_block<CW, TF, RW, true, RA>(A, b, tok0, buf[d], tabW, tabA, acc);
           const int nb = b + PF * blk_stride;
           if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, buf[d]);
         }
@@ -454,45 +468,175 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 }
 
 // ----------------------------------------------------------------------------
-// MFMA kernel, prefill tiling: 2 x 2 waves, each 64 columns x 64 tokens, over
-// the whole reduction; WG tile 128 columns x 128 tokens.  Tiles are ordered
-// column-major over the XCDs so that one XCD's L2 holds few weight columns.
+// MFMA kernel, prefill tiling: WX x WY waves, each 16*CW columns x 16*TF
+// tokens over the whole reduction; tiles ordered column-major over the XCDs
+// so that one XCD's L2 holds few weight columns.
+//
+// Both pair tables share one 64 KiB region: row `byte` (256 bytes) holds 32
+// copies of the weight entry, then 32 of the activation entry, so the byte
+// offset of either is byte * 256 + (lane mod 32) * 4 (+ 128 for activations)
+// - one v_perm_b32 per byte, and 32 lanes read 32 different banks.
 // ----------------------------------------------------------------------------
-constexpr int PF_TF = 4;
+__device__ __forceinline__ half8_t expand_dual(uint32_t w, const char* tab, uint32_t lane4) {
+  uint4_t r;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
+    r[b] = *reinterpret_cast<const uint32_t*>(tab + off);
+  }
+  return __builtin_bit_cast(half8_t, r);
+}
 
-__global__ void __launch_bounds__(256) k_gemm_mfma_prefill(GemmArgs A, int ncx, int nty) {
-  __shared__ uint32_t tabW[256 * DEC_R];
-  __shared__ uint32_t tabA[256 * DEC_R];
+// Per-lane byte offsets of the codes of one wave (block 0); a block's offset
+// travels in an SGPR.  Reads past either tensor return 0.
+template <int CW, int TF>
+struct PrefillAddr {
+  __amdgpu_buffer_rsrc_t rw, ra;
+  uint32_t woff[4];   // row 4g + s, column j0 + CW*m
+  uint32_t aoff[TF];  // token tok0 + 16f + m, word 4g
+  uint32_t wblk;      // bytes per block of 16 weight rows
+};
+
+template <int CW, int TF>
+__device__ __forceinline__ void load_block_pf(const PrefillAddr<CW, TF>& ad, int blk,
+                                              BlockCodes<CW, TF>& bc) {
+  const int sw = (int)((uint32_t)blk * ad.wblk);
+  const int sa = blk * 64;
+#pragma unroll
+  for (int f = 0; f < TF; ++f)
+    bc.av[f] = __builtin_bit_cast(
+        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.ra, (int)ad.aoff[f], sa, 0));
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if constexpr (CW % 4 == 0) {
+#pragma unroll
+      for (int h = 0; h < CW / 4; ++h) {
+        const uint4_t v = __builtin_bit_cast(
+            uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)(ad.woff[s] + 16u * h), sw, 0));
+#pragma unroll
+        for (int c = 0; c < 4; ++c) bc.wv[s][4 * h + c] = v[c];
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < CW; ++c)
+        bc.wv[s][c] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)(ad.woff[s] + 4u * c), sw, 0);
+    }
+  }
+}
+
+// KMASK: zero the activation operand of words past the end of the reduction
+// (only the last block can hold them; they would read the next token's codes).
+template <int CW, int TF, bool KMASK>
+__device__ __forceinline__ void mma_block_pf(int blk, int KB, const BlockCodes<CW, TF>& bc,
+                                             const char* tab, uint32_t l4w, uint32_t l4a,
+                                             float4_t (&acc)[CW][TF]) {
+  const int g = (threadIdx.x & 63) >> 4;
+  const int kw0 = blk * 16 + 4 * g;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    half8_t bf[TF];
+#pragma unroll
+    for (int f = 0; f < TF; ++f) {
+      bf[f] = expand_dual(bc.av[f][s], tab, l4a);
+      if (KMASK && kw0 + s >= KB) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int c = 0; c < CW; ++c) {
+      const half8_t af = expand_dual(bc.wv[s][c], tab, l4w);
+#pragma unroll
+      for (int f = 0; f < TF; ++f)
+        acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[f], acc[c][f], 0, 0, 0);
+    }
+  }
+}
+
+template <int CW, int TF, int WX, int WY, bool FULLK>
+__global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, int ncx, int nty) {
+  constexpr int NT = WX * WY * 64;
+  __shared__ uint32_t tab[256 * 64];  // 64 KiB: both pair tables
   __shared__ uint16_t cbs[2][16];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, m = lane & 15;
 
   const int r = xcd_tile(blockIdx.x, ncx * nty);
   const int cx = r / nty, ty = r % nty;
-  const int j0 = cx * 128 + (wave & 1) * 64;
-  const int tok0 = ty * 128 + (wave >> 1) * 64;
-  const int nblk = (A.d_in / 8 + 15) / 16;
-  const bool active = j0 < A.d_out && tok0 < A.n;
+  const int j0 = (cx * WX + wave % WX) * 16 * CW;
+  const int tok0 = (ty * WY + wave / WX) * 16 * TF;
+  const int KB = A.d_in >> 3;
+  const int nblk = (KB + 15) / 16;
 
-  BlockCodes<4, PF_TF> first;
-  if (active) load_block<4, PF_TF>(A, 0, j0, tok0, first);
-  build_tables<DEC_R, DEC_R>(A.lut, cbs, tabW, tabA, tid, 256);
+  PrefillAddr<CW, TF> ad;
+  ad.rw = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(A.idx_w), 0,
+                                            (int)((uint32_t)KB * (uint32_t)A.d_out * 4u), 0x00020000);
+  ad.ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(A.idx_act), 0,
+                                            (int)((uint32_t)A.n * (uint32_t)KB * 4u), 0x00020000);
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    ad.woff[s] = ((uint32_t)(4 * g + s) * (uint32_t)A.d_out + (uint32_t)(j0 + CW * m)) * 4u;
+#pragma unroll
+  for (int f = 0; f < TF; ++f)
+    ad.aoff[f] = ((uint32_t)(tok0 + 16 * f + m) * (uint32_t)KB + 4u * g) * 4u;
+  ad.wblk = 16u * (uint32_t)A.d_out * 4u;
 
-  float4_t acc[4][PF_TF];
-#pragma unroll
-  for (int c = 0; c < 4; ++c)
-#pragma unroll
-    for (int f = 0; f < PF_TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
+  // first block's loads in flight while the tables are built
+  BlockCodes<CW, TF> buf[2];
+  load_block_pf<CW, TF>(ad, 0, buf[0]);
+  if (tid < 16) cbs[0][tid] = A.lut->cb_wgt[tid];
+  else if (tid < 32) cbs[1][tid - 16] = A.lut->cb_act[tid - 16];
+  __syncthreads();
+  for (int e = tid; e < 256 * 64; e += NT) {
+    const int byte = e >> 6, side = (e >> 5) & 1;  // 0: weights, 1: activations
+    tab[e] = (uint32_t)cbs[side][byte & 15] | ((uint32_t)cbs[side][byte >> 4] << 16);
+  }
+  __syncthreads();
 
-  if (active) mfma_blocks<4, PF_TF, DEC_R>(A, j0, tok0, 0, nblk, 1, first, tabW, tabA, acc);
+  float4_t acc[CW][TF];
+#pragma unroll
+  for (int c = 0; c < CW; ++c)
+#pragma unroll
+    for (int f = 0; f < TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int g = lane >> 4, tc = lane & 15;
+  const char* tb = reinterpret_cast<const char*>(tab);
+  const uint32_t l4w = (uint32_t)(lane & 31) * 4u, l4a = l4w + 128u;
+  // full blocks; a partial last block (FULLK false) is peeled off and masked
+  const int nfull = FULLK ? nblk : nblk - 1;
+  for (int blk = 0; blk < nfull; blk += 2) {
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
+    for (int d = 0; d < 2; ++d) {
+      const int b = blk + d;
+      if (b < nfull) {
+        if (b + 1 < nblk) load_block_pf<CW, TF>(ad, b + 1, buf[d ^ 1]);
+        mma_block_pf<CW, TF, false>(b, KB, buf[d], tb, l4w, l4a, acc);
+      }
+    }
+  }
+  if constexpr (!FULLK) {
+    if (nfull & 1)
+      mma_block_pf<CW, TF, true>(nfull, KB, buf[1], tb, l4w, l4a, acc);
+    else
+      mma_block_pf<CW, TF, true>(nfull, KB, buf[0], tb, l4w, l4a, acc);
+  }
+
+  const int tc = lane & 15;
 #pragma unroll
-    for (int f = 0; f < PF_TF; ++f)
+  for (int c = 0; c < CW; ++c)
+#pragma unroll
+    for (int f = 0; f < TF; ++f)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        store_out(A, tok0 + 16 * f + tc, j0 + 4 * (4 * g + q) + c, acc[c][f][q]);
+        store_out(A, tok0 + 16 * f + tc, j0 + CW * (4 * g + q) + c, acc[c][f][q]);
+}
+
+template <int CW, int TF, int WX, int WY>
+static void launch_prefill(const GemmArgs& a, hipStream_t s) {
+  const int ncx = (a.d_out + WX * 16 * CW - 1) / (WX * 16 * CW);
+  const int nty = (a.n + WY * 16 * TF - 1) / (WY * 16 * TF);
+  if ((a.d_in / 8) % 16 == 0)
+    hipLaunchKernelGGL((k_gemm_mfma_prefill<CW, TF, WX, WY, true>), dim3(ncx * nty),
+                       dim3(WX * WY * 64), 0, s, a, ncx, nty);
+  else
+    hipLaunchKernelGGL((k_gemm_mfma_prefill<CW, TF, WX, WY, false>), dim3(ncx * nty),
+                       dim3(WX * WY * 64), 0, s, a, ncx, nty);
 }
 
 template <int CW, int TF, int NW>
@@ -528,8 +672,7 @@ hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s) {
   } else if (a.n <= 32) {
     launch_gemv_tf<2>(a, s);
   } else {
-    const int ncx = (a.d_out + 127) / 128, nty = (a.n + 127) / 128;
-    hipLaunchKernelGGL(k_gemm_mfma_prefill, dim3(ncx * nty), dim3(256), 0, s, a, ncx, nty);
+    launch_prefill<4, 4, 2, 2>(a, s);
   }
   return hipGetLastError();
 }
