@@ -30,7 +30,6 @@ namespace oasis {
 // shared helpers
 // ----------------------------------------------------------------------------
 constexpr int DEC_R = 8;   // replication of the byte -> fp16 pair tables
-constexpr int HALF_R = 32;  // one copy per lane of a half-wave: conflict-free
 constexpr int WIDE_R = 64;  // one copy per lane: lane l always reads bank l
 
 // byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes,
@@ -60,9 +59,8 @@ __device__ __forceinline__ void build_tables(const oasis_lut_block* lut, uint16_
 // Eight codes -> eight fp16 centroid values (channel order kept: VGPR v holds
 // the two channels of byte v).  R == WIDE_R: the byte offset of entry
 // (byte, lane) is byte * 256 + lane * 4, assembled by one v_perm_b32 from the
-// code word and the lane's offset (bank = lane, no conflicts).  R == HALF_R:
-// byte * 128 + (lane mod 32) * 4, also conflict-free (a wave's LDS read is
-// served 32 lanes at a time).  Otherwise entry byte * R + (lane mod R).
+// code word and the lane's offset (bank = lane, no conflicts).  Otherwise
+// entry byte * R + (lane mod R).
 template <int R>
 __device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, uint32_t lane) {
   uint4_t r;
@@ -72,15 +70,6 @@ __device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, 
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
-      r[b] = *reinterpret_cast<const uint32_t*>(base + off);
-    }
-  } else if constexpr (R == HALF_R) {
-    // byte offset (byte << 7) | (lane mod 32) * 4: 32 lanes, 32 banks
-    const char* base = reinterpret_cast<const char*>(tab);
-    const uint32_t lane4 = (lane & 31u) * 4u;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const uint32_t off = (((w >> (8 * b)) & 0xFFu) << 7) | lane4;
       r[b] = *reinterpret_cast<const uint32_t*>(base + off);
     }
   } else {
@@ -100,64 +89,7 @@ struct BlockCodes {
   uint32_t wv[4][CW];
 };
 
-template <int CW>
-__device__ __forceinline__ void load_words(const uint32_t* __restrict__ row, int j, int d_out,
-                                           uint32_t (&out)[CW]) {
-  if (CW % 4 == 0 && (d_out & 3) == 0 && j + CW - 1 < d_out) {
-#pragma unroll
-    for (int h = 0; h < CW / 4; ++h) {
-      const uint4_t v = *reinterpret_cast<const uint4_t*>(row + j + 4 * h);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) out[4 * h + c] = v[c];
-    }
-  } else if (CW == 2 && (d_out & 1) == 0 && j + 1 < d_out) {
-    const uint2 v = *reinterpret_cast<const uint2*>(row + j);
-    out[0] = v.x;
-    out[CW - 1] = v.y;
-  } else {
-#pragma unroll
-    for (int c = 0; c < CW; ++c) out[c] = (j + c < d_out) ? row[j + c] : 0u;
-  }
-}
-
-template <int CW, int TF>
-__device__ __forceinline__ void load_block(const GemmArgs& A, int blk, int j0, int tok0,
-                                           BlockCodes<CW, TF>& bc) {
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, m = lane & 15;
-  const int KB = A.d_in >> 3;
-  const int d_out = A.d_out;
-  const size_t arow_words = (size_t)KB;
-  const uint32_t* aw = reinterpret_cast<const uint32_t*>(A.idx_act);
-  const int kw0 = blk * 16 + 4 * g;  // this lane group's first word in the block
-#pragma unroll
-  for (int f = 0; f < TF; ++f) {
-    const int tok = tok0 + 16 * f + m;
-    bc.av[f] = uint4_t{0u, 0u, 0u, 0u};
-    if (tok < A.n) {
-      const uint32_t* src = aw + (size_t)tok * arow_words + kw0;
-      if (kw0 + 3 < KB && (arow_words & 3) == 0) {
-        bc.av[f] = *reinterpret_cast<const uint4_t*>(src);
-      } else {
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          if (kw0 + s < KB) bc.av[f][s] = src[s];
-      }
-    }
-  }
-#pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const int kw = kw0 + s;
-    if (kw < KB) {
-      load_words<CW>(A.idx_w + (size_t)kw * d_out, j0 + CW * m, d_out, bc.wv[s]);
-    } else {
-#pragma unroll
-      for (int c = 0; c < CW; ++c) bc.wv[s][c] = 0u;
-    }
-  }
-}
-
-// Buffer-load form of load_block for the GEMV kernel.  Per-lane byte offsets
+// Buffer loads of a block of codes for the GEMV kernel.  Per-lane byte offsets
 // are computed once; the block's offset travels in an SGPR.  The buffer
 // descriptors carry the tensors' sizes, so a read past the end returns 0
 // instead of faulting: columns past d_out or tokens past n only feed outputs
@@ -217,7 +149,7 @@ __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
 // CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
 // MASK: zero the activation operand of words past d_in and of tokens past n
 // (needed when those words hold codes that are not 0 contributions).
-template <int CW, int TF, int RW, bool MASK = true, int RA = DEC_R>
+template <int CW, int TF, int RW, bool MASK = true>
 __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
                                           const BlockCodes<CW, TF>& bc, const uint32_t* tabW,
                                           const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
@@ -231,7 +163,7 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
     half8_t bf[TF];
 #pragma unroll
     for (int f = 0; f < TF; ++f) {
-      bf[f] = expand_word<RA>(bc.av[f][s], tabA, lane);
+      bf[f] = expand_word<DEC_R>(bc.av[f][s], tabA, lane);
       if constexpr (MASK) {
         const bool tok_ok = (tok0 + 16 * f + m) < A.n;
         if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
@@ -247,48 +179,11 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
   }
 }
 
-// Blocks blk_begin, blk_begin + stride, ... < blk_end of one wave with PF
-// blocks' codes in flight: after a block is expanded and multiplied its
-// registers are refilled with the block PF strides ahead.  `first` holds the
-// codes of blk_begin (loaded by the caller before the decode tables were
-// built).
-template <int CW, int TF, int RW, int PF = 1, int RA = DEC_R>
-__device__ __forceinline__ void mfma_blocks(const GemmArgs& A, int j0, int tok0, int blk_begin,
-                                            int blk_end, int blk_stride,
-                                            BlockCodes<CW, TF>& first, const uint32_t* tabW,
-                                            const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
-  if constexpr (PF == 1) {
-    BlockCodes<CW, TF> cur = first;
-    for (int blk = blk_begin; blk < blk_end; blk += blk_stride) {
-      BlockCodes<CW, TF> nxt;
-      const int nb = blk + blk_stride;
-      if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, nxt);
-      mma_block<CW, TF, RW, true, RA>(A, blk, tok0, cur, tabW, tabA, acc);
-      if (nb < blk_end) cur = nxt;
-    }
-  } else {
-    BlockCodes<CW, TF> buf[PF];
-    buf[0] = first;
-#pragma unroll
-    for (int d = 1; d < PF; ++d)
-      if (blk_begin + d * blk_stride < blk_end)
-        load_block<CW, TF>(A, blk_begin + d * blk_stride, j0, tok0, buf[d]);
-    for (int blk = blk_begin; blk < blk_end; blk += PF * blk_stride) {
-#pragma unroll
-      for (int d = 0; d < PF; ++d) {
-        const int b = blk + d * blk_stride;
-        if (b < blk_end) {
-          mma_block<CW, TF, RW, true, RA>(A, b, tok0, buf[d], tabW, tabA, acc);
-          const int nb = b + PF * blk_stride;
-          if (nb < blk_end) load_block<CW, TF>(A, nb, j0, tok0, buf[d]);
-        }
-      }
-    }
-  }
-}
-
-// mfma_blocks for the GEMV kernel: buffer loads, PF blocks in flight,
-// activation masking only for a partial last K block.
+// Blocks blk_begin, blk_begin + stride, ... < blk_end of one GEMV wave with
+// PF blocks' codes in flight (buffer loads): after a block is expanded and
+// multiplied its registers are refilled with the block PF strides ahead.
+// `first` holds the codes of blk_begin (loaded before the decode tables were
+// built).  Activations are masked only for a partial last K block.
 template <int CW, int TF, int PF, bool FULLK>
 __device__ __forceinline__ void gemv_blocks(const GemmArgs& A, const GemvAddr& ad, int blk_begin,
                                             int blk_end, int blk_stride,
@@ -488,11 +383,13 @@ __device__ __forceinline__ half8_t expand_dual(uint32_t w, const char* tab, uint
 }
 
 // Per-lane byte offsets of the codes of one wave (block 0); a block's offset
-// travels in an SGPR.  Reads past either tensor return 0.
+// travels in an SGPR.  Reads past either tensor return 0.  Weight lane m of
+// column tile c holds column j0 + 16c + m, so the MFMA's output rows 4g..4g+3
+// are 4 consecutive columns: each lane stores 16 contiguous bytes.
 template <int CW, int TF>
 struct PrefillAddr {
   __amdgpu_buffer_rsrc_t rw, ra;
-  uint32_t woff[4];   // row 4g + s, column j0 + CW*m
+  uint32_t woff[4];   // row 4g + s, column j0 + m (tile c: + 64c bytes)
   uint32_t aoff[TF];  // token tok0 + 16f + m, word 4g
   uint32_t wblk;      // bytes per block of 16 weight rows
 };
@@ -507,21 +404,10 @@ __device__ __forceinline__ void load_block_pf(const PrefillAddr<CW, TF>& ad, int
     bc.av[f] = __builtin_bit_cast(
         uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.ra, (int)ad.aoff[f], sa, 0));
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    if constexpr (CW % 4 == 0) {
+  for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int h = 0; h < CW / 4; ++h) {
-        const uint4_t v = __builtin_bit_cast(
-            uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)(ad.woff[s] + 16u * h), sw, 0));
-#pragma unroll
-        for (int c = 0; c < 4; ++c) bc.wv[s][4 * h + c] = v[c];
-      }
-    } else {
-#pragma unroll
-      for (int c = 0; c < CW; ++c)
-        bc.wv[s][c] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)(ad.woff[s] + 4u * c), sw, 0);
-    }
-  }
+    for (int c = 0; c < CW; ++c)
+      bc.wv[s][c] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)(ad.woff[s] + 64u * c), sw, 0);
 }
 
 // KMASK: zero the activation operand of words past the end of the reduction
@@ -572,7 +458,7 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
                                             (int)((uint32_t)A.n * (uint32_t)KB * 4u), 0x00020000);
 #pragma unroll
   for (int s = 0; s < 4; ++s)
-    ad.woff[s] = ((uint32_t)(4 * g + s) * (uint32_t)A.d_out + (uint32_t)(j0 + CW * m)) * 4u;
+    ad.woff[s] = ((uint32_t)(4 * g + s) * (uint32_t)A.d_out + (uint32_t)(j0 + m)) * 4u;
 #pragma unroll
   for (int f = 0; f < TF; ++f)
     ad.aoff[f] = ((uint32_t)(tok0 + 16 * f + m) * (uint32_t)KB + 4u * g) * 4u;
@@ -617,14 +503,30 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
       mma_block_pf<CW, TF, true>(nfull, KB, buf[0], tb, l4w, l4a, acc);
   }
 
+  // lane (g, tc) of tile (c, f): token tok0 + 16f + tc, columns
+  // j0 + 16c + 4g .. + 3
   const int tc = lane & 15;
+  const bool vec = (A.d_out & 3) == 0;
 #pragma unroll
-  for (int c = 0; c < CW; ++c)
+  for (int c = 0; c < CW; ++c) {
+    const int j = j0 + 16 * c + 4 * g;
+    if (vec && j + 3 < A.d_out) {
+      const float4_t sw = *reinterpret_cast<const float4_t*>(A.w_scale + j);
 #pragma unroll
-    for (int f = 0; f < TF; ++f)
+      for (int f = 0; f < TF; ++f) {
+        const int tok = tok0 + 16 * f + tc;
+        if (tok >= A.n) continue;
+        float4_t* dst = reinterpret_cast<float4_t*>(A.y + (size_t)tok * A.d_out + j);
+        const float4_t v = A.act_scale[tok] * sw * acc[c][f];
+        *dst = A.accumulate ? *dst + v : v;
+      }
+    } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        store_out(A, tok0 + 16 * f + tc, j0 + CW * (4 * g + q) + c, acc[c][f][q]);
+      for (int f = 0; f < TF; ++f)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) store_out(A, tok0 + 16 * f + tc, j + q, acc[c][f][q]);
+    }
+  }
 }
 
 template <int CW, int TF, int WX, int WY>
