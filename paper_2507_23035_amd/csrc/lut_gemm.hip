@@ -12,7 +12,7 @@
 // (entry (a, w) = C_A[a] * C_W[w]), so the sum over p is the dense
 // contraction sum_p C_A[a_ip] * C_W[w_pj] of exact fp16 centroid values.
 // Codes are expanded to those fp16 values in registers (a byte of two codes
-// selects a packed pair from a 256-entry LDS table) and fed to
+// selects a packed pair from an LDS table) and fed to
 // v_mfma_f32_16x16x32_f16.  Every product equals its LUT entry bit for bit;
 // only the fp32 summation order differs from the literal scheme.
 //
@@ -20,7 +20,7 @@
 // B = activation codes (column = token).  Lane (g, m), g = lane / 16, holds the
 // 8 codes of one 32-bit word.  Within a block of 16 words (128 channels) lane
 // group g and step s use word 4g + s on both sides, so the weight rows are read
-// as full 256-byte segments and each token's 4 words as one 16-byte load; the
+// as contiguous segments and each token's 4 words as one 16-byte load; the
 // order in which channels enter the MFMA is irrelevant to the sum.
 #include "common.h"
 
@@ -29,55 +29,52 @@ namespace oasis {
 // ----------------------------------------------------------------------------
 // shared helpers
 // ----------------------------------------------------------------------------
-constexpr int DEC_R = 8;   // replication of the byte -> fp16 pair tables
-constexpr int WIDE_R = 64;  // one copy per lane: lane l always reads bank l
 
-// byte b -> (C[b & 15] | C[b >> 4] << 16): the two fp16 centroids of its codes,
-// replicated R times (entry b * R + r).  `cb` is the codebook staged in LDS.
-template <int R>
-__device__ __forceinline__ void build_pair_table(uint32_t* tab, const uint16_t* cb, int tid,
-                                                 int nthreads) {
-  for (int e = tid; e < 256 * R; e += nthreads) {
-    const int b = e / R;
-    tab[e] = (uint32_t)cb[b & 15] | ((uint32_t)cb[b >> 4] << 16);
+// Dual decode table in LDS (64 KiB): row `byte` (256 bytes) holds 32 copies of
+// the weight entry pair(C_W, byte), then 32 copies of the activation entry
+// pair(C_A, byte), pair(C, b) = C[b & 15] | C[b >> 4] << 16 (fp16 bits).  Lane
+// l reads copy l mod 32, so the byte offset of an entry is
+// byte * 256 + (l mod 32) * 4 (+ 128 for activations): one v_perm_b32 per byte,
+// and the 32 lanes of a half-wave always hit 32 different banks.  Written with
+// 16-byte stores; each thread loads the few codebook entries it needs straight
+// from the LUT block (chunk c of 16 bytes: row c / 16, side (c / 8) mod 2).
+template <int NT>
+struct DualTableLoader {
+  static_assert(NT % 256 == 0 && 4096 % NT == 0, "256..4096 threads");
+  uint32_t lo;
+  uint32_t hi[4096 / NT];
+  __device__ __forceinline__ void load(const oasis_lut_block* lut, int tid) {
+    const uint16_t* cb = ((tid >> 3) & 1) ? lut->cb_act : lut->cb_wgt;
+    lo = cb[(tid >> 4) & 15];
+#pragma unroll
+    for (int j = 0; j < 4096 / NT; ++j) hi[j] = cb[(tid + NT * j) >> 8];
   }
-}
-
-// Stage both codebooks of the LUT block in LDS, then build both pair tables.
-template <int RW, int RA>
-__device__ __forceinline__ void build_tables(const oasis_lut_block* lut, uint16_t (&cbs)[2][16],
-                                             uint32_t* tabW, uint32_t* tabA, int tid,
-                                             int nthreads) {
-  if (tid < 16) cbs[0][tid] = lut->cb_wgt[tid];
-  else if (tid < 32) cbs[1][tid - 16] = lut->cb_act[tid - 16];
-  __syncthreads();
-  build_pair_table<RW>(tabW, cbs[0], tid, nthreads);
-  build_pair_table<RA>(tabA, cbs[1], tid, nthreads);
-  __syncthreads();
-}
-
-// Eight codes -> eight fp16 centroid values (channel order kept: VGPR v holds
-// the two channels of byte v).  R == WIDE_R: the byte offset of entry
-// (byte, lane) is byte * 256 + lane * 4, assembled by one v_perm_b32 from the
-// code word and the lane's offset (bank = lane, no conflicts).  Otherwise
-// entry byte * R + (lane mod R).
-template <int R>
-__device__ __forceinline__ half8_t expand_word(uint32_t w, const uint32_t* tab, uint32_t lane) {
-  uint4_t r;
-  if constexpr (R == WIDE_R) {
-    const char* base = reinterpret_cast<const char*>(tab);
-    const uint32_t lane4 = lane * 4u;  // < 256: fits the low byte
+  __device__ __forceinline__ void store(uint32_t* tab, int tid) const {
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
-      r[b] = *reinterpret_cast<const uint32_t*>(base + off);
+    for (int j = 0; j < 4096 / NT; ++j) {
+      const uint32_t v = lo | (hi[j] << 16);
+      reinterpret_cast<uint4_t*>(tab)[tid + NT * j] = uint4_t{v, v, v, v};
     }
-  } else {
-    const uint32_t lo = lane & (R - 1);
+  }
+};
+
+// Eight codes -> eight fp16 centroid values (VGPR v holds the two channels of
+// byte v): the table offset of byte v is assembled by one v_perm_b32 from the
+// code word and the lane's offset `lane4` (< 256).
+__device__ __forceinline__ half8_t expand_dual(uint32_t w, const char* tab, uint32_t lane4) {
+  uint4_t r;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) r[b] = tab[((w >> (8 * b)) & 0xFFu) * R + lo];
+  for (int b = 0; b < 4; ++b) {
+    const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
+    r[b] = *reinterpret_cast<const uint32_t*>(tab + off);
   }
   return __builtin_bit_cast(half8_t, r);
+}
+
+// C_W[code] from the weight half of the dual table (row `code` holds
+// pair(C_W, code), whose low half is C_W[code]).
+__device__ __forceinline__ float weight_centroid(const char* tab, uint32_t code, uint32_t lane4) {
+  return h2f((uint16_t)*reinterpret_cast<const uint32_t*>(tab + ((code << 8) | lane4)));
 }
 
 // Raw codes of one block of 16 words for one wave: the activation words of
@@ -147,31 +144,28 @@ __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
 
 // Expand the codes of one block to fp16 centroid values and run its MFMAs:
 // CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
-// MASK: zero the activation operand of words past d_in and of tokens past n
-// (needed when those words hold codes that are not 0 contributions).
-template <int CW, int TF, int RW, bool MASK = true>
-__device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
-                                          const BlockCodes<CW, TF>& bc, const uint32_t* tabW,
-                                          const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, m = lane & 15;
-  const int KB = A.d_in >> 3;
+// Activations of tokens past n (tok_ok false) are not expanded; MASK also
+// zeroes the words past d_in of a partial last block.
+template <int CW, int TF, bool MASK>
+__device__ __forceinline__ void mma_block(int KB, int blk, const BlockCodes<CW, TF>& bc,
+                                          const char* tab, uint32_t l4w, uint32_t l4a,
+                                          const bool (&tok_ok)[TF], float4_t (&acc)[CW][TF]) {
+  const int g = (threadIdx.x & 63) >> 4;
   const int kw0 = blk * 16 + 4 * g;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    const bool live = (kw0 + s) < KB;  // words past the end contribute nothing
+    const bool live = !MASK || (kw0 + s) < KB;  // words past the end contribute nothing
     half8_t bf[TF];
 #pragma unroll
     for (int f = 0; f < TF; ++f) {
-      bf[f] = expand_word<DEC_R>(bc.av[f][s], tabA, lane);
-      if constexpr (MASK) {
-        const bool tok_ok = (tok0 + 16 * f + m) < A.n;
-        if (!(live && tok_ok)) bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
-      }
+      if (tok_ok[f] && live)
+        bf[f] = expand_dual(bc.av[f][s], tab, l4a);
+      else
+        bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
     }
 #pragma unroll
     for (int c = 0; c < CW; ++c) {
-      const half8_t af = expand_word<RW>(bc.wv[s][c], tabW, lane);
+      const half8_t af = expand_dual(bc.wv[s][c], tab, l4w);
 #pragma unroll
       for (int f = 0; f < TF; ++f)
         acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[f], acc[c][f], 0, 0, 0);
@@ -182,25 +176,20 @@ __device__ __forceinline__ void mma_block(const GemmArgs& A, int blk, int tok0,
 // Blocks blk_begin, blk_begin + stride, ... < blk_end of one GEMV wave with
 // PF blocks' codes in flight (buffer loads): after a block is expanded and
 // multiplied its registers are refilled with the block PF strides ahead.
-// `first` holds the codes of blk_begin (loaded before the decode tables were
-// built).  Activations are masked only for a partial last K block.
+// `buf` holds the codes of the first PF blocks (loaded before the table was
+// built).
 template <int CW, int TF, int PF, bool FULLK>
-__device__ __forceinline__ void gemv_blocks(const GemmArgs& A, const GemvAddr& ad, int blk_begin,
+__device__ __forceinline__ void gemv_blocks(int KB, const GemvAddr& ad, int blk_begin,
                                             int blk_end, int blk_stride,
-                                            BlockCodes<CW, TF>& first, const uint32_t* tabW,
-                                            const uint32_t* tabA, float4_t (&acc)[CW][TF]) {
-  BlockCodes<CW, TF> buf[PF];
-  buf[0] = first;
-#pragma unroll
-  for (int d = 1; d < PF; ++d)
-    if (blk_begin + d * blk_stride < blk_end)
-      load_block_buf<CW, TF>(ad, blk_begin + d * blk_stride, buf[d]);
+                                            BlockCodes<CW, TF> (&buf)[PF], const char* tab,
+                                            uint32_t l4w, uint32_t l4a, const bool (&tok_ok)[TF],
+                                            float4_t (&acc)[CW][TF]) {
   for (int blk = blk_begin; blk < blk_end; blk += PF * blk_stride) {
 #pragma unroll
     for (int d = 0; d < PF; ++d) {
       const int b = blk + d * blk_stride;
       if (b < blk_end) {
-        mma_block<CW, TF, WIDE_R, !FULLK>(A, b, 0, buf[d], tabW, tabA, acc);
+        mma_block<CW, TF, !FULLK>(KB, b, buf[d], tab, l4w, l4a, tok_ok, acc);
         const int nb = b + PF * blk_stride;
         if (nb < blk_end) load_block_buf<CW, TF>(ad, nb, buf[d]);
       }
@@ -222,59 +211,64 @@ __device__ __forceinline__ void store_out(const GemmArgs& A, int tok, int j, flo
 
 // Outlier compensation of one column tile (fused variant).  Every listed
 // outlier (token i, channel p, residual r) reads the words of input channel p
-// for the tile's columns - rows this workgroup has just streamed, so they are
-// L2 hits - and adds r * C_W[code] per column.  Thread t owns token
-// t / T (T = threads per token), four consecutive columns and a slice of the
-// token's entries; 16 entries' row loads are issued before any is used.  The
-// slices' register sums are added through LDS in a fixed order (part).
-// `cwtab` is C_W replicated once per lane: entry (code, lane) at byte offset
-// code * 256 + lane * 4, so the 64 lanes of a wave never share a bank.
-template <int COLS, int B>
-__device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvAddr& ad, int j0,
-                                                  const float* cwtab, float* part, int nslices,
-                                                  int tid, int nthreads, int slots) {
-  constexpr int QUADS = COLS / 4;
-  const int T = nthreads / slots;  // threads per token, a multiple of QUADS
-  const int i = tid / T, u = tid - i * T;
-  const int quad = u % QUADS, slice = u / QUADS;
+// for the tile's columns - rows this workgroup streams, so mostly L2 hits -
+// and adds r * C_W[code] per column.  Thread t owns token t / T (T = threads
+// per token), four consecutive columns and a slice of the token's entries; B
+// entries' row loads are issued before any is used.  With PRE the first B
+// entries of the slice come preloaded (`first`).
+template <int B>
+struct CompEntries {
+  int p[B];
+  float r[B];
+};
+
+template <int B>
+__device__ __forceinline__ void comp_entries(const GemmArgs& A, int i, int e0, int nslices,
+                                             CompEntries<B>& ce) {
   const int k = A.k, E = 2 * k;
+  const float* res = A.residual + (size_t)i * E;
+  const int32_t* mx = A.max_idx + (size_t)i * k;
+  const int32_t* mn = A.min_idx + (size_t)i * k;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const int e = min(e0 + b * nslices, E - 1);
+    const bool live = e0 + b * nslices < E;
+    const int p = e < k ? mx[e] : mn[e - k];
+    ce.p[b] = live && p >= 0 && p < A.d_in ? p : -1;
+    ce.r[b] = res[e];
+  }
+}
+
+template <int COLS, int B, bool PRE>
+__device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvAddr& ad, int j0,
+                                                  const char* tab, int nslices, int i, int quad,
+                                                  int slice, const CompEntries<B>& first,
+                                                  float (&acc)[4]) {
+  const int E = 2 * A.k;
   const uint32_t d_out = (uint32_t)A.d_out;
   const uint32_t col4 = (uint32_t)(j0 + 4 * quad) * 4u;
-  const uint32_t lane4 = (uint32_t)(threadIdx.x & 63) * 4u;
-  const char* ctab = reinterpret_cast<const char*>(cwtab);
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  if (i < A.n) {
-    const float* res = A.residual + (size_t)i * E;
-    const int32_t* mx = A.max_idx + (size_t)i * k;
-    const int32_t* mn = A.min_idx + (size_t)i * k;
-    for (int e0 = slice; e0 < E; e0 += B * nslices) {
-      float r[B];
-      uint32_t sh[B];
-      uint4_t w[B];
+  const uint32_t l4 = (uint32_t)(threadIdx.x & 31) * 4u;
+  CompEntries<B> ce = first;
+  for (int e0 = slice; e0 < E; e0 += B * nslices) {
+    if (!PRE || e0 != slice) comp_entries<B>(A, i, e0, nslices, ce);
+    uint32_t sh[B];
+    float r[B];
+    uint4_t w[B];
 #pragma unroll
-      for (int b = 0; b < B; ++b) {
-        const int e = min(e0 + b * nslices, E - 1);
-        const int p = e < k ? mx[e] : mn[e - k];
-        const bool live = (e0 + b * nslices) < E && p >= 0 && p < A.d_in;
-        r[b] = live ? res[e] : 0.0f;
-        const uint32_t pp = live ? (uint32_t)p : 0u;
-        sh[b] = 4u * (pp & 7u);
-        w[b] = __builtin_bit_cast(
-            uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)((pp >> 3) * d_out * 4u + col4),
-                                                           0, 0));
-      }
-#pragma unroll
-      for (int b = 0; b < B; ++b)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const uint32_t code = (w[b][c] >> sh[b]) & 15u;
-          acc[c] += r[b] * *reinterpret_cast<const float*>(ctab + ((code << 8) | lane4));
-        }
+    for (int b = 0; b < B; ++b) {
+      const bool live = ce.p[b] >= 0;
+      const uint32_t pp = live ? (uint32_t)ce.p[b] : 0u;
+      r[b] = live ? ce.r[b] : 0.0f;
+      sh[b] = 4u * (pp & 7u);
+      w[b] = __builtin_bit_cast(
+          uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)((pp >> 3) * d_out * 4u + col4),
+                                                         0, 0));
     }
-  }
-  if (i < slots) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) part[(i * nslices + slice) * COLS + 4 * quad + c] = acc[c];
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        acc[c] += r[b] * weight_centroid(tab, (w[b][c] >> sh[b]) & 15u, l4);
   }
 }
 
@@ -282,83 +276,113 @@ __device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvA
 // MFMA kernel, few tokens (GEMV-like): one workgroup per 16*CW output
 // columns, its NW waves interleave the K blocks and are summed through LDS,
 // so every output is written once, without atomics.  With outlier lists
-// (A.k > 0) the workgroup also adds the compensation of its columns.
+// (A.k > 0) the workgroup also adds the compensation of its columns; each
+// wave starts its share as soon as its own blocks are done.
+//
+// Prologue order matters: the codebook entries for the decode table are
+// requested first, then the scales and the first outlier entries, then the
+// weight codes, so building the table waits only for the codebook while the
+// weight stream is in flight.
 // ----------------------------------------------------------------------------
-template <int CW, int TF, int NW, int PF, bool FULLK>
+template <int CW, int TF, int NW, int PF, bool FULLK, int B>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
+  constexpr int NT = NW * 64;
   constexpr int SLOTS = 16 * TF, COLS = 16 * CW;
-  constexpr int NSLICES = (NW * 64 / SLOTS) / (COLS / 4) > 0 ? (NW * 64 / SLOTS) / (COLS / 4) : 1;
-  static_assert((NW * 64 / SLOTS) % (COLS / 4) == 0, "threads per token must cover the columns");
+  constexpr int NSLICES = (NT / SLOTS) / (COLS / 4) > 0 ? (NT / SLOTS) / (COLS / 4) : 1;
+  static_assert((NT / SLOTS) % (COLS / 4) == 0, "threads per token must cover the columns");
   constexpr int RED_FLOATS = 4 * NW * CW * TF * 64;
   constexpr int PART_FLOATS = SLOTS * NSLICES * COLS;
-  static_assert(4 * (RED_FLOATS + PART_FLOATS + 16 * 64) <= 256 * WIDE_R * 4,
-                "reduction buffers fit in tabW");
-  // 64 KiB; after the main loop it holds the wave reduction and the
-  // compensation partials
-  __shared__ uint32_t tabW[256 * WIDE_R];
-  __shared__ uint32_t tabA[256 * DEC_R];
-  __shared__ uint16_t cbs[2][16];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  static_assert(4 * (RED_FLOATS + PART_FLOATS) <= 64 * 1024, "reduction buffers fit in the table");
+  constexpr int EPT = (SLOTS * COLS + NT - 1) / NT;  // outputs per thread in the epilogue
+  __shared__ uint32_t tab[256 * 64];  // 64 KiB decode table; after the main loop the reduction
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  const int j0 = xcd_tile(blockIdx.x, ntiles) * 16 * CW;
-  const int nblk = (A.d_in / 8 + 15) / 16;
+  const int j0 = xcd_tile(blockIdx.x, ntiles) * COLS;
+  const int KB = A.d_in >> 3;
+  const int nblk = (KB + 15) / 16;
   const bool fused = A.k > 0;
 
-  // issue the first block's loads, then build the tables while they fly
+  // ---- prologue: codebook entries, scales, outlier entries, weight codes
+  DualTableLoader<NT> dt;
+  dt.load(A.lut, tid);
+  float sc[EPT];  // s_j * t_i of this thread's epilogue outputs (s_j alone for the compensation)
+  float swj[EPT];
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    const int o = tid + NT * q;
+    const int tok = min(o / COLS, A.n - 1), j = min(j0 + o % COLS, A.d_out - 1);
+    swj[q] = A.w_scale[j];
+    sc[q] = A.act_scale[tok] * swj[q];
+  }
+  const int T = NT / SLOTS;  // compensation threads per token
+  const int ci = tid / T, cu = tid - ci * T;
+  const int cquad = cu % (COLS / 4), cslice = cu / (COLS / 4);
+  // a few entries are worth holding through the main loop, many are not
+  constexpr bool PRE = B <= 4;
+  CompEntries<B> ce0;
+  if (PRE && fused && ci < A.n) comp_entries<B>(A, ci, cslice, NSLICES, ce0);
   const GemvAddr ad = gemv_addr<CW>(A, j0);
-  BlockCodes<CW, TF> first;
-  if (wave < nblk) load_block_buf<CW, TF>(ad, wave, first);
-  build_tables<WIDE_R, DEC_R>(A.lut, cbs, tabW, tabA, tid, NW * 64);
+  BlockCodes<CW, TF> buf[PF];
+#pragma unroll
+  for (int d = 0; d < PF; ++d)
+    if (wave + d * NW < nblk) load_block_buf<CW, TF>(ad, wave + d * NW, buf[d]);
+  dt.store(tab, tid);
+  __syncthreads();  // decode table
 
   float4_t acc[CW][TF];
 #pragma unroll
   for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
-
+  bool tok_ok[TF];
+#pragma unroll
+  for (int f = 0; f < TF; ++f) tok_ok[f] = 16 * f + (lane & 15) < A.n;
+  const char* tb = reinterpret_cast<const char*>(tab);
+  const uint32_t l4w = (uint32_t)(lane & 31) * 4u, l4a = l4w + 128u;
   if (wave < nblk)
-    gemv_blocks<CW, TF, PF, FULLK>(A, ad, wave, nblk, NW, first, tabW, tabA, acc);
-  __syncthreads();  // every wave is done with tabW: reuse it for the reduction
-  float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tabW);
-  float* part = reinterpret_cast<float*>(tabW) + RED_FLOATS;  // compensation partials
-  float* cwtab = part + PART_FLOATS;                           // C_W, one copy per lane
+    gemv_blocks<CW, TF, PF, FULLK>(KB, ad, wave, nblk, NW, buf, tb, l4w, l4a, tok_ok, acc);
+
+  // outlier branch: reads only rows 0..15 of the table (weight centroids),
+  // which nothing overwrites before the next barrier
+  float cacc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (fused && ci < A.n)
+    tile_compensation<COLS, B, PRE>(A, ad, j0, tb, NSLICES, ci, cquad, cslice, ce0, cacc);
+  __syncthreads();  // every wave is done with the table: reuse it for the reduction
+  float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tab);
+  float* part = reinterpret_cast<float*>(tab) + RED_FLOATS;  // compensation partials
 #pragma unroll
   for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) red[wave][c * TF + f][lane] = acc[c][f];
-  // outlier branch, after the main loop so its weight rows are warm in L2
-  if (fused) {
-    for (int q = tid; q < 16 * 64; q += NW * 64) cwtab[q] = h2f(cbs[0][q >> 6]);
-    __syncthreads();
-    // entries in flight per thread: about a token's share per slice, <= 16
-    if (2 * A.k <= 4 * NSLICES)
-      tile_compensation<COLS, 4>(A, ad, j0, cwtab, part, NSLICES, tid, NW * 64, SLOTS);
-    else
-      tile_compensation<COLS, 16>(A, ad, j0, cwtab, part, NSLICES, tid, NW * 64, SLOTS);
+  if (fused && ci < SLOTS) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) part[(ci * NSLICES + cslice) * COLS + 4 * cquad + c] = cacc[c];
   }
   __syncthreads();
 
-  const int g = lane >> 4, tc = lane & 15;
-  for (int t = wave; t < CW * TF; t += NW) {
-    float4_t v = red[0][t][lane];
+  // ---- epilogue: thread -> output (token o / COLS, column j0 + o % COLS)
+  const float* redf = reinterpret_cast<const float*>(tab);
 #pragma unroll
-    for (int w = 1; w < NW; ++w) v += red[w][t][lane];
-    const int c = t / TF, f = t % TF;
-    const int tok = 16 * f + tc;
+  for (int q = 0; q < EPT; ++q) {
+    const int o = tid + NT * q;
+    const int tok = o / COLS, jl = o % COLS;
+    const int j = j0 + jl;
+    if (o >= SLOTS * COLS || tok >= A.n || j >= A.d_out) continue;
+    const int c = jl % CW, mrow = jl / CW;
+    const int t = c * TF + (tok >> 4);
+    const int ln = (mrow >> 2) * 16 + (tok & 15);
+    float v = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int jl = CW * (4 * g + r) + c;
-      const int j = j0 + jl;
-      if (tok >= A.n || j >= A.d_out) continue;
-      float* dst = A.y + (size_t)tok * A.d_out + j;
-      float val = A.act_scale[tok] * A.w_scale[j] * v[r];
-      if (fused) {
-        float cs = 0.0f;
-        for (int sl = 0; sl < NSLICES; ++sl) cs += part[(tok * NSLICES + sl) * COLS + jl];
-        val += A.w_scale[j] * cs;
-      }
-      *dst = A.accumulate ? *dst + val : val;
+    for (int w = 0; w < NW; ++w) v += redf[((w * CW * TF + t) * 64 + ln) * 4 + (mrow & 3)];
+    float val = sc[q] * v;
+    if (fused) {
+      float cs = 0.0f;
+      for (int sl = 0; sl < NSLICES; ++sl) cs += part[(tok * NSLICES + sl) * COLS + jl];
+      val += swj[q] * cs;
     }
+    float* dst = A.y + (size_t)tok * A.d_out + j;
+    *dst = A.accumulate ? *dst + val : val;
   }
 }
 
@@ -372,15 +396,6 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 // offset of either is byte * 256 + (lane mod 32) * 4 (+ 128 for activations)
 // - one v_perm_b32 per byte, and 32 lanes read 32 different banks.
 // ----------------------------------------------------------------------------
-__device__ __forceinline__ half8_t expand_dual(uint32_t w, const char* tab, uint32_t lane4) {
-  uint4_t r;
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const uint32_t off = __builtin_amdgcn_perm(w, lane4, 0x0C0C0000u | ((4u + b) << 8));
-    r[b] = *reinterpret_cast<const uint32_t*>(tab + off);
-  }
-  return __builtin_bit_cast(half8_t, r);
-}
 
 // Per-lane byte offsets of the codes of one wave (block 0); a block's offset
 // travels in an SGPR.  Reads past either tensor return 0.  Weight lane m of
@@ -439,8 +454,7 @@ __device__ __forceinline__ void mma_block_pf(int blk, int KB, const BlockCodes<C
 template <int CW, int TF, int WX, int WY, bool FULLK>
 __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, int ncx, int nty) {
   constexpr int NT = WX * WY * 64;
-  __shared__ uint32_t tab[256 * 64];  // 64 KiB: both pair tables
-  __shared__ uint16_t cbs[2][16];
+  __shared__ uint32_t tab[256 * 64];  // 64 KiB dual decode table
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, m = lane & 15;
 
@@ -464,16 +478,13 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
     ad.aoff[f] = ((uint32_t)(tok0 + 16 * f + m) * (uint32_t)KB + 4u * g) * 4u;
   ad.wblk = 16u * (uint32_t)A.d_out * 4u;
 
-  // first block's loads in flight while the tables are built
+  // codebook entries first, then the first block's codes: building the table
+  // waits only for the codebook
+  DualTableLoader<NT> dt;
+  dt.load(A.lut, tid);
   BlockCodes<CW, TF> buf[2];
   load_block_pf<CW, TF>(ad, 0, buf[0]);
-  if (tid < 16) cbs[0][tid] = A.lut->cb_wgt[tid];
-  else if (tid < 32) cbs[1][tid - 16] = A.lut->cb_act[tid - 16];
-  __syncthreads();
-  for (int e = tid; e < 256 * 64; e += NT) {
-    const int byte = e >> 6, side = (e >> 5) & 1;  // 0: weights, 1: activations
-    tab[e] = (uint32_t)cbs[side][byte & 15] | ((uint32_t)cbs[side][byte >> 4] << 16);
-  }
+  dt.store(tab, tid);
   __syncthreads();
 
   float4_t acc[CW][TF];
@@ -541,16 +552,27 @@ static void launch_prefill(const GemmArgs& a, hipStream_t s) {
                        dim3(WX * WY * 64), 0, s, a, ncx, nty);
 }
 
-template <int CW, int TF, int NW>
-static void launch_gemv(const GemmArgs& a, hipStream_t s) {
+template <int CW, int TF, int NW, int B>
+static void launch_gemv_b(const GemmArgs& a, hipStream_t s) {
   const int ntiles = (a.d_out + 16 * CW - 1) / (16 * CW);
   constexpr int PF = 2;  // blocks in flight per wave
   if ((a.d_in / 8) % 16 == 0)
-    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true>), dim3(ntiles), dim3(NW * 64), 0,
-                       s, a, ntiles);
-  else
-    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false>), dim3(ntiles), dim3(NW * 64),
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true, B>), dim3(ntiles), dim3(NW * 64),
                        0, s, a, ntiles);
+  else
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false, B>), dim3(ntiles),
+                       dim3(NW * 64), 0, s, a, ntiles);
+}
+
+// Outlier entries in flight per compensation thread: about a token's share of
+// one slice, at most 8.
+template <int CW, int TF, int NW>
+static void launch_gemv(const GemmArgs& a, hipStream_t s) {
+  constexpr int NSLICES = (NW * 64 / (16 * TF)) / (4 * CW);
+  if (2 * a.k <= 4 * NSLICES)
+    launch_gemv_b<CW, TF, NW, 4>(a, s);
+  else
+    launch_gemv_b<CW, TF, NW, 8>(a, s);
 }
 
 template <int TF>

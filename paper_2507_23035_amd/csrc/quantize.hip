@@ -1,356 +1,443 @@
 // Per-token activation quantization with dynamic top-k outlier detection.
 //
-// One workgroup per token.  The token is staged in LDS once; then
+// One workgroup per token computes
 //   * the per-token scale t = absmax (Sec. III-A),
 //   * the cluster index of every channel by the mid-point boundary rule of the
 //     Clustering Unit (Sec. IV-C): a = #{c : x >= fp32(t * b_c)},
 //   * the k largest and k smallest channels (the job of the Orizuru engine,
 //     Sec. IV-D) with ties to the lower channel, in pop order,
 //   * the residual of every listed outlier (Sec. III-C2).
-// The top-k is a two-pass radix select on order-preserving 16-bit keys
-// (-0 folded into +0) shared by the max and min lists: pass 1 histograms the
-// high byte while the token is staged, pass 2 the low byte inside the boundary
-// bucket, which fixes the
-// threshold key T and the count G of keys strictly beyond it.  Keys beyond T
-// (G < k of them) are ranked among themselves, one lane per candidate; keys
-// equal to T are taken in channel order, which one block-wide scan provides.  The
-// paper's tree pops in exactly this order; the select needs two histogram
-// passes instead of k pops.
 //
-// Each thread owns a contiguous run of channels (a multiple of 8, read from
-// LDS as 16-byte vectors), so channel order inside a tie is the order of the
-// block scan; the pass that counts ties also writes the run's cluster codes.  Small batches use 512-thread workgroups (short runs, latency
-// bound), large batches 256-thread ones (many tokens per CU).
+// Every fp16 value x becomes an order-preserving 16-bit key (-0 folded into
+// +0).  Each thread holds VR runs of 8 consecutive channels in registers, so
+// thread order is channel order; the raw token is also staged in LDS for the
+// few channels the lists take.
+//
+// Clustering in key space: an fp16 x satisfies x >= P (P fp32) exactly when
+// x >= Q, Q the smallest fp16 (or +-inf) not below P, i.e. when
+// key(x) >= key(Q).  The 15 boundary keys are derived from the fp32 boundaries
+// once per token, so the index is the number of boundary keys <= key(x): a
+// 256-entry table over the key's high byte gives the count at the start of
+// that bucket and the low byte of the first boundary inside it.  Unless two
+// centroids are very close, at most one boundary falls inside a bucket; keys
+// in a bucket with more take the full 15-compare count.  This is the fp32 rule
+// of the oracle, bit for bit, at one LDS lookup per channel.
+//
+// Top-k is a two-level radix select on the keys shared by the max and min
+// lists: a histogram of the high byte fixes the bucket holding the k-th
+// largest (smallest) key, a histogram of the low byte inside it the exact
+// threshold key T and the count G < k of keys strictly beyond it.  Keys equal
+// to T are taken in channel order (a block-wide exclusive count gives each its
+// rank); the G keys beyond T are ranked among themselves.  The paper's trees
+// pop in exactly this order; the select replaces k sequential pops by two
+// histogram passes.  Every wave scans the histograms itself (DPP prefix sums),
+// so a level costs one barrier, and only the keys at or beyond a threshold
+// are visited after the counts.
 #include "common.h"
 
 namespace oasis {
 
-template <int NT>
-struct QuantSmem {
-  uint32_t hist1[256];
-  uint16_t bucket[256];  // per high byte of the key: first | last cluster index << 8
-  float P[16];           // scaled boundaries
-  uint32_t hist2_max[256];
-  uint32_t hist2_min[256];
-  float ca[16];
-  uint64_t scan_tmp[3][NT / 64];  // one per block scan: no barrier between reuses
-  uint32_t red_tmp[NT / 64];
-  uint32_t ctl[8];    // B1/G1 of the max and min lists, then T/G of both
+struct __align__(16) QuantSmem {
+  uint32_t hist1[256];     // high byte of the key
+  uint32_t hist2[2][256];  // low byte inside the max / min boundary bucket
+  uint16_t bucket[256];    // first index | inside count << 4 | low byte << 8
+  float ca[16];            // C_A in fp32
+  uint32_t wmax[16];       // per-wave absmax
+  uint32_t wtot[2][16];    // per-wave totals of the two packed count pairs
 };
 
-// Dynamic LDS after the fixed part: token (2 B per channel, 16-byte padded),
-// max candidates (4 B each), min candidates (4 B + a 4-byte duplicate flag).
+// Dynamic LDS after the fixed part: the token (2 B per channel), then G < k
+// candidates per list, each a sort key and its residual (max list, then min
+// list), padded to a multiple of 4.
 static size_t dyn_bytes(int d_in, int k) {
-  size_t xs = ((size_t)d_in * 2 + 15) / 16 * 16;
-  return xs + (size_t)k * 12;
+  const size_t k4 = ((size_t)k + 3) & ~(size_t)3;
+  return (size_t)d_in * 2 + 16 * k4;
 }
 
-size_t quantize_lds_bytes(int d_in, int k) {
-  return sizeof(QuantSmem<1024>) + dyn_bytes(d_in, k);
-}
+size_t quantize_lds_bytes(int d_in, int k) { return sizeof(QuantSmem) + dyn_bytes(d_in, k); }
 
+// fp16 bits -> order-preserving key; -0 and +0 share key 0x8000.
 __device__ __forceinline__ uint32_t ord_key(uint32_t bits) {
-  if (bits == 0x8000u) bits = 0;  // -0 == +0
-  return (bits & 0x8000u) ? (~bits & 0xFFFFu) : (bits | 0x8000u);
+  if (bits == 0x8000u) bits = 0;
+  return (bits & 0x8000u) ? (bits ^ 0xFFFFu) : (bits | 0x8000u);
 }
 
-template <int NT>
-__device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* tmp) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = max(v, (uint32_t)__shfl_xor(v, off, 64));
-  if (lane == 0) tmp[wid] = v;
-  __syncthreads();
-  uint32_t r = 0;
-#pragma unroll
-  for (int w = 0; w < NT / 64; ++w) r = max(r, tmp[w]);
-  return r;  // `tmp` is not reused: no trailing barrier
-}
-
-// CLUSTER: write scale and codes.  TOPK: write outlier lists and residuals.
-template <int NT, bool CLUSTER, bool TOPK>
+template <int NT, int VR, bool CLUSTER, bool TOPK>
 __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
 #pragma clang fp contract(off)
+  constexpr int NW = NT / 64;
+  static_assert(NT >= 256 && NW <= 16, "256..1024 threads");
+  static_assert(VR >= 1 && 8 * VR <= 64, "at most 64 channels per thread");
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  QuantSmem<NT>& S = *reinterpret_cast<QuantSmem<NT>*>(smem_raw);
-  const int d_in = A.d_in, k = A.k;
-  unsigned char* dyn = smem_raw + sizeof(QuantSmem<NT>);
-  uint16_t* xs = reinterpret_cast<uint16_t*>(dyn);
-  const size_t xs_bytes = ((size_t)d_in * 2 + 15) / 16 * 16;
-  uint32_t* cand_max = reinterpret_cast<uint32_t*>(dyn + xs_bytes);
-  uint32_t* cand_min = cand_max + k;
-  uint32_t* cand_dup = cand_min + k;
-
-  const int tid = threadIdx.x;
+  QuantSmem& S = *reinterpret_cast<QuantSmem*>(smem_raw);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int i = blockIdx.x;
-  const uint16_t* xrow = A.x + (size_t)i * d_in;
-  const uint4* xs4 = reinterpret_cast<const uint4*>(xs);
+  const int d_in = A.d_in, k = A.k, nvec = d_in >> 3;
+  const bool topk = TOPK && k > 0;  // uniform
+  const uint32_t k4 = ((uint32_t)k + 3u) & ~3u;
+  uint16_t* xs = reinterpret_cast<uint16_t*>(smem_raw + sizeof(QuantSmem));
+  uint32_t* cmax = reinterpret_cast<uint32_t*>(xs + d_in);  // d_in % 8 == 0: 16-byte aligned
+  float* rmax = reinterpret_cast<float*>(cmax + k4);
+  uint32_t* cmin = reinterpret_cast<uint32_t*>(rmax + k4);
+  float* rmin = reinterpret_cast<float*>(cmin + k4);
 
-  const bool topk = TOPK && k > 0;                 // uniform across the block
-  const bool fused_cluster = CLUSTER && topk;      // codes written by the count pass
+  // ---- the token into registers (runs tid*VR .. tid*VR + VR - 1)
+  uint4 xv[VR];
+  const uint4* xrow = reinterpret_cast<const uint4*>(A.x + (size_t)i * d_in);
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    const int v = tid * VR + u;
+    xv[u] = v < nvec ? xrow[v] : make_uint4(0u, 0u, 0u, 0u);
+  }
   if (tid < 256) {
     S.hist1[tid] = 0;
-    S.hist2_max[tid] = 0;
-    S.hist2_min[tid] = 0;
+    S.hist2[0][tid] = 0;
+    S.hist2[1][tid] = 0;
   }
   if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
-  if (tid < 8) S.ctl[tid] = 0;
-  __syncthreads();  // histograms cleared
+  __syncthreads();  // histograms cleared, C_A staged
 
-  // ---- stage the token in LDS (coalesced 16-byte loads), find absmax and
-  // build the histogram of the key's high byte (pass 1 of the top-k select)
+  // keys, two per word (even channel low)
+  uint32_t key[VR][4];
   uint32_t amax = 0;
-  const int nvec = d_in / 8;
-  for (int v = tid; v < nvec; v += NT) {
-    uint4 q = reinterpret_cast<const uint4*>(xrow)[v];
-    reinterpret_cast<uint4*>(xs)[v] = q;
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-    for (int h = 0; h < 4; ++h) amax = max(amax, max(w[h] & 0x7FFFu, (w[h] >> 16) & 0x7FFFu));
-    if (topk) {
+  for (int u = 0; u < VR; ++u) {
+    const bool live = tid * VR + u < nvec;
+    const uint32_t w[4] = {xv[u].x, xv[u].y, xv[u].z, xv[u].w};
 #pragma unroll
-      for (int h = 0; h < 8; ++h)
-        atomicAdd(&S.hist1[ord_key((w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu) >> 8], 1u);
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = w[q] & 0xFFFFu, hi = w[q] >> 16;
+      key[u][q] = ord_key(lo) | (ord_key(hi) << 16);
+      amax = max(amax, max(lo & 0x7FFFu, hi & 0x7FFFu));
+    }
+    if (topk && live) {
+      reinterpret_cast<uint4*>(xs)[tid * VR + u] = xv[u];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        atomicAdd(&S.hist1[(key[u][q] >> 8) & 0xFFu], 1u);
+        atomicAdd(&S.hist1[key[u][q] >> 24], 1u);
+      }
     }
   }
-  amax = block_max<NT>(amax, S.red_tmp);  // barrier: xs and hist1 complete
+  amax = wave_max(amax);
+  if (lane == 0) S.wmax[wave] = amax;
+  __syncthreads();  // absmax partials, level-1 histogram
 
+#pragma unroll
+  for (int w = 0; w < NW; ++w) amax = max(amax, S.wmax[w]);
   const float t = (A.scale_mode == OASIS_SCALE_NONE) ? 1.0f : h2f((uint16_t)amax);
   if (CLUSTER && tid == 0) A.act_scale[i] = t;
 
-  // ---- scaled cluster boundaries P_c = fp32(t * b_c), b_c = (c_c + c_{c+1}) * 0.5
+  // ---- boundary keys: lane c computes key(Q_c), Q_c = the smallest fp16 not
+  // below P_c = fp32(t * b_c), b_c = fp32(C_A[c] + C_A[c+1]) * 0.5
   const int nb = (1 << A.b_a) - 1;
-  float P[15];
-#pragma unroll
-  for (int c = 0; c < 15; ++c) {
-    const float bc = (S.ca[c] + S.ca[c + 1]) * 0.5f;
-    P[c] = t * bc;
+  uint32_t kq_lane = 0x10000u;  // above every key: boundaries past the last one
+  if (lane < nb) {
+    const float bc = (S.ca[lane] + S.ca[lane + 1]) * 0.5f;
+    const float P = t * bc;
+    const _Float16 h = (_Float16)P;  // round to nearest even
+    kq_lane = ord_key(__builtin_bit_cast(uint16_t, h)) + ((float)h < P ? 1u : 0u);
   }
-  auto cluster = [&](float x) -> uint32_t {
+  uint32_t KQ[15];
+#pragma unroll
+  for (int c = 0; c < 15; ++c) KQ[c] = (uint32_t)__builtin_amdgcn_readlane((int)kq_lane, c);
+  // cluster index by the full count
+  auto code_full = [&](uint32_t kk) -> uint32_t {
     uint32_t a = 0;
 #pragma unroll
-    for (int c = 0; c < 15; ++c) a += (c < nb && x >= P[c]) ? 1u : 0u;
+    for (int c = 0; c < 15; ++c) a += kk >= KQ[c] ? 1u : 0u;
     return a;
   };
-
-  // ---- cluster index of every channel, packed 8 per word.  The index is
-  // monotone in the order-preserving key, so the keys sharing a high byte span
-  // a range [first, last] of indices; only the few buckets a boundary crosses
-  // need compares: a = first + #{first <= c < last : x >= P_c}.  The table is
-  // visible after the next barrier.
-  if (CLUSTER) {
-    if (tid < 16) S.P[tid] = tid < nb ? P[tid < 15 ? tid : 14] : 0.0f;
-    if (tid < 256) {
-      auto bits_of = [](uint32_t key) -> uint16_t {  // inverse of ord_key
-        return (uint16_t)((key & 0x8000u) ? (key & 0x7FFFu) : (~key & 0xFFFFu));
-      };
-      const uint32_t lo = cluster(h2f(bits_of((uint32_t)tid << 8)));
-      const uint32_t hi = cluster(h2f(bits_of(((uint32_t)tid << 8) | 0xFFu)));
-      S.bucket[tid] = (uint16_t)(lo | (hi << 8));
-    }
-  }
-  auto code8 = [&](const uint4& q) -> uint32_t {
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-    uint32_t packed = 0;
+  if (tid < 256) {  // bucket tid: keys tid*256 .. tid*256 + 255
+    const uint32_t base = (uint32_t)tid << 8;
+    uint32_t first = 0, upto = 0;
 #pragma unroll
-    for (int h = 0; h < 8; ++h) {
-      const uint32_t bits = (w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
-      const uint32_t e = S.bucket[ord_key(bits) >> 8];
-      uint32_t a = e & 0xFFu;
-      const uint32_t last = e >> 8;
-      if (a < last) {  // a boundary lies inside this bucket
-        const float x = h2f((uint16_t)bits);
-        uint32_t add = 0;
-        for (uint32_t c = a; c < last; ++c) add += x >= S.P[c] ? 1u : 0u;
-        a += add;
-      }
-      packed |= a << (4 * h);
+    for (int c = 0; c < 15; ++c) {
+      first += KQ[c] <= base ? 1u : 0u;
+      upto += KQ[c] <= base + 255u ? 1u : 0u;
     }
-    return packed;
+    // KQ[first], the first boundary inside if any, from lane `first` of this wave
+    const uint32_t kf = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(first << 2), (int)kq_lane);
+    S.bucket[tid] = (uint16_t)(first | ((upto - first) << 4) | ((kf & 0xFFu) << 8));
+  }
+  // cluster index of one key from the table (visible after the next barrier);
+  // `multi` flags a bucket with two or more boundaries (then use code_full)
+  auto code_fast = [&](uint32_t kk, bool& multi) -> uint32_t {
+    const uint32_t e = S.bucket[kk >> 8];
+    const uint32_t nin = (e >> 4) & 15u;
+    multi |= nin > 1u;
+    return (e & 15u) + ((nin != 0u && (kk & 0xFFu) >= (e >> 8)) ? 1u : 0u);
+  };
+  auto residual_of = [&](uint32_t kk, uint32_t bits) -> float {
+    bool multi = false;
+    uint32_t a = code_fast(kk, multi);
+    if (multi) a = code_full(kk);
+    const float x = h2f((uint16_t)bits);
+    return x - t * S.ca[a];  // t * C_A exact: a product of two fp16 values
   };
   uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
+  auto store_codes = [&]() {
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      const int v = tid * VR + u;
+      if (v < nvec) {
+        bool multi = false;
+        uint32_t packed = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          packed |= code_fast(key[u][q] & 0xFFFFu, multi) << (8 * q);
+          packed |= code_fast(key[u][q] >> 16, multi) << (8 * q + 4);
+        }
+        if (multi) {
+          packed = 0;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            packed |= (code_full(key[u][q] & 0xFFFFu) << (8 * q)) |
+                      (code_full(key[u][q] >> 16) << (8 * q + 4));
+        }
+        arow[v] = packed;
+      }
+    }
+  };
   if (!topk) {
     if (CLUSTER) {
-      __syncthreads();
-      for (int v = tid; v < nvec; v += NT) arow[v] = code8(xs4[v]);  // coalesced
+      __syncthreads();  // bucket table
+      store_codes();
     }
     return;
   }
 
-  // contiguous run of channels owned by this thread, in 8-channel vectors
-  const int vpt = (nvec + NT - 1) / NT;
-  const int v0 = min(nvec, tid * vpt), v1 = min(nvec, v0 + vpt);
-
-  // ---- pass 1 (histogram built while staging): the high-byte buckets that
-  // hold the k-th largest and the k-th smallest key
+  // ---- level 1: the high-byte buckets holding the k-th largest and k-th
+  // smallest key (each wave scans the histogram itself)
+  uint32_t B1max, G1max, B1min, G1min;
   {
-    const uint32_t h = tid < 256 ? S.hist1[tid] : 0u;
-    const uint32_t pre = (uint32_t)block_scan64<NT>(h, S.scan_tmp[0]);  // keys with byte <= tid
-    if (tid < 256) {
-      const uint32_t suf_excl = (uint32_t)d_in - pre;  // keys with high byte > tid
-      if (suf_excl < (uint32_t)k && (uint32_t)k <= suf_excl + h) {
-        S.ctl[0] = tid;
-        S.ctl[1] = suf_excl;
-      }
-      const uint32_t pre_excl = pre - h;
-      if (pre_excl < (uint32_t)k && (uint32_t)k <= pre) {
-        S.ctl[2] = tid;
-        S.ctl[3] = pre_excl;
-      }
-    }
-  }
-  __syncthreads();
-  const uint32_t B1max = S.ctl[0], G1max = S.ctl[1], B1min = S.ctl[2], G1min = S.ctl[3];
-
-  // ---- pass 2: low byte inside the two boundary buckets
-  for (int v = v0; v < v1; ++v) {
-    const uint4 q = xs4[v];
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    const uint4 h = *reinterpret_cast<const uint4*>(&S.hist1[4 * lane]);
+    const uint32_t hs[4] = {h.x, h.y, h.z, h.w};
+    const uint32_t sum = h.x + h.y + h.z + h.w;
+    uint32_t pre = wave_incl_scan(sum) - sum;  // keys in buckets below 4*lane
+    uint32_t fmax = 0, gmax = 0, fmin = 0, gmin = 0;
+    bool hit_max = false, hit_min = false;
 #pragma unroll
-    for (int h = 0; h < 8; ++h) {
-      const uint32_t key = ord_key((w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu);
-      if ((key >> 8) == B1max) atomicAdd(&S.hist2_max[key & 255u], 1u);
-      if ((key >> 8) == B1min) atomicAdd(&S.hist2_min[key & 255u], 1u);
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t below = pre, upto = pre + hs[q];
+      const uint32_t above = (uint32_t)d_in - upto;  // keys in buckets above
+      const bool hm = above < (uint32_t)k && (uint32_t)k <= above + hs[q];
+      const bool hn = below < (uint32_t)k && (uint32_t)k <= upto;
+      fmax = hm ? (uint32_t)(4 * lane + q) : fmax;
+      gmax = hm ? above : gmax;
+      fmin = hn ? (uint32_t)(4 * lane + q) : fmin;
+      gmin = hn ? below : gmin;
+      hit_max |= hm;
+      hit_min |= hn;
+      pre = upto;
+    }
+    // exactly one bucket holds each threshold; the guard keeps lanes < 64
+    const int lm = __builtin_ctzll(__ballot(hit_max) | (1ull << 63));
+    const int ln = __builtin_ctzll(__ballot(hit_min) | (1ull << 63));
+    B1max = __builtin_amdgcn_readlane(fmax, lm);
+    G1max = __builtin_amdgcn_readlane(gmax, lm);
+    B1min = __builtin_amdgcn_readlane(fmin, ln);
+    G1min = __builtin_amdgcn_readlane(gmin, ln);
+  }
+  // ---- level 2: low bytes inside the two boundary buckets
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    if (tid * VR + u < nvec) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
+          if ((kk >> 8) == B1max) atomicAdd(&S.hist2[0][kk & 0xFFu], 1u);
+          if ((kk >> 8) == B1min) atomicAdd(&S.hist2[1][kk & 0xFFu], 1u);
+        }
+      }
     }
   }
-  __syncthreads();
+  __syncthreads();  // level-2 histograms, bucket table
+
+  uint32_t Tmax, Gmax, Tmin, Gmin;
   {
-    const uint32_t hm = tid < 256 ? S.hist2_max[tid] : 0u;
-    const uint32_t hn = tid < 256 ? S.hist2_min[tid] : 0u;
-    const uint64_t pre = block_scan64<NT>(((uint64_t)hn << 32) | hm, S.scan_tmp[1]);
-    const uint32_t pre_m = (uint32_t)pre, pre_n = (uint32_t)(pre >> 32);
-    if (tid < 256) {
-      const uint32_t kk = (uint32_t)k - G1max;
-      // keys of the max list's boundary bucket with a low byte above tid
-      const uint32_t suf_excl = S.hist1[B1max] - pre_m;
-      if (suf_excl < kk && kk <= suf_excl + hm) {
-        S.ctl[4] = (B1max << 8) | tid;  // threshold key of the max list
-        S.ctl[5] = G1max + suf_excl;    // keys strictly greater
-      }
-      const uint32_t kn = (uint32_t)k - G1min;
-      const uint32_t pre_excl = pre_n - hn;
-      if (pre_excl < kn && kn <= pre_n) {
-        S.ctl[6] = (B1min << 8) | tid;  // threshold key of the min list
-        S.ctl[7] = G1min + pre_excl;    // keys strictly smaller
-      }
+    const uint4 hm = *reinterpret_cast<const uint4*>(&S.hist2[0][4 * lane]);
+    const uint4 hn = *reinterpret_cast<const uint4*>(&S.hist2[1][4 * lane]);
+    const uint32_t ms[4] = {hm.x, hm.y, hm.z, hm.w}, ns[4] = {hn.x, hn.y, hn.z, hn.w};
+    const uint32_t summ = hm.x + hm.y + hm.z + hm.w, sumn = hn.x + hn.y + hn.z + hn.w;
+    uint32_t prem = wave_incl_scan(summ) - summ, pren = wave_incl_scan(sumn) - sumn;
+    const uint32_t totm = S.hist1[B1max];
+    const uint32_t kk = (uint32_t)k - G1max, kn = (uint32_t)k - G1min;
+    uint32_t tm = 0, gm = 0, tn = 0, gn = 0;
+    bool hit_max = false, hit_min = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t uptom = prem + ms[q];
+      const uint32_t above = totm - uptom;  // keys of the bucket with a higher low byte
+      const bool hmq = above < kk && kk <= above + ms[q];
+      tm = hmq ? ((B1max << 8) | (uint32_t)(4 * lane + q)) : tm;
+      gm = hmq ? G1max + above : gm;
+      const uint32_t upton = pren + ns[q];
+      const bool hnq = pren < kn && kn <= upton;
+      tn = hnq ? ((B1min << 8) | (uint32_t)(4 * lane + q)) : tn;
+      gn = hnq ? G1min + pren : gn;
+      hit_max |= hmq;
+      hit_min |= hnq;
+      prem = uptom;
+      pren = upton;
     }
+    const int lm = __builtin_ctzll(__ballot(hit_max) | (1ull << 63));
+    const int ln = __builtin_ctzll(__ballot(hit_min) | (1ull << 63));
+    Tmax = __builtin_amdgcn_readlane(tm, lm);
+    Gmax = __builtin_amdgcn_readlane(gm, lm);
+    Tmin = __builtin_amdgcn_readlane(tn, ln);
+    Gmin = __builtin_amdgcn_readlane(gn, ln);
   }
-  __syncthreads();
   // G < k holds by construction; the clamp only keeps every index in bounds.
-  const uint32_t Tmax = S.ctl[4], Tmin = S.ctl[6];
-  const uint32_t Gmax = min(S.ctl[5], (uint32_t)k - 1u);
-  const uint32_t Gmin = min(S.ctl[7], (uint32_t)k - 1u);
+  Gmax = min(Gmax, (uint32_t)k - 1u);
+  Gmin = min(Gmin, (uint32_t)k - 1u);
   const uint32_t need_max = (uint32_t)k - Gmax, need_min = (uint32_t)k - Gmin;
 
-  // ---- per-thread counts, in channel order, of (max-list ties, min-list ties,
-  // keys above Tmax, keys below Tmin), 16 bits each: one 64-bit block scan
-  // gives every thread its tie ranks and its candidate slots.  (Exclusive
-  // prefixes stay below 2^16 because d_in <= 65536.)  The same pass writes the
-  // cluster codes of the thread's run.
-  uint64_t cnt = 0;
-  for (int v = v0; v < v1; ++v) {
-    const uint4 q = xs4[v];
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  // ---- codes; per-thread counts in channel order of (max-list ties, min-list
+  // ties) and (keys above Tmax, keys below Tmin), 16 bits each; the keys at
+  // or beyond a threshold (the only ones a list can take)
+  if (CLUSTER) store_codes();
+  uint32_t c_tie = 0, c_out = 0;
+  uint64_t special = 0;
 #pragma unroll
-    for (int h = 0; h < 8; ++h) {
-      const uint32_t key = ord_key((w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu);
-      cnt += (uint64_t)(key == Tmax) | ((uint64_t)(key == Tmin) << 16) |
-             ((uint64_t)(key > Tmax) << 32) | ((uint64_t)(key < Tmin) << 48);
+  for (int u = 0; u < VR; ++u) {
+    if (tid * VR + u < nvec) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
+          c_tie += (kk == Tmax ? 1u : 0u) + (kk == Tmin ? 0x10000u : 0u);
+          c_out += (kk > Tmax ? 1u : 0u) + (kk < Tmin ? 0x10000u : 0u);
+          special |= (uint64_t)((kk >= Tmax) | (kk <= Tmin)) << (8 * u + 2 * q + hh);
+        }
+      }
     }
-    if (fused_cluster) arow[v] = code8(q);
   }
-  const uint64_t excl = block_scan64<NT>(cnt, S.scan_tmp[2]) - cnt;
-  uint32_t rank_max = (uint32_t)(excl & 0xFFFFu), rank_min = (uint32_t)((excl >> 16) & 0xFFFFu);
-  uint32_t slot_max = (uint32_t)((excl >> 32) & 0xFFFFu), slot_min = (uint32_t)(excl >> 48);
+  // block-wide exclusive prefix: wave scan, wave totals through LDS.  A
+  // prefix counts keys before this thread, < 65536, so the fields never carry.
+  const uint32_t inc_tie = wave_incl_scan(c_tie), inc_out = wave_incl_scan(c_out);
+  if (lane == 63) {
+    S.wtot[0][wave] = inc_tie;
+    S.wtot[1][wave] = inc_out;
+  }
+  // pad the candidate lists to a multiple of 4 with entries that never rank
+  // first (sort keys are compared after XOR with 0 for the max list and with
+  // ~0 for the min list, which turns a pad into 0)
+  if (tid < 4) {
+    if (Gmax + (uint32_t)tid < k4) cmax[Gmax + tid] = 0u;
+    if (Gmin + (uint32_t)tid < k4) cmin[Gmin + tid] = 0xFFFFFFFFu;
+  }
+  __syncthreads();  // wave totals
+  uint32_t ex_tie = inc_tie - c_tie, ex_out = inc_out - c_out;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if (w < wave) {
+      ex_tie += S.wtot[0][w];
+      ex_out += S.wtot[1][w];
+    }
+  }
+  uint32_t rank_max = ex_tie & 0xFFFFu, rank_min = ex_tie >> 16;
+  uint32_t slot_max = ex_out & 0xFFFFu, slot_min = ex_out >> 16;
 
   const size_t krow = (size_t)i * k;
   const size_t rrow = (size_t)i * 2 * k;
-  auto residual_of = [&](float x) -> float {
-    const float xhat = t * S.ca[cluster(x)];  // exact: a product of two fp16 values
-    return x - xhat;
-  };
-
-  // ---- collect: direct output for threshold ties, candidate slots for the rest
-  for (int v = v0; v < v1; ++v) {
-    const uint4 q = xs4[v];
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int h = 0; h < 8; ++h) {
-      const uint32_t bits = (w[h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
-      const uint32_t key = ord_key(bits);
-      const int p = 8 * v + h;
-      bool in_max = key > Tmax;
-      if (key == Tmax) {
-        in_max = rank_max < need_max;
-        if (in_max) {
-          const uint32_t pos = Gmax + rank_max;
-          A.max_idx[krow + pos] = p;
-          A.residual[rrow + pos] = residual_of(h2f((uint16_t)bits));
-        }
-        ++rank_max;
-      } else if (in_max) {
-        if (slot_max < Gmax) cand_max[slot_max] = (key << 16) | (0xFFFFu - (uint32_t)p);
-        ++slot_max;
-      }
-      if (key == Tmin) {
-        if (rank_min < need_min) {
-          const uint32_t pos = Gmin + rank_min;
-          A.min_idx[krow + pos] = p;
-          A.residual[rrow + k + pos] = in_max ? 0.0f : residual_of(h2f((uint16_t)bits));
-        }
-        ++rank_min;
-      } else if (key < Tmin) {
-        if (slot_min < Gmin) {
-          cand_min[slot_min] = (key << 16) | (uint32_t)p;
-          cand_dup[slot_min] = in_max ? 1u : 0u;
-        }
-        ++slot_min;
-      }
+  // ---- collect, in channel order: threshold ties go straight to their list
+  // position, the keys beyond the thresholds to candidate slots
+  while (special) {
+    const int e = __builtin_ctzll(special);
+    special &= special - 1;
+    const int p = 8 * (tid * VR + (e >> 3)) + (e & 7);
+    const uint32_t bits = xs[p];  // staged by this thread
+    const uint32_t kk = ord_key(bits);
+    const float r = residual_of(kk, bits);
+    const bool tie_max = kk == Tmax && rank_max < need_max;
+    const bool in_max = kk > Tmax || tie_max;
+    if (tie_max) {
+      A.max_idx[krow + Gmax + rank_max] = p;
+      A.residual[rrow + Gmax + rank_max] = r;
     }
+    if (kk > Tmax && slot_max < Gmax) {
+      cmax[slot_max] = (kk << 16) | (0xFFFFu - (uint32_t)p);
+      rmax[slot_max] = r;
+    }
+    if (kk == Tmin && rank_min < need_min) {
+      A.min_idx[krow + Gmin + rank_min] = p;
+      A.residual[rrow + k + Gmin + rank_min] = in_max ? 0.0f : r;
+    }
+    if (kk < Tmin && slot_min < Gmin) {
+      cmin[slot_min] = (kk << 16) | (uint32_t)p;
+      rmin[slot_min] = in_max ? 0.0f : r;
+    }
+    rank_max += kk == Tmax ? 1u : 0u;
+    slot_max += kk > Tmax ? 1u : 0u;
+    rank_min += kk == Tmin ? 1u : 0u;
+    slot_min += kk < Tmin ? 1u : 0u;
   }
-  __syncthreads();
+  __syncthreads();  // candidates
 
-  // ---- rank the candidates: one lane per candidate, counting the
-  // candidates that pop before it (broadcast LDS reads, no serial chain)
-  for (uint32_t c = tid; c < Gmax + Gmin; c += NT) {
-    if (c < Gmax) {
-      const uint32_t key = cand_max[c];
+  // ---- rank the candidates: the first half of the waves the max list, the
+  // second half the min list; each counts the candidates that pop before it
+  {
+    constexpr int HALF = NT / 2;
+    const bool is_max = wave < NW / 2;  // uniform
+    const uint32_t G = is_max ? Gmax : Gmin;
+    const uint32_t flip = is_max ? 0u : 0xFFFFFFFFu;
+    const uint32_t* cand = is_max ? cmax : cmin;
+    const uint4* c4 = reinterpret_cast<const uint4*>(cand);
+    const uint32_t nq = (G + 3u) / 4u;
+    for (uint32_t c = (uint32_t)(tid & (HALF - 1)); c < G; c += HALF) {
+      const uint32_t mine = cand[c] ^ flip;
       uint32_t rank = 0;
-#pragma unroll 4
-      for (uint32_t q = 0; q < Gmax; ++q) rank += cand_max[q] > key ? 1u : 0u;
-      const int p = (int)(0xFFFFu - (key & 0xFFFFu));
-      A.max_idx[krow + rank] = p;
-      A.residual[rrow + rank] = residual_of(h2f(xs[p]));
-    } else {
-      const uint32_t cm = c - Gmax;
-      const uint32_t key = cand_min[cm];
-      uint32_t rank = 0;
-#pragma unroll 4
-      for (uint32_t q = 0; q < Gmin; ++q) rank += cand_min[q] < key ? 1u : 0u;
-      const int p = (int)(key & 0xFFFFu);
-      A.min_idx[krow + rank] = p;
-      A.residual[rrow + k + rank] = cand_dup[cm] ? 0.0f : residual_of(h2f(xs[p]));
+#pragma unroll 2
+      for (uint32_t q = 0; q < nq; ++q) {
+        const uint4 o = c4[q];  // the same 16 bytes in every lane
+        rank += ((o.x ^ flip) > mine ? 1u : 0u) + ((o.y ^ flip) > mine ? 1u : 0u) +
+                ((o.z ^ flip) > mine ? 1u : 0u) + ((o.w ^ flip) > mine ? 1u : 0u);
+      }
+      if (is_max) {
+        A.max_idx[krow + rank] = (int)(0xFFFFu - (mine & 0xFFFFu));
+        A.residual[rrow + rank] = rmax[c];
+      } else {
+        A.min_idx[krow + rank] = (int)(~mine & 0xFFFFu);
+        A.residual[rrow + k + rank] = rmin[c];
+      }
     }
   }
 }
 
-template <int NT, bool CL, bool TK>
+template <int NT, int VR, bool CL, bool TK>
 static hipError_t launch_nt(const QuantArgs& a, hipStream_t s) {
-  const size_t lds = sizeof(QuantSmem<NT>) + dyn_bytes(a.d_in, TK ? a.k : 0);
+  const size_t lds = sizeof(QuantSmem) + (TK ? dyn_bytes(a.d_in, a.k) : 0);
   if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_quantize<NT, CL, TK>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_quantize<NT, VR, CL, TK>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((k_quantize<NT, CL, TK>), dim3(a.n), dim3(NT), lds, s, a);
+  hipLaunchKernelGGL((k_quantize<NT, VR, CL, TK>), dim3(a.n), dim3(NT), lds, s, a);
   return hipGetLastError();
+}
+
+// Runs of 8 channels per thread (VR) for NT threads.
+template <int NT, bool CL, bool TK>
+static hipError_t launch_vr(const QuantArgs& a, int nvec, hipStream_t s) {
+  if (nvec <= NT) return launch_nt<NT, 1, CL, TK>(a, s);
+  if (nvec <= 2 * NT) return launch_nt<NT, 2, CL, TK>(a, s);
+  if (nvec <= 4 * NT) return launch_nt<NT, 4, CL, TK>(a, s);
+  return launch_nt<NT, 8, CL, TK>(a, s);
 }
 
 template <bool CL, bool TK>
 static hipError_t launch_parts(const QuantArgs& a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
-  // few tokens: wide workgroups keep each token's serial phases short
-  return a.n <= 64 ? launch_nt<512, CL, TK>(a, s) : launch_nt<256, CL, TK>(a, s);
+  const int nvec = a.d_in / 8;
+  if (nvec > 8 * 256 || (a.n <= 64 && nvec > 512)) return launch_vr<1024, CL, TK>(a, nvec, s);
+  // few tokens: short runs per thread (latency); many: 256 threads per token
+  if (a.n <= 64) return launch_vr<512, CL, TK>(a, nvec, s);
+  return launch_vr<256, CL, TK>(a, nvec, s);
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s) { return launch_parts<true, true>(a, s); }
