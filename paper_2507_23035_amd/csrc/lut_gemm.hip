@@ -35,25 +35,55 @@ namespace oasis {
 // pair(C_A, byte), pair(C, b) = C[b & 15] | C[b >> 4] << 16 (fp16 bits).  Lane
 // l reads copy l mod 32, so the byte offset of an entry is
 // byte * 256 + (l mod 32) * 4 (+ 128 for activations): one v_perm_b32 per byte,
-// and the 32 lanes of a half-wave always hit 32 different banks.  Written with
-// 16-byte stores; each thread loads the few codebook entries it needs straight
-// from the LUT block (chunk c of 16 bytes: row c / 16, side (c / 8) mod 2).
-template <int NT>
+// and the 32 lanes of a half-wave always hit 32 different banks.
+// Written with 16-byte stores by the first four waves only (16 stores per
+// lane): wave w, lane l, step j writes chunk c = 1024 w + l + 64 j, i.e. row
+// c / 16, side (l / 8) mod 2, low code (l / 16 + 4 j) mod 16 and high code
+// 4 w + j / 4.  The codebooks come in through scalar loads - four waves per
+// workgroup rather than all of them ask for the same 64 bytes - off the vector
+// memory queue that the weight stream fills; every code index is then a
+// compile-time constant or lane / 16.
 struct DualTableLoader {
-  static_assert(NT % 256 == 0 && 4096 % NT == 0, "256..4096 threads");
-  uint32_t lo;
-  uint32_t hi[4096 / NT];
-  __device__ __forceinline__ void load(const oasis_lut_block* lut, int tid) {
-    const uint16_t* cb = ((tid >> 3) & 1) ? lut->cb_act : lut->cb_wgt;
-    lo = cb[(tid >> 4) & 15];
+  uint32_t cw[8], ca[8];  // C_W, C_A as fp16 pairs (SGPRs)
+  uint32_t hw[2], ha[2];  // the pairs holding codes 4w .. 4w + 3
+  // wave < 4 only
+  __device__ __forceinline__ void load(const oasis_lut_block* lut, uint32_t wave) {
+    const uint32_t* w32 = reinterpret_cast<const uint32_t*>(lut->cb_wgt);
+    const uint32_t* a32 = reinterpret_cast<const uint32_t*>(lut->cb_act);
 #pragma unroll
-    for (int j = 0; j < 4096 / NT; ++j) hi[j] = cb[(tid + NT * j) >> 8];
+    for (int q = 0; q < 8; ++q) {
+      cw[q] = w32[q];
+      ca[q] = a32[q];
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      hw[q] = w32[2 * wave + q];
+      ha[q] = a32[2 * wave + q];
+    }
   }
-  __device__ __forceinline__ void store(uint32_t* tab, int tid) const {
+  __device__ __forceinline__ void store(uint32_t* tab, uint32_t wave, int lane) const {
+    const bool act = (lane >> 3) & 1;
+    const int lq = lane >> 4;
+    auto half = [](uint32_t pair, int h) -> uint32_t { return (pair >> (16 * h)) & 0xFFFFu; };
+    // low code of step j: lane / 16 + 4 (j mod 4); high code: 4w + j / 4
+    uint32_t lo[4], hi[4];
 #pragma unroll
-    for (int j = 0; j < 4096 / NT; ++j) {
-      const uint32_t v = lo | (hi[j] << 16);
-      reinterpret_cast<uint4_t*>(tab)[tid + NT * j] = uint4_t{v, v, v, v};
+    for (int jj = 0; jj < 4; ++jj) {
+      uint32_t lw = 0, la = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int code = u + 4 * jj;
+        lw = lq == u ? half(cw[code >> 1], code & 1) : lw;
+        la = lq == u ? half(ca[code >> 1], code & 1) : la;
+      }
+      lo[jj] = act ? la : lw;
+      hi[jj] = (act ? half(ha[jj >> 1], jj & 1) : half(hw[jj >> 1], jj & 1)) << 16;
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t v = lo[j & 3] | hi[j >> 2];
+      reinterpret_cast<uint4_t*>(tab)[1024u * wave + (uint32_t)lane + 64u * (uint32_t)j] =
+          uint4_t{v, v, v, v};
     }
   }
 };
@@ -144,32 +174,49 @@ __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
 
 // Expand the codes of one block to fp16 centroid values and run its MFMAs:
 // CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
-// Activations of tokens past n (tok_ok false) are not expanded; MASK also
-// zeroes the words past d_in of a partial last block.
+// Steps are taken SB at a time: all their table reads are issued before the
+// first MFMA, so the LDS latency is paid once per batch.  Activations of
+// tokens past n (tok_ok false) are not expanded (one branch per token tile);
+// MASK also zeroes the words past d_in of a partial last block.
 template <int CW, int TF, bool MASK>
 __device__ __forceinline__ void mma_block(int KB, int blk, const BlockCodes<CW, TF>& bc,
                                           const char* tab, uint32_t l4w, uint32_t l4a,
                                           const bool (&tok_ok)[TF], float4_t (&acc)[CW][TF]) {
+  constexpr int SB = CW * TF >= 4 ? 2 : 4;
   const int g = (threadIdx.x & 63) >> 4;
   const int kw0 = blk * 16 + 4 * g;
+  const half8_t zero = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const bool live = !MASK || (kw0 + s) < KB;  // words past the end contribute nothing
-    half8_t bf[TF];
+  for (int s0 = 0; s0 < 4; s0 += SB) {
+    half8_t af[SB][CW], bf[SB][TF];
+#pragma unroll
+    for (int s = 0; s < SB; ++s)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) af[s][c] = expand_dual(bc.wv[s0 + s][c], tab, l4w);
 #pragma unroll
     for (int f = 0; f < TF; ++f) {
-      if (tok_ok[f] && live)
-        bf[f] = expand_dual(bc.av[f][s], tab, l4a);
-      else
-        bf[f] = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      if (tok_ok[f]) {
+#pragma unroll
+        for (int s = 0; s < SB; ++s) bf[s][f] = expand_dual(bc.av[f][s0 + s], tab, l4a);
+      } else {
+#pragma unroll
+        for (int s = 0; s < SB; ++s) bf[s][f] = zero;
+      }
+    }
+    if constexpr (MASK) {  // words past the end contribute nothing
+#pragma unroll
+      for (int s = 0; s < SB; ++s)
+        if (kw0 + s0 + s >= KB)
+#pragma unroll
+          for (int f = 0; f < TF; ++f) bf[s][f] = zero;
     }
 #pragma unroll
-    for (int c = 0; c < CW; ++c) {
-      const half8_t af = expand_dual(bc.wv[s][c], tab, l4w);
+    for (int s = 0; s < SB; ++s)
 #pragma unroll
-      for (int f = 0; f < TF; ++f)
-        acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[f], acc[c][f], 0, 0, 0);
-    }
+      for (int c = 0; c < CW; ++c)
+#pragma unroll
+        for (int f = 0; f < TF; ++f)
+          acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[s][c], bf[s][f], acc[c][f], 0, 0, 0);
   }
 }
 
@@ -239,36 +286,46 @@ __device__ __forceinline__ void comp_entries(const GemmArgs& A, int i, int e0, i
   }
 }
 
-template <int COLS, int B, bool PRE>
-__device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvAddr& ad, int j0,
-                                                  const char* tab, int nslices, int i, int quad,
-                                                  int slice, const CompEntries<B>& first,
-                                                  float (&acc)[4]) {
-  const int E = 2 * A.k;
+// Row words of the tile's columns for B entries (buffer loads; entries with
+// p < 0 read row 0 and are given a zero residual).
+template <int B>
+__device__ __forceinline__ void comp_rows(const GemmArgs& A, const GemvAddr& ad, uint32_t col4,
+                                          const CompEntries<B>& ce, uint4_t (&w)[B]) {
   const uint32_t d_out = (uint32_t)A.d_out;
-  const uint32_t col4 = (uint32_t)(j0 + 4 * quad) * 4u;
-  const uint32_t l4 = (uint32_t)(threadIdx.x & 31) * 4u;
-  CompEntries<B> ce = first;
-  for (int e0 = slice; e0 < E; e0 += B * nslices) {
-    if (!PRE || e0 != slice) comp_entries<B>(A, i, e0, nslices, ce);
-    uint32_t sh[B];
-    float r[B];
-    uint4_t w[B];
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const bool live = ce.p[b] >= 0;
-      const uint32_t pp = live ? (uint32_t)ce.p[b] : 0u;
-      r[b] = live ? ce.r[b] : 0.0f;
-      sh[b] = 4u * (pp & 7u);
-      w[b] = __builtin_bit_cast(
-          uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)((pp >> 3) * d_out * 4u + col4),
-                                                         0, 0));
+  for (int b = 0; b < B; ++b) {
+    const uint32_t pp = ce.p[b] >= 0 ? (uint32_t)ce.p[b] : 0u;
+    w[b] = __builtin_bit_cast(
+        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)((pp >> 3) * d_out * 4u + col4),
+                                                       0, 0));
+  }
+}
+
+template <int COLS, int B, bool PRE>
+__device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvAddr& ad, uint32_t col4,
+                                                  const char* tab, int nslices, int i, int slice,
+                                                  const CompEntries<B>& first,
+                                                  const uint4_t (&first_rows)[B], float (&acc)[4]) {
+  const int E = 2 * A.k;
+  const uint32_t l4 = (uint32_t)(threadIdx.x & 31) * 4u;
+  for (int e0 = slice; e0 < E; e0 += B * nslices) {
+    CompEntries<B> ce;
+    uint4_t w[B];
+    if (PRE && e0 == slice) {
+      ce = first;
+#pragma unroll
+      for (int b = 0; b < B; ++b) w[b] = first_rows[b];
+    } else {
+      comp_entries<B>(A, i, e0, nslices, ce);
+      comp_rows<B>(A, ad, col4, ce, w);
     }
 #pragma unroll
-    for (int b = 0; b < B; ++b)
+    for (int b = 0; b < B; ++b) {
+      const uint32_t sh = ce.p[b] >= 0 ? 4u * ((uint32_t)ce.p[b] & 7u) : 0u;
+      const float r = ce.p[b] >= 0 ? ce.r[b] : 0.0f;
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        acc[c] += r[b] * weight_centroid(tab, (w[b][c] >> sh[b]) & 15u, l4);
+      for (int c = 0; c < 4; ++c) acc[c] += r * weight_centroid(tab, (w[b][c] >> sh) & 15u, l4);
+    }
   }
 }
 
@@ -279,10 +336,9 @@ __device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvA
 // (A.k > 0) the workgroup also adds the compensation of its columns; each
 // wave starts its share as soon as its own blocks are done.
 //
-// Prologue order matters: the codebook entries for the decode table are
-// requested first, then the scales and the first outlier entries, then the
-// weight codes, so building the table waits only for the codebook while the
-// weight stream is in flight.
+// Prologue: the codebooks (scalar loads), the scales and the first outlier
+// entries, then the weight codes; building the table waits only for the
+// codebooks while the weight stream is in flight.
 // ----------------------------------------------------------------------------
 template <int CW, int TF, int NW, int PF, bool FULLK, int B>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
@@ -304,8 +360,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   const bool fused = A.k > 0;
 
   // ---- prologue: codebook entries, scales, outlier entries, weight codes
-  DualTableLoader<NT> dt;
-  dt.load(A.lut, tid);
+  DualTableLoader dt;
+  if (wave < 4) dt.load(A.lut, (uint32_t)wave);
   float sc[EPT];  // s_j * t_i of this thread's epilogue outputs (s_j alone for the compensation)
   float swj[EPT];
 #pragma unroll
@@ -319,7 +375,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   const int ci = tid / T, cu = tid - ci * T;
   const int cquad = cu % (COLS / 4), cslice = cu / (COLS / 4);
   // a few entries are worth holding through the main loop, many are not
-  constexpr bool PRE = B <= 4;
+  constexpr bool PRE = B <= 4 && TF == 1 && CW <= 2;
   CompEntries<B> ce0;
   if (PRE && fused && ci < A.n) comp_entries<B>(A, ci, cslice, NSLICES, ce0);
   const GemvAddr ad = gemv_addr<CW>(A, j0);
@@ -327,7 +383,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 #pragma unroll
   for (int d = 0; d < PF; ++d)
     if (wave + d * NW < nblk) load_block_buf<CW, TF>(ad, wave + d * NW, buf[d]);
-  dt.store(tab, tid);
+  if (wave < 4) dt.store(tab, (uint32_t)wave, lane);
   __syncthreads();  // decode table
 
   float4_t acc[CW][TF];
@@ -340,6 +396,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   for (int f = 0; f < TF; ++f) tok_ok[f] = 16 * f + (lane & 15) < A.n;
   const char* tb = reinterpret_cast<const char*>(tab);
   const uint32_t l4w = (uint32_t)(lane & 31) * 4u, l4a = l4w + 128u;
+  // the preloaded entries' row words, in flight during the main loop
+  const uint32_t ccol4 = (uint32_t)(j0 + 4 * cquad) * 4u;
+  uint4_t crow0[B];
+  if (PRE && fused && ci < A.n) comp_rows<B>(A, ad, ccol4, ce0, crow0);
   if (wave < nblk)
     gemv_blocks<CW, TF, PF, FULLK>(KB, ad, wave, nblk, NW, buf, tb, l4w, l4a, tok_ok, acc);
 
@@ -347,7 +407,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   // which nothing overwrites before the next barrier
   float cacc[4] = {0.f, 0.f, 0.f, 0.f};
   if (fused && ci < A.n)
-    tile_compensation<COLS, B, PRE>(A, ad, j0, tb, NSLICES, ci, cquad, cslice, ce0, cacc);
+    tile_compensation<COLS, B, PRE>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0, cacc);
   __syncthreads();  // every wave is done with the table: reuse it for the reduction
   float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tab);
   float* part = reinterpret_cast<float*>(tab) + RED_FLOATS;  // compensation partials
@@ -478,13 +538,13 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
     ad.aoff[f] = ((uint32_t)(tok0 + 16 * f + m) * (uint32_t)KB + 4u * g) * 4u;
   ad.wblk = 16u * (uint32_t)A.d_out * 4u;
 
-  // codebook entries first, then the first block's codes: building the table
-  // waits only for the codebook
-  DualTableLoader<NT> dt;
-  dt.load(A.lut, tid);
+  // codebooks (scalar loads), then the first block's codes
+  DualTableLoader dt;
+  const uint32_t uwave = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+  if (uwave < 4) dt.load(A.lut, uwave);
   BlockCodes<CW, TF> buf[2];
   load_block_pf<CW, TF>(ad, 0, buf[0]);
-  dt.store(tab, tid);
+  if (uwave < 4) dt.store(tab, uwave, lane);
   __syncthreads();
 
   float4_t acc[CW][TF];

@@ -169,40 +169,39 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     multi |= nin > 1u;
     return (e & 15u) + ((nin != 0u && (kk & 0xFFu) >= (e >> 8)) ? 1u : 0u);
   };
-  auto residual_of = [&](uint32_t kk, uint32_t bits) -> float {
-    bool multi = false;
-    uint32_t a = code_fast(kk, multi);
-    if (multi) a = code_full(kk);
-    const float x = h2f((uint16_t)bits);
-    return x - t * S.ca[a];  // t * C_A exact: a product of two fp16 values
+  // packed cluster indices of the thread's runs (8 per word, channel 8v + h in
+  // bits 4h..4h+3); 0 for runs past d_in
+  uint32_t codes[VR];
+  auto make_codes = [&]() {
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      bool multi = false;
+      uint32_t packed = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        packed |= code_fast(key[u][q] & 0xFFFFu, multi) << (8 * q);
+        packed |= code_fast(key[u][q] >> 16, multi) << (8 * q + 4);
+      }
+      if (multi) {
+        packed = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          packed |= (code_full(key[u][q] & 0xFFFFu) << (8 * q)) |
+                    (code_full(key[u][q] >> 16) << (8 * q + 4));
+      }
+      codes[u] = tid * VR + u < nvec ? packed : 0u;
+    }
   };
   uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
   auto store_codes = [&]() {
 #pragma unroll
-    for (int u = 0; u < VR; ++u) {
-      const int v = tid * VR + u;
-      if (v < nvec) {
-        bool multi = false;
-        uint32_t packed = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          packed |= code_fast(key[u][q] & 0xFFFFu, multi) << (8 * q);
-          packed |= code_fast(key[u][q] >> 16, multi) << (8 * q + 4);
-        }
-        if (multi) {
-          packed = 0;
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            packed |= (code_full(key[u][q] & 0xFFFFu) << (8 * q)) |
-                      (code_full(key[u][q] >> 16) << (8 * q + 4));
-        }
-        arow[v] = packed;
-      }
-    }
+    for (int u = 0; u < VR; ++u)
+      if (tid * VR + u < nvec) arow[tid * VR + u] = codes[u];
   };
   if (!topk) {
     if (CLUSTER) {
       __syncthreads();  // bucket table
+      make_codes();
       store_codes();
     }
     return;
@@ -299,6 +298,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   // ---- codes; per-thread counts in channel order of (max-list ties, min-list
   // ties) and (keys above Tmax, keys below Tmin), 16 bits each; the keys at
   // or beyond a threshold (the only ones a list can take)
+  make_codes();
   if (CLUSTER) store_codes();
   uint32_t c_tie = 0, c_out = 0;
   uint64_t special = 0;
@@ -351,9 +351,16 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     const int e = __builtin_ctzll(special);
     special &= special - 1;
     const int p = 8 * (tid * VR + (e >> 3)) + (e & 7);
-    const uint32_t bits = xs[p];  // staged by this thread
+    uint32_t cw = codes[0];
+#pragma unroll
+    for (int u = 1; u < VR; ++u) cw = (e >> 3) == u ? codes[u] : cw;
+    const uint32_t a = (cw >> (4 * (e & 7))) & 15u;
+    // two independent LDS reads: the raw value (staged by this thread) and its
+    // centroid; t * C_A[a] is exact, a product of two fp16 values
+    const uint32_t bits = xs[p];
+    const float xhat = t * S.ca[a];
     const uint32_t kk = ord_key(bits);
-    const float r = residual_of(kk, bits);
+    const float r = h2f((uint16_t)bits) - xhat;
     const bool tie_max = kk == Tmax && rank_max < need_max;
     const bool in_max = kk > Tmax || tie_max;
     if (tie_max) {
@@ -392,7 +399,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     for (uint32_t c = (uint32_t)(tid & (HALF - 1)); c < G; c += HALF) {
       const uint32_t mine = cand[c] ^ flip;
       uint32_t rank = 0;
-#pragma unroll 2
+#pragma unroll 4
       for (uint32_t q = 0; q < nq; ++q) {
         const uint4 o = c4[q];  // the same 16 bytes in every lane
         rank += ((o.x ^ flip) > mine ? 1u : 0u) + ((o.y ^ flip) > mine ? 1u : 0u) +
@@ -434,10 +441,15 @@ template <bool CL, bool TK>
 static hipError_t launch_parts(const QuantArgs& a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   const int nvec = a.d_in / 8;
-  if (nvec > 8 * 256 || (a.n <= 64 && nvec > 512)) return launch_vr<1024, CL, TK>(a, nvec, s);
   // few tokens: short runs per thread (latency); many: 256 threads per token
-  if (a.n <= 64) return launch_vr<512, CL, TK>(a, nvec, s);
-  return launch_vr<256, CL, TK>(a, nvec, s);
+  // while runs of 4 vectors suffice (register pressure), then wider
+  if (a.n <= 64) {
+    if (nvec <= 512) return launch_vr<512, CL, TK>(a, nvec, s);
+    return launch_vr<1024, CL, TK>(a, nvec, s);
+  }
+  if (nvec <= 4 * 256) return launch_vr<256, CL, TK>(a, nvec, s);
+  if (nvec <= 4 * 512) return launch_vr<512, CL, TK>(a, nvec, s);
+  return launch_vr<1024, CL, TK>(a, nvec, s);
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s) { return launch_parts<true, true>(a, s); }
