@@ -166,9 +166,10 @@ def test_scale_mode_none():
     run_full(synth.make_layer(spec), scale_mode=oasis.SCALE_NONE)
 
 
-def test_degenerate_tokens():
+@pytest.mark.parametrize("k", [6, 40])  # 40: compensation inside the GEMV main loop
+def test_degenerate_tokens(k):
     """Constant tokens, an all-zero token, signed zeros and heavy ties."""
-    L = synth.make_layer(synth.custom(6, 128, 72, 6, seed=12))
+    L = synth.make_layer(synth.custom(6, 128, 72, k, seed=12))
     x = L.x.copy()
     x[0, :] = np.float16(1.5)                                  # constant: lists overlap
     x[1, :] = np.float16(0.0)                                  # all zero: t = 0
