@@ -3,7 +3,9 @@
 A step is one pass of the whole path over one synthetic layer: build the LUT
 block, quantize the activations (scale, codes, top-k outliers, residuals),
 then the LUT-GEMM and the outlier compensation (one fused call for few
-tokens; --path selects the schedule).
+tokens; --path selects the schedule).  (Building the LUT block on a second
+stream, overlapping the previous step, was slower: the cross-stream waits
+inside the graph cost more than the 1.7 us launch they hide.)
 Inputs are resident in HBM when timing starts; the weight codes are rotated
 over enough copies (> 512 MiB in total) that the 256 MiB last-level cache
 cannot serve them.  The timed steps are captured once into one HIP graph and
@@ -284,27 +286,33 @@ def main():
         names = ["build_lut", "quantize_act", "outlier_compensate", "lut_gemm"]
         gemm_name = "lut_gemm"
 
-    def step(c):
+    def step(i):
+        """Step i (weight copy i mod copies)."""
+        c = i % copies
         main = torch.cuda.current_stream()
-        calls["build_lut"](c)
+        L = lut
+        oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
         if path == "fused":
-            calls["quantize_act"](c)
-            calls["lut_gemm_compensated"](c)
+            oasis.quantize_act(x, L, b_a, k, out=q)
+            oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w,
+                                       q["max_idx"], q["min_idx"], q["residual"], y=y)
         elif path == "lookahead":
             # main branch and outlier detection run concurrently (Sec. III-C)
             side.wait_stream(main)
             with torch.cuda.stream(side):
-                oasis.detect_outliers(x, lut, b_a, k, out=q, stream=side)
-            calls["cluster_act"](c)
-            oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, algo,
+                oasis.detect_outliers(x, L, b_a, k, out=q, stream=side)
+            oasis.cluster_act(x, L, b_a, out=q)
+            oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo,
                            y=y, accumulate=False)
             main.wait_stream(side)
-            oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut,
+            oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], L,
                                      b_w, s_w, d_in, y=y, accumulate=True)
         else:
-            calls["quantize_act"](c)
-            calls["outlier_compensate"](c)
-            calls["lut_gemm"](c)
+            oasis.quantize_act(x, L, b_a, k, out=q)
+            oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], L,
+                                     b_w, s_w, d_in, y=y, accumulate=False)
+            oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo, y=y,
+                           accumulate=True)
 
     nsteps = args.steps
 
@@ -313,12 +321,12 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for i in range(first, first + count):
-                step(i % copies)
+                step(i)
         return g
 
     # prime the library and the allocator outside capture
-    for c in range(min(copies, 2)):
-        step(c)
+    for i in range(2):
+        step(i)
     torch.cuda.synchronize()
     mode = "eager" if args.eager else "graph"
     if mode == "graph":
@@ -342,13 +350,35 @@ def main():
         elapsed = time.perf_counter() - t0
     else:
         for i in range(args.warmup):
-            step(i % copies)
+            step(i)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(args.warmup, args.warmup + nsteps):
-            step(i % copies)
+            step(i)
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
+
+    # ---- the schedule keeps every dependence: the last timed step's output
+    # equals one eager, single-stream pass over the same weight copy (the
+    # kernels are deterministic, so bit for bit)
+    y_sched = y.clone()
+    last = args.warmup + nsteps - 1
+    c_last = last % copies
+    oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
+    if path == "lookahead":
+        q1 = oasis.quantize_act(x, lut, b_a, k)
+        y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a, b_w,
+                               algo)
+        oasis.outlier_compensate(q1["max_idx"], q1["min_idx"], q1["residual"], idx_w[c_last], lut,
+                                 b_w, s_w, d_in, y=y_ref, accumulate=True)
+    else:
+        y_ref = oasis.forward(x, lut, idx_w[c_last], s_w, b_a, b_w, k, algo=algo,
+                              fused=path == "fused")["y"]
+    torch.cuda.synchronize()
+    schedule_ok = bool(torch.equal(y_sched, y_ref)) if algo == oasis.ALGO_MFMA else bool(
+        torch.allclose(y_sched, y_ref, rtol=1e-4, atol=1e-3))
+    if not schedule_ok:
+        print("bench.py: the timed schedule's output differs from an eager pass", file=sys.stderr)
 
     # ---- per-call durations: `nsteps` back-to-back launches of one call (same
     # arguments, rotating weight copies) queued behind a spin kernel, so the
@@ -411,6 +441,7 @@ def main():
                    "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
                    "path": path,
                    "weight_copies": copies},
+        "schedule_check": schedule_ok,
         "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),
         "kernel_us": {kk: round(v, 3) for kk, v in kern_us.items()},
         "roofline": roofline,
