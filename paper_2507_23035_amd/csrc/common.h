@@ -50,6 +50,15 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Sum over aligned groups of P consecutive lanes (P = 1, 2, 4 or 8, the same
+// in every lane); every lane of a group receives the group's sum.
+__device__ __forceinline__ uint32_t group_sum(uint32_t v, uint32_t P) {
+  if (P >= 2u) v += __builtin_amdgcn_update_dpp(0u, v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+  if (P >= 4u) v += __builtin_amdgcn_update_dpp(0u, v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+  if (P >= 8u) v += __builtin_amdgcn_update_dpp(0u, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  return v;
+}
+
 // Inclusive scan of one 64-bit value per thread over the block (NT threads).
 // Each call needs its own `tmp` (NT / 64 words): there is no trailing barrier.
 template <int NT>

@@ -26,13 +26,14 @@
 // Top-k is a two-level radix select on the keys shared by the max and min
 // lists: a histogram of the high byte fixes the bucket holding the k-th
 // largest (smallest) key, a histogram of the low byte inside it the exact
-// threshold key T and the count G < k of keys strictly beyond it.  Keys equal
-// to T are taken in channel order (a block-wide exclusive count gives each its
-// rank); the G keys beyond T are ranked among themselves.  The paper's trees
-// pop in exactly this order; the select replaces k sequential pops by two
-// histogram passes.  Every wave scans the histograms itself (DPP prefix sums),
-// so a level costs one barrier, and only the keys at or beyond a threshold
-// are visited after the counts.
+// threshold key T, the count G < k of keys strictly beyond it and the count N
+// of keys equal to it.  A list takes every key beyond T and, when N fits the
+// k - G places left, every key equal to T; otherwise the first k - G of those
+// in channel order (a block-wide exclusive count ranks them).  The k entries
+// of a list are then ranked by their sort key (key, channel), which is
+// distinct per channel.  The paper's trees pop in exactly this order; the
+// select replaces k sequential pops by two histogram passes.  Every wave scans
+// the histograms itself (DPP prefix sums), so a level costs one barrier.
 #include "common.h"
 
 namespace oasis {
@@ -43,12 +44,13 @@ struct __align__(16) QuantSmem {
   uint16_t bucket[256];    // first index | inside count << 4 | low byte << 8
   float ca[16];            // C_A in fp32
   uint32_t wmax[16];       // per-wave absmax
-  uint32_t wtot[2][16];    // per-wave totals of the two packed count pairs
+  uint32_t wtot[16];       // per-wave tie counts (max | min << 16), cut case only
+  uint32_t nalloc;         // list slots handed out (max | min << 16)
 };
 
-// Dynamic LDS after the fixed part: the token (2 B per channel), then G < k
-// candidates per list, each a sort key and its residual (max list, then min
-// list), padded to a multiple of 4.
+// Dynamic LDS after the fixed part: the token (2 B per channel), then the k
+// entries of each list, a sort key and the channel's cluster index (max list,
+// then min list), padded to a multiple of 4.
 static size_t dyn_bytes(int d_in, int k) {
   const size_t k4 = ((size_t)k + 3) & ~(size_t)3;
   return (size_t)d_in * 2 + 16 * k4;
@@ -78,9 +80,9 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   const uint32_t k4 = ((uint32_t)k + 3u) & ~3u;
   uint16_t* xs = reinterpret_cast<uint16_t*>(smem_raw + sizeof(QuantSmem));
   uint32_t* cmax = reinterpret_cast<uint32_t*>(xs + d_in);  // d_in % 8 == 0: 16-byte aligned
-  float* rmax = reinterpret_cast<float*>(cmax + k4);
-  uint32_t* cmin = reinterpret_cast<uint32_t*>(rmax + k4);
-  float* rmin = reinterpret_cast<float*>(cmin + k4);
+  uint32_t* amax_ = cmax + k4;
+  uint32_t* cmin = amax_ + k4;
+  uint32_t* amin_ = cmin + k4;
 
   // ---- the token into registers (runs tid*VR .. tid*VR + VR - 1)
   uint4 xv[VR];
@@ -96,6 +98,14 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     S.hist2[1][tid] = 0;
   }
   if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
+  if (tid == 0) S.nalloc = 0;
+  // pad both lists to a multiple of 4 with entries that never rank first
+  // (sort keys are compared after XOR with 0 for the max list and with ~0 for
+  // the min list, which turns a pad into 0)
+  if (TOPK && tid < 4 && (uint32_t)(k + tid) < k4) {
+    cmax[k + tid] = 0u;
+    cmin[k + tid] = 0xFFFFFFFFu;
+  }
   __syncthreads();  // histograms cleared, C_A staged
 
   // keys, two per word (even channel low)
@@ -256,7 +266,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   }
   __syncthreads();  // level-2 histograms, bucket table
 
-  uint32_t Tmax, Gmax, Tmin, Gmin;
+  uint32_t Tmax, Gmax, Tmin, Gmin, Nmax, Nmin;  // N: keys equal to the threshold
   {
     const uint4 hm = *reinterpret_cast<const uint4*>(&S.hist2[0][4 * lane]);
     const uint4 hn = *reinterpret_cast<const uint4*>(&S.hist2[1][4 * lane]);
@@ -265,7 +275,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     uint32_t prem = wave_incl_scan(summ) - summ, pren = wave_incl_scan(sumn) - sumn;
     const uint32_t totm = S.hist1[B1max];
     const uint32_t kk = (uint32_t)k - G1max, kn = (uint32_t)k - G1min;
-    uint32_t tm = 0, gm = 0, tn = 0, gn = 0;
+    uint32_t tm = 0, gm = 0, tn = 0, gn = 0, nm = 0, nn = 0;
     bool hit_max = false, hit_min = false;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -274,10 +284,12 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       const bool hmq = above < kk && kk <= above + ms[q];
       tm = hmq ? ((B1max << 8) | (uint32_t)(4 * lane + q)) : tm;
       gm = hmq ? G1max + above : gm;
+      nm = hmq ? ms[q] : nm;
       const uint32_t upton = pren + ns[q];
       const bool hnq = pren < kn && kn <= upton;
       tn = hnq ? ((B1min << 8) | (uint32_t)(4 * lane + q)) : tn;
       gn = hnq ? G1min + pren : gn;
+      nn = hnq ? ns[q] : nn;
       hit_max |= hmq;
       hit_min |= hnq;
       prem = uptom;
@@ -289,128 +301,173 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     Gmax = __builtin_amdgcn_readlane(gm, lm);
     Tmin = __builtin_amdgcn_readlane(tn, ln);
     Gmin = __builtin_amdgcn_readlane(gn, ln);
+    Nmax = __builtin_amdgcn_readlane(nm, lm);
+    Nmin = __builtin_amdgcn_readlane(nn, ln);
   }
   // G < k holds by construction; the clamp only keeps every index in bounds.
   Gmax = min(Gmax, (uint32_t)k - 1u);
   Gmin = min(Gmin, (uint32_t)k - 1u);
   const uint32_t need_max = (uint32_t)k - Gmax, need_min = (uint32_t)k - Gmin;
 
-  // ---- codes; per-thread counts in channel order of (max-list ties, min-list
-  // ties) and (keys above Tmax, keys below Tmin), 16 bits each; the keys at
-  // or beyond a threshold (the only ones a list can take)
   make_codes();
   if (CLUSTER) store_codes();
-  uint32_t c_tie = 0, c_out = 0;
-  uint64_t special = 0;
+
+  // ---- list membership, one bit per channel.  A key beyond a threshold
+  // always enters its list.  A key equal to it enters too, unless the value
+  // occurs more often than the list has room for: then only the first `need`
+  // such keys in channel order do, ranked by a block-wide exclusive count.
+  const bool cut = Nmax > need_max || Nmin > need_min;  // uniform
+  // one bit per channel of the thread: 32-bit masks while they suffice
+  using mask_t = typename std::conditional<(8 * VR <= 32), uint32_t, uint64_t>::type;
+  mask_t mmax = 0, mmin = 0;
+  if (!cut) {
 #pragma unroll
-  for (int u = 0; u < VR; ++u) {
-    if (tid * VR + u < nvec) {
+    for (int u = 0; u < VR; ++u) {
+      if (tid * VR + u < nvec) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < 4; ++q) {
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
-          c_tie += (kk == Tmax ? 1u : 0u) + (kk == Tmin ? 0x10000u : 0u);
-          c_out += (kk > Tmax ? 1u : 0u) + (kk < Tmin ? 0x10000u : 0u);
-          special |= (uint64_t)((kk >= Tmax) | (kk <= Tmin)) << (8 * u + 2 * q + hh);
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
+            mmax |= (mask_t)(kk >= Tmax ? 1u : 0u) << (8 * u + 2 * q + hh);
+            mmin |= (mask_t)(kk <= Tmin ? 1u : 0u) << (8 * u + 2 * q + hh);
+          }
+        }
+      }
+    }
+  } else {
+    uint32_t c_tie = 0;  // (max ties, min ties), 16 bits each: < 65536 channels
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      if (tid * VR + u < nvec) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
+            c_tie += (kk == Tmax ? 1u : 0u) + (kk == Tmin ? 0x10000u : 0u);
+          }
+        }
+      }
+    }
+    const uint32_t inc = wave_incl_scan(c_tie);
+    if (lane == 63) S.wtot[wave] = inc;
+    __syncthreads();  // wave tie totals
+    uint32_t ex = inc - c_tie;
+    {
+      uint32_t wt[NW];
+#pragma unroll
+      for (int j = 0; j < NW / 4; ++j) {
+        const uint4 v = reinterpret_cast<const uint4*>(S.wtot)[j];
+        wt[4 * j] = v.x;
+        wt[4 * j + 1] = v.y;
+        wt[4 * j + 2] = v.z;
+        wt[4 * j + 3] = v.w;
+      }
+#pragma unroll
+      for (int w = 0; w < NW; ++w) ex += w < wave ? wt[w] : 0u;
+    }
+    uint32_t rm = ex & 0xFFFFu, rn = ex >> 16;
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      if (tid * VR + u < nvec) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
+            const bool em = kk == Tmax, en = kk == Tmin;
+            const bool im = kk > Tmax || (em && rm < need_max);
+            const bool in = kk < Tmin || (en && rn < need_min);
+            mmax |= (mask_t)(im ? 1u : 0u) << (8 * u + 2 * q + hh);
+            mmin |= (mask_t)(in ? 1u : 0u) << (8 * u + 2 * q + hh);
+            rm += em ? 1u : 0u;
+            rn += en ? 1u : 0u;
+          }
         }
       }
     }
   }
-  // block-wide exclusive prefix: wave scan, wave totals through LDS.  A
-  // prefix counts keys before this thread, < 65536, so the fields never carry.
-  const uint32_t inc_tie = wave_incl_scan(c_tie), inc_out = wave_incl_scan(c_out);
-  if (lane == 63) {
-    S.wtot[0][wave] = inc_tie;
-    S.wtot[1][wave] = inc_out;
-  }
-  // pad the candidate lists to a multiple of 4 with entries that never rank
-  // first (sort keys are compared after XOR with 0 for the max list and with
-  // ~0 for the min list, which turns a pad into 0)
-  if (tid < 4) {
-    if (Gmax + (uint32_t)tid < k4) cmax[Gmax + tid] = 0u;
-    if (Gmin + (uint32_t)tid < k4) cmin[Gmin + tid] = 0xFFFFFFFFu;
-  }
-  __syncthreads();  // wave totals
-  uint32_t ex_tie = inc_tie - c_tie, ex_out = inc_out - c_out;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    if (w < wave) {
-      ex_tie += S.wtot[0][w];
-      ex_out += S.wtot[1][w];
-    }
-  }
-  uint32_t rank_max = ex_tie & 0xFFFFu, rank_min = ex_tie >> 16;
-  uint32_t slot_max = ex_out & 0xFFFFu, slot_min = ex_out >> 16;
 
-  const size_t krow = (size_t)i * k;
-  const size_t rrow = (size_t)i * 2 * k;
-  // ---- collect, in channel order: threshold ties go straight to their list
-  // position, the keys beyond the thresholds to candidate slots
-  while (special) {
-    const int e = __builtin_ctzll(special);
-    special &= special - 1;
-    const int p = 8 * (tid * VR + (e >> 3)) + (e & 7);
+  // ---- each list holds exactly k entries; slots in any order (the ranking
+  // sorts them), taken per lane from one LDS counter
+  const uint32_t cnt = (uint32_t)__builtin_popcountll((uint64_t)mmax) |
+                       ((uint32_t)__builtin_popcountll((uint64_t)mmin) << 16);
+  // wave prefix, then one LDS atomic per wave (lane 63 holds the wave total)
+  const uint32_t inc = wave_incl_scan(cnt);
+  uint32_t wbase = 0;
+  if (lane == 63) wbase = atomicAdd(&S.nalloc, inc);
+  const uint32_t slot = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 63) + inc - cnt;
+  uint32_t smax = slot & 0xFFFFu, smin = slot >> 16;
+  mask_t m = mmax | mmin;
+  const uint32_t p0 = 8u * (uint32_t)(tid * VR);
+  while (m) {
+    const int e = __builtin_ctzll((uint64_t)m);
+    m &= m - 1;
+    uint32_t w = key[0][0];
+#pragma unroll
+    for (int j = 1; j < 4 * VR; ++j) w = (e >> 1) == j ? key[j >> 2][j & 3] : w;
+    const uint32_t kk = (w >> (16 * (e & 1))) & 0xFFFFu;
     uint32_t cw = codes[0];
 #pragma unroll
     for (int u = 1; u < VR; ++u) cw = (e >> 3) == u ? codes[u] : cw;
     const uint32_t a = (cw >> (4 * (e & 7))) & 15u;
-    // two independent LDS reads: the raw value (staged by this thread) and its
-    // centroid; t * C_A[a] is exact, a product of two fp16 values
-    const uint32_t bits = xs[p];
-    const float xhat = t * S.ca[a];
-    const uint32_t kk = ord_key(bits);
-    const float r = h2f((uint16_t)bits) - xhat;
-    const bool tie_max = kk == Tmax && rank_max < need_max;
-    const bool in_max = kk > Tmax || tie_max;
-    if (tie_max) {
-      A.max_idx[krow + Gmax + rank_max] = p;
-      A.residual[rrow + Gmax + rank_max] = r;
+    const uint32_t p = p0 + (uint32_t)e;
+    const bool im = ((mmax >> e) & 1u) != 0u, in = ((mmin >> e) & 1u) != 0u;
+    if (im && smax < (uint32_t)k) {
+      cmax[smax] = (kk << 16) | (0xFFFFu - p);
+      amax_[smax] = a;
     }
-    if (kk > Tmax && slot_max < Gmax) {
-      cmax[slot_max] = (kk << 16) | (0xFFFFu - (uint32_t)p);
-      rmax[slot_max] = r;
+    if (in && smin < (uint32_t)k) {
+      cmin[smin] = (kk << 16) | p;
+      amin_[smin] = a | (im ? 16u : 0u);  // 16: the channel is on the max list too
     }
-    if (kk == Tmin && rank_min < need_min) {
-      A.min_idx[krow + Gmin + rank_min] = p;
-      A.residual[rrow + k + Gmin + rank_min] = in_max ? 0.0f : r;
-    }
-    if (kk < Tmin && slot_min < Gmin) {
-      cmin[slot_min] = (kk << 16) | (uint32_t)p;
-      rmin[slot_min] = in_max ? 0.0f : r;
-    }
-    rank_max += kk == Tmax ? 1u : 0u;
-    slot_max += kk > Tmax ? 1u : 0u;
-    rank_min += kk == Tmin ? 1u : 0u;
-    slot_min += kk < Tmin ? 1u : 0u;
+    smax += im ? 1u : 0u;
+    smin += in ? 1u : 0u;
   }
-  __syncthreads();  // candidates
+  __syncthreads();  // both lists
 
-  // ---- rank the candidates: the first half of the waves the max list, the
-  // second half the min list; each counts the candidates that pop before it
+  // ---- rank: the first half of the waves the max list, the second half the
+  // min list.  P lanes share an entry, each counting the entries that pop
+  // before it over every P-th quad; a DPP sum combines the P counts.  Sort
+  // keys (key, channel) are distinct, so the ranks are the list positions.
+  const size_t krow = (size_t)i * k;
+  const size_t rrow = (size_t)i * 2 * k;
   {
     constexpr int HALF = NT / 2;
     const bool is_max = wave < NW / 2;  // uniform
-    const uint32_t G = is_max ? Gmax : Gmin;
     const uint32_t flip = is_max ? 0u : 0xFFFFFFFFu;
     const uint32_t* cand = is_max ? cmax : cmin;
+    const uint32_t* aux = is_max ? amax_ : amin_;
     const uint4* c4 = reinterpret_cast<const uint4*>(cand);
-    const uint32_t nq = (G + 3u) / 4u;
-    for (uint32_t c = (uint32_t)(tid & (HALF - 1)); c < G; c += HALF) {
+    const uint32_t nq = k4 / 4u;
+    uint32_t P = 1;  // uniform
+    while (P < 8u && P < nq && 2u * P * (uint32_t)k <= (uint32_t)HALF) P *= 2u;
+    const uint32_t lt = (uint32_t)tid & (uint32_t)(HALF - 1), part = lt & (P - 1u);
+    for (uint32_t c = lt / P; c < (uint32_t)k; c += (uint32_t)HALF / P) {
       const uint32_t mine = cand[c] ^ flip;
+      const uint32_t ax = aux[c];
+      const uint32_t p = is_max ? 0xFFFFu - (mine & 0xFFFFu) : (~mine & 0xFFFFu);
+      // two independent LDS reads: the raw value and its centroid; t * C_A[a]
+      // is exact, a product of two fp16 values
+      const uint32_t bits = xs[p];
+      const float xhat = t * S.ca[ax & 15u];
       uint32_t rank = 0;
-#pragma unroll 4
-      for (uint32_t q = 0; q < nq; ++q) {
-        const uint4 o = c4[q];  // the same 16 bytes in every lane
+      for (uint32_t qq = part; qq < nq; qq += P) {
+        const uint4 o = c4[qq];  // the same 16 bytes in every lane of the group
         rank += ((o.x ^ flip) > mine ? 1u : 0u) + ((o.y ^ flip) > mine ? 1u : 0u) +
                 ((o.z ^ flip) > mine ? 1u : 0u) + ((o.w ^ flip) > mine ? 1u : 0u);
       }
-      if (is_max) {
-        A.max_idx[krow + rank] = (int)(0xFFFFu - (mine & 0xFFFFu));
-        A.residual[rrow + rank] = rmax[c];
-      } else {
-        A.min_idx[krow + rank] = (int)(~mine & 0xFFFFu);
-        A.residual[rrow + k + rank] = rmin[c];
+      rank = group_sum(rank, P);
+      if (part == 0u) {
+        const float r = (ax & 16u) ? 0.0f : h2f((uint16_t)bits) - xhat;
+        if (is_max) {
+          A.max_idx[krow + rank] = (int)p;
+          A.residual[rrow + rank] = r;
+        } else {
+          A.min_idx[krow + rank] = (int)p;
+          A.residual[rrow + k + rank] = r;
+        }
       }
     }
   }
