@@ -23,17 +23,20 @@
 // in a bucket with more take the full 15-compare count.  This is the fp32 rule
 // of the oracle, bit for bit, at one LDS lookup per channel.
 //
-// Top-k is a two-level radix select on the keys shared by the max and min
-// lists: a histogram of the high byte fixes the bucket holding the k-th
-// largest (smallest) key, a histogram of the low byte inside it the exact
-// threshold key T, the count G < k of keys strictly beyond it and the count N
-// of keys equal to it.  A list takes every key beyond T and, when N fits the
-// k - G places left, every key equal to T; otherwise the first k - G of those
-// in channel order (a block-wide exclusive count ranks them).  The k entries
-// of a list are then ranked by their sort key (key, channel), which is
-// distinct per channel.  The paper's trees pop in exactly this order; the
-// select replaces k sequential pops by two histogram passes.  Every wave scans
-// the histograms itself (DPP prefix sums), so a level costs one barrier.
+// Top-k is a radix select on the keys shared by the max and min lists: a
+// histogram of the high byte fixes the bucket holding the k-th largest
+// (smallest) key and the count G of keys in the buckets beyond it.  When the
+// boundary bucket is small (G plus its size fits the list area) and the two
+// candidate sets are disjoint, a list takes every key of the boundary bucket
+// and beyond, and ranking them by (key, channel) - distinct per channel -
+// keeps the first k.  Otherwise a histogram of the low byte inside the bucket
+// gives the exact threshold key T, the count G < k of keys beyond it and the
+// count N of keys equal to it; a list takes every key beyond T and, when N
+// fits the k - G places left, every key equal to T, else the first k - G of
+// those in channel order (a block-wide exclusive count ranks them).  The
+// paper's trees pop in exactly this order; the select replaces k sequential
+// pops by histogram passes.  Every wave scans the histograms itself (DPP
+// prefix sums), so a level costs one barrier.
 #include "common.h"
 
 namespace oasis {
@@ -48,13 +51,17 @@ struct __align__(16) QuantSmem {
   uint32_t nalloc;         // list slots handed out (max | min << 16)
 };
 
-// Dynamic LDS after the fixed part: the token (2 B per channel), then the k
-// entries of each list, a sort key and the channel's cluster index (max list,
-// then min list), padded to a multiple of 4.
-static size_t dyn_bytes(int d_in, int k) {
-  const size_t k4 = ((size_t)k + 3) & ~(size_t)3;
-  return (size_t)d_in * 2 + 16 * k4;
+// Entries a list area holds: k rounded up to 4, plus room for the keys of a
+// boundary bucket beyond the k-th (a multiple of 4).
+__host__ __device__ inline uint32_t list_cap(int k) {
+  const uint32_t k4 = ((uint32_t)k + 3u) & ~3u;
+  return k4 + (k4 / 2u > 32u ? ((k4 / 2u) & ~3u) : 32u);
 }
+
+// Dynamic LDS after the fixed part: the token (2 B per channel), then the two
+// list areas, each list_cap(k) sort keys and as many cluster indices (max
+// list, then min list).
+static size_t dyn_bytes(int d_in, int k) { return (size_t)d_in * 2 + 16 * (size_t)list_cap(k); }
 
 size_t quantize_lds_bytes(int d_in, int k) { return sizeof(QuantSmem) + dyn_bytes(d_in, k); }
 
@@ -77,12 +84,12 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   const int i = blockIdx.x;
   const int d_in = A.d_in, k = A.k, nvec = d_in >> 3;
   const bool topk = TOPK && k > 0;  // uniform
-  const uint32_t k4 = ((uint32_t)k + 3u) & ~3u;
+  const uint32_t lcap = topk ? list_cap(k) : 0u;
   uint16_t* xs = reinterpret_cast<uint16_t*>(smem_raw + sizeof(QuantSmem));
   uint32_t* cmax = reinterpret_cast<uint32_t*>(xs + d_in);  // d_in % 8 == 0: 16-byte aligned
-  uint32_t* amax_ = cmax + k4;
-  uint32_t* cmin = amax_ + k4;
-  uint32_t* amin_ = cmin + k4;
+  uint32_t* amax_ = cmax + lcap;
+  uint32_t* cmin = amax_ + lcap;
+  uint32_t* amin_ = cmin + lcap;
 
   // ---- the token into registers (runs tid*VR .. tid*VR + VR - 1)
   uint4 xv[VR];
@@ -99,13 +106,6 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   }
   if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
   if (tid == 0) S.nalloc = 0;
-  // pad both lists to a multiple of 4 with entries that never rank first
-  // (sort keys are compared after XOR with 0 for the max list and with ~0 for
-  // the min list, which turns a pad into 0)
-  if (TOPK && tid < 4 && (uint32_t)(k + tid) < k4) {
-    cmax[k + tid] = 0u;
-    cmin[k + tid] = 0xFFFFFFFFu;
-  }
   __syncthreads();  // histograms cleared, C_A staged
 
   // keys, two per word (even channel low)
@@ -219,13 +219,13 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
 
   // ---- level 1: the high-byte buckets holding the k-th largest and k-th
   // smallest key (each wave scans the histogram itself)
-  uint32_t B1max, G1max, B1min, G1min;
+  uint32_t B1max, G1max, B1min, G1min, H1max, H1min;  // H1: keys in the bucket
   {
     const uint4 h = *reinterpret_cast<const uint4*>(&S.hist1[4 * lane]);
     const uint32_t hs[4] = {h.x, h.y, h.z, h.w};
     const uint32_t sum = h.x + h.y + h.z + h.w;
     uint32_t pre = wave_incl_scan(sum) - sum;  // keys in buckets below 4*lane
-    uint32_t fmax = 0, gmax = 0, fmin = 0, gmin = 0;
+    uint32_t fmax = 0, gmax = 0, fmin = 0, gmin = 0, hmx = 0, hmn = 0;
     bool hit_max = false, hit_min = false;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -237,6 +237,8 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       gmax = hm ? above : gmax;
       fmin = hn ? (uint32_t)(4 * lane + q) : fmin;
       gmin = hn ? below : gmin;
+      hmx = hm ? hs[q] : hmx;
+      hmn = hn ? hs[q] : hmn;
       hit_max |= hm;
       hit_min |= hn;
       pre = upto;
@@ -248,11 +250,17 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     G1max = __builtin_amdgcn_readlane(gmax, lm);
     B1min = __builtin_amdgcn_readlane(fmin, ln);
     G1min = __builtin_amdgcn_readlane(gmin, ln);
+    H1max = __builtin_amdgcn_readlane(hmx, lm);
+    H1min = __builtin_amdgcn_readlane(hmn, ln);
   }
+  // One level suffices when both lists fit every key of their boundary bucket
+  // and the two candidate sets are disjoint: the lists then take all those
+  // keys and the ranking by (key, channel) keeps the first k of each.
+  const bool one_level = G1max + H1max <= lcap && G1min + H1min <= lcap && B1max > B1min;
   // ---- level 2: low bytes inside the two boundary buckets
 #pragma unroll
   for (int u = 0; u < VR; ++u) {
-    if (tid * VR + u < nvec) {
+    if (!one_level && tid * VR + u < nvec) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
 #pragma unroll
@@ -266,57 +274,78 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   }
   __syncthreads();  // level-2 histograms, bucket table
 
-  uint32_t Tmax, Gmax, Tmin, Gmin, Nmax, Nmin;  // N: keys equal to the threshold
-  {
-    const uint4 hm = *reinterpret_cast<const uint4*>(&S.hist2[0][4 * lane]);
-    const uint4 hn = *reinterpret_cast<const uint4*>(&S.hist2[1][4 * lane]);
-    const uint32_t ms[4] = {hm.x, hm.y, hm.z, hm.w}, ns[4] = {hn.x, hn.y, hn.z, hn.w};
-    const uint32_t summ = hm.x + hm.y + hm.z + hm.w, sumn = hn.x + hn.y + hn.z + hn.w;
-    uint32_t prem = wave_incl_scan(summ) - summ, pren = wave_incl_scan(sumn) - sumn;
-    const uint32_t totm = S.hist1[B1max];
-    const uint32_t kk = (uint32_t)k - G1max, kn = (uint32_t)k - G1min;
-    uint32_t tm = 0, gm = 0, tn = 0, gn = 0, nm = 0, nn = 0;
-    bool hit_max = false, hit_min = false;
+  // thresholds: keys >= Tmax enter the max list, keys <= Tmin the min list;
+  // L entries each (one level: the whole boundary buckets; two levels: k)
+  uint32_t Tmax, Tmin, Lmax, Lmin;
+  bool cut = false;
+  uint32_t need_max = 0, need_min = 0;
+  if (one_level) {
+    Tmax = B1max << 8;
+    Tmin = (B1min << 8) | 0xFFu;
+    Lmax = G1max + H1max;
+    Lmin = G1min + H1min;
+  } else {
+    uint32_t Gmax, Gmin, Nmax, Nmin;  // N: keys equal to the threshold
+    {
+      const uint4 hm = *reinterpret_cast<const uint4*>(&S.hist2[0][4 * lane]);
+      const uint4 hn = *reinterpret_cast<const uint4*>(&S.hist2[1][4 * lane]);
+      const uint32_t ms[4] = {hm.x, hm.y, hm.z, hm.w}, ns[4] = {hn.x, hn.y, hn.z, hn.w};
+      const uint32_t summ = hm.x + hm.y + hm.z + hm.w, sumn = hn.x + hn.y + hn.z + hn.w;
+      uint32_t prem = wave_incl_scan(summ) - summ, pren = wave_incl_scan(sumn) - sumn;
+      const uint32_t totm = S.hist1[B1max];
+      const uint32_t kk = (uint32_t)k - G1max, kn = (uint32_t)k - G1min;
+      uint32_t tm = 0, gm = 0, tn = 0, gn = 0, nm = 0, nn = 0;
+      bool hit_max = false, hit_min = false;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t uptom = prem + ms[q];
-      const uint32_t above = totm - uptom;  // keys of the bucket with a higher low byte
-      const bool hmq = above < kk && kk <= above + ms[q];
-      tm = hmq ? ((B1max << 8) | (uint32_t)(4 * lane + q)) : tm;
-      gm = hmq ? G1max + above : gm;
-      nm = hmq ? ms[q] : nm;
-      const uint32_t upton = pren + ns[q];
-      const bool hnq = pren < kn && kn <= upton;
-      tn = hnq ? ((B1min << 8) | (uint32_t)(4 * lane + q)) : tn;
-      gn = hnq ? G1min + pren : gn;
-      nn = hnq ? ns[q] : nn;
-      hit_max |= hmq;
-      hit_min |= hnq;
-      prem = uptom;
-      pren = upton;
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t uptom = prem + ms[q];
+        const uint32_t above = totm - uptom;  // keys of the bucket with a higher low byte
+        const bool hmq = above < kk && kk <= above + ms[q];
+        tm = hmq ? ((B1max << 8) | (uint32_t)(4 * lane + q)) : tm;
+        gm = hmq ? G1max + above : gm;
+        nm = hmq ? ms[q] : nm;
+        const uint32_t upton = pren + ns[q];
+        const bool hnq = pren < kn && kn <= upton;
+        tn = hnq ? ((B1min << 8) | (uint32_t)(4 * lane + q)) : tn;
+        gn = hnq ? G1min + pren : gn;
+        nn = hnq ? ns[q] : nn;
+        hit_max |= hmq;
+        hit_min |= hnq;
+        prem = uptom;
+        pren = upton;
+      }
+      const int lm = __builtin_ctzll(__ballot(hit_max) | (1ull << 63));
+      const int ln = __builtin_ctzll(__ballot(hit_min) | (1ull << 63));
+      Tmax = __builtin_amdgcn_readlane(tm, lm);
+      Gmax = __builtin_amdgcn_readlane(gm, lm);
+      Tmin = __builtin_amdgcn_readlane(tn, ln);
+      Gmin = __builtin_amdgcn_readlane(gn, ln);
+      Nmax = __builtin_amdgcn_readlane(nm, lm);
+      Nmin = __builtin_amdgcn_readlane(nn, ln);
     }
-    const int lm = __builtin_ctzll(__ballot(hit_max) | (1ull << 63));
-    const int ln = __builtin_ctzll(__ballot(hit_min) | (1ull << 63));
-    Tmax = __builtin_amdgcn_readlane(tm, lm);
-    Gmax = __builtin_amdgcn_readlane(gm, lm);
-    Tmin = __builtin_amdgcn_readlane(tn, ln);
-    Gmin = __builtin_amdgcn_readlane(gn, ln);
-    Nmax = __builtin_amdgcn_readlane(nm, lm);
-    Nmin = __builtin_amdgcn_readlane(nn, ln);
+    // G < k holds by construction; the clamp only keeps every index in bounds.
+    Gmax = min(Gmax, (uint32_t)k - 1u);
+    Gmin = min(Gmin, (uint32_t)k - 1u);
+    need_max = (uint32_t)k - Gmax;
+    need_min = (uint32_t)k - Gmin;
+    // a key equal to a threshold enters its list unless the value occurs more
+    // often than the list has room for: then only the first `need` such keys
+    // in channel order do, ranked by a block-wide exclusive count
+    cut = Nmax > need_max || Nmin > need_min;
+    Lmax = Lmin = (uint32_t)k;
   }
-  // G < k holds by construction; the clamp only keeps every index in bounds.
-  Gmax = min(Gmax, (uint32_t)k - 1u);
-  Gmin = min(Gmin, (uint32_t)k - 1u);
-  const uint32_t need_max = (uint32_t)k - Gmax, need_min = (uint32_t)k - Gmin;
+  // pad both lists to a multiple of 4 with entries that never rank first
+  // (sort keys are compared after XOR with 0 for the max list and with ~0 for
+  // the min list, which turns a pad into 0)
+  if (tid < 4) {
+    if (Lmax + (uint32_t)tid < lcap) cmax[Lmax + tid] = 0u;
+    if (Lmin + (uint32_t)tid < lcap) cmin[Lmin + tid] = 0xFFFFFFFFu;
+  }
 
   make_codes();
   if (CLUSTER) store_codes();
 
-  // ---- list membership, one bit per channel.  A key beyond a threshold
-  // always enters its list.  A key equal to it enters too, unless the value
-  // occurs more often than the list has room for: then only the first `need`
-  // such keys in channel order do, ranked by a block-wide exclusive count.
-  const bool cut = Nmax > need_max || Nmin > need_min;  // uniform
+  // ---- list membership, one bit per channel
   // one bit per channel of the thread: 32-bit masks while they suffice
   using mask_t = typename std::conditional<(8 * VR <= 32), uint32_t, uint64_t>::type;
   mask_t mmax = 0, mmin = 0;
@@ -389,8 +418,8 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     }
   }
 
-  // ---- each list holds exactly k entries; slots in any order (the ranking
-  // sorts them), taken per lane from one LDS counter
+  // ---- each list holds exactly L entries; slots in any order (the ranking
+  // sorts them), a block-wide count through one LDS counter
   const uint32_t cnt = (uint32_t)__builtin_popcountll((uint64_t)mmax) |
                        ((uint32_t)__builtin_popcountll((uint64_t)mmin) << 16);
   // wave prefix, then one LDS atomic per wave (lane 63 holds the wave total)
@@ -414,11 +443,11 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     const uint32_t a = (cw >> (4 * (e & 7))) & 15u;
     const uint32_t p = p0 + (uint32_t)e;
     const bool im = ((mmax >> e) & 1u) != 0u, in = ((mmin >> e) & 1u) != 0u;
-    if (im && smax < (uint32_t)k) {
+    if (im && smax < Lmax) {
       cmax[smax] = (kk << 16) | (0xFFFFu - p);
       amax_[smax] = a;
     }
-    if (in && smin < (uint32_t)k) {
+    if (in && smin < Lmin) {
       cmin[smin] = (kk << 16) | p;
       amin_[smin] = a | (im ? 16u : 0u);  // 16: the channel is on the max list too
     }
@@ -440,11 +469,12 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     const uint32_t* cand = is_max ? cmax : cmin;
     const uint32_t* aux = is_max ? amax_ : amin_;
     const uint4* c4 = reinterpret_cast<const uint4*>(cand);
-    const uint32_t nq = k4 / 4u;
+    const uint32_t L = is_max ? Lmax : Lmin;
+    const uint32_t nq = (L + 3u) / 4u;
     uint32_t P = 1;  // uniform
-    while (P < 8u && P < nq && 2u * P * (uint32_t)k <= (uint32_t)HALF) P *= 2u;
+    while (P < 8u && P < nq && 2u * P * L <= (uint32_t)HALF) P *= 2u;
     const uint32_t lt = (uint32_t)tid & (uint32_t)(HALF - 1), part = lt & (P - 1u);
-    for (uint32_t c = lt / P; c < (uint32_t)k; c += (uint32_t)HALF / P) {
+    for (uint32_t c = lt / P; c < L; c += (uint32_t)HALF / P) {
       const uint32_t mine = cand[c] ^ flip;
       const uint32_t ax = aux[c];
       const uint32_t p = is_max ? 0xFFFFu - (mine & 0xFFFFu) : (~mine & 0xFFFFu);
@@ -459,7 +489,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
                 ((o.z ^ flip) > mine ? 1u : 0u) + ((o.w ^ flip) > mine ? 1u : 0u);
       }
       rank = group_sum(rank, P);
-      if (part == 0u) {
+      if (part == 0u && rank < (uint32_t)k) {
         const float r = (ax & 16u) ? 0.0f : h2f((uint16_t)bits) - xhat;
         if (is_max) {
           A.max_idx[krow + rank] = (int)p;

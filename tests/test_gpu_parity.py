@@ -182,6 +182,21 @@ def test_degenerate_tokens(k):
     run_full(L)
 
 
+def test_crowded_boundary_buckets():
+    """Tokens whose boundary buckets hold far more keys than the lists: the
+    select needs the low-byte level and the channel-order ties."""
+    L = synth.make_layer(synth.custom(5, 1024, 64, 16, seed=17))
+    rng = np.random.default_rng(17)
+    x = L.x.copy()
+    x[0, :] = rng.uniform(1.0, 1.25, 1024).astype(np.float16)     # one high-byte bucket
+    x[1, :] = rng.uniform(-1.25, -1.0, 1024).astype(np.float16)
+    x[1, [3, 500, 901]] = np.float16(9.0)                         # a few beyond it
+    x[2, :] = rng.uniform(0.9, 1.1, 1024).astype(np.float16)      # two buckets
+    x[3, :] = np.float16(rng.integers(-3, 4, 1024))               # seven values, many ties
+    L.x = x
+    run_full(L)
+
+
 def test_empty_batch():
     L = synth.make_layer(synth.custom(2, 64, 32, 2, seed=13))
     x, idx_w, s_w, lut = upload(L)
