@@ -130,21 +130,26 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       }
     }
   }
+  // boundary mid-points b_c = fp32(C_A[c] + C_A[c+1]) * 0.5 in lane c (they
+  // do not depend on the token)
+  const int nb = (1 << A.b_a) - 1;
+  const float bc = lane < nb ? (S.ca[lane] + S.ca[lane + 1]) * 0.5f : 0.0f;
   amax = wave_max(amax);
   if (lane == 0) S.wmax[wave] = amax;
   __syncthreads();  // absmax partials, level-1 histogram
 
 #pragma unroll
-  for (int w = 0; w < NW; ++w) amax = max(amax, S.wmax[w]);
+  for (int j = 0; j < NW / 4; ++j) {
+    const uint4 m = reinterpret_cast<const uint4*>(S.wmax)[j];
+    amax = max(amax, max(max(m.x, m.y), max(m.z, m.w)));
+  }
   const float t = (A.scale_mode == OASIS_SCALE_NONE) ? 1.0f : h2f((uint16_t)amax);
   if (CLUSTER && tid == 0) A.act_scale[i] = t;
 
   // ---- boundary keys: lane c computes key(Q_c), Q_c = the smallest fp16 not
-  // below P_c = fp32(t * b_c), b_c = fp32(C_A[c] + C_A[c+1]) * 0.5
-  const int nb = (1 << A.b_a) - 1;
+  // below P_c = fp32(t * b_c)
   uint32_t kq_lane = 0x10000u;  // above every key: boundaries past the last one
   if (lane < nb) {
-    const float bc = (S.ca[lane] + S.ca[lane + 1]) * 0.5f;
     const float P = t * bc;
     const _Float16 h = (_Float16)P;  // round to nearest even
     kq_lane = ord_key(__builtin_bit_cast(uint16_t, h)) + ((float)h < P ? 1u : 0u);
