@@ -260,6 +260,12 @@ def main():
     if path == "auto":
         path = "fused" if (n <= 32 and algo == oasis.ALGO_MFMA) else "separate"
     side = torch.cuda.Stream()
+    # the outlier branch of the separate and look-ahead schedules reads the
+    # codes in the row layout (one input channel = d_out/2 contiguous bytes)
+    idx_wr = []
+    if path != "fused":
+        rows = oasis.pack_weight_rows(layer.w_idx).view(np.int32)
+        idx_wr = [torch.from_numpy(rows).to(dev) for _ in range(copies)]
 
     # Every call of the path, with the arguments the step uses (c = weight copy).
     calls = {
@@ -267,8 +273,8 @@ def main():
         "quantize_act": lambda c: oasis.quantize_act(x, lut, b_a, k, out=q),
         "cluster_act": lambda c: oasis.cluster_act(x, lut, b_a, out=q),
         "detect_outliers": lambda c: oasis.detect_outliers(x, lut, b_a, k, out=q),
-        "outlier_compensate": lambda c: oasis.outlier_compensate(
-            q["max_idx"], q["min_idx"], q["residual"], idx_w[c], lut, b_w, s_w, d_in, y=y,
+        "outlier_compensate": lambda c: oasis.outlier_compensate_rows(
+            q["max_idx"], q["min_idx"], q["residual"], idx_wr[c], lut, b_w, s_w, d_in, y=y,
             accumulate=False),
         "lut_gemm": lambda c: oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut,
                                              b_a, b_w, algo, y=y, accumulate=True),
@@ -305,12 +311,12 @@ def main():
             oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo,
                            y=y, accumulate=False)
             main.wait_stream(side)
-            oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], L,
-                                     b_w, s_w, d_in, y=y, accumulate=True)
+            oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr[c],
+                                          L, b_w, s_w, d_in, y=y, accumulate=True)
         else:
             oasis.quantize_act(x, L, b_a, k, out=q)
-            oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w[c], L,
-                                     b_w, s_w, d_in, y=y, accumulate=False)
+            oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr[c],
+                                          L, b_w, s_w, d_in, y=y, accumulate=False)
             oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo, y=y,
                            accumulate=True)
 
@@ -365,15 +371,22 @@ def main():
     last = args.warmup + nsteps - 1
     c_last = last % copies
     oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
-    if path == "lookahead":
-        q1 = oasis.quantize_act(x, lut, b_a, k)
-        y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a, b_w,
-                               algo)
-        oasis.outlier_compensate(q1["max_idx"], q1["min_idx"], q1["residual"], idx_w[c_last], lut,
-                                 b_w, s_w, d_in, y=y_ref, accumulate=True)
+    if path == "fused":
+        y_ref = oasis.forward(x, lut, idx_w[c_last], s_w, b_a, b_w, k, algo=algo, fused=True)["y"]
     else:
-        y_ref = oasis.forward(x, lut, idx_w[c_last], s_w, b_a, b_w, k, algo=algo,
-                              fused=path == "fused")["y"]
+        q1 = oasis.quantize_act(x, lut, b_a, k)
+        if path == "lookahead":
+            y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a,
+                                   b_w, algo)
+            oasis.outlier_compensate_rows(q1["max_idx"], q1["min_idx"], q1["residual"],
+                                          idx_wr[c_last], lut, b_w, s_w, d_in, y=y_ref,
+                                          accumulate=True)
+        else:
+            y_ref = oasis.outlier_compensate_rows(q1["max_idx"], q1["min_idx"], q1["residual"],
+                                                  idx_wr[c_last], lut, b_w, s_w, d_in,
+                                                  accumulate=False)
+            oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a, b_w,
+                           algo, y=y_ref, accumulate=True)
     torch.cuda.synchronize()
     schedule_ok = bool(torch.equal(y_sched, y_ref)) if algo == oasis.ALGO_MFMA else bool(
         torch.allclose(y_sched, y_ref, rtol=1e-4, atol=1e-3))

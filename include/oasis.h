@@ -29,6 +29,10 @@
  *              4e..4e+3.  (Input-channel-major, so one input channel of all
  *              output columns, which the compensation fetches, is one
  *              contiguous row of words.)
+ *  - idx_wr  : uint32 [d_in][ceil(d_out/8)]; word m of row p holds the codes
+ *              of input channel p for output columns 8m..8m+7, column 8m+c
+ *              in bits 4c..4c+3 (the row layout: one input channel is d_out/2
+ *              contiguous bytes; read by oasis_outlier_compensate_rows).
  *  - y       : fp32 [n][d_out], row-major.
  */
 #ifndef OASIS_H
@@ -188,6 +192,25 @@ int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, con
                              int accumulate, hipStream_t stream);
 
 /*
+ * oasis_outlier_compensate_rows - the same error compensation (Sec. III-C2)
+ * from the weight codes in the row layout idx_wr (see oasis_pack_weight_rows):
+ * each listed outlier channel p reads exactly row p, d_out/2 bytes, where the
+ * idx_w layout costs 4 bytes per (outlier, column).  For many tokens.
+ *   idx_wr : DEVICE uint32 [d_in][ceil(d_out/8)]; word m of row p holds the
+ *            codes of input channel p for output columns 8m..8m+7, column
+ *            8m+c in bits 4c..4c+3 (zero past d_out).
+ *   Every other argument, the result and accumulate as in
+ *   oasis_outlier_compensate (sums in list order per output).
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, TOO_LARGE (d_in * ceil(d_out/8) * 4
+ * >= 2^31), LAUNCH.
+ */
+int oasis_outlier_compensate_rows(const int32_t* max_idx, const int32_t* min_idx,
+                                  const float* residual, int n, int k, const uint32_t* idx_wr,
+                                  const oasis_lut_block* lut, int b_w, const float* w_scale,
+                                  int d_in, int d_out, float* y, int accumulate,
+                                  hipStream_t stream);
+
+/*
  * oasis_lut_gemm_compensated - main branch and outlier branch in one call
  * (look-ahead computation with error compensation, Sec. III-C):
  *   y (+)= Y* + Y', with Y* as in oasis_lut_gemm and Y' as in
@@ -212,6 +235,15 @@ int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, i
  * (host memory, d_in/8 * d_out words).  Errors: NULL, SHAPE.
  */
 int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out);
+
+/*
+ * oasis_pack_weight_rows - HOST helper: pack w_idx uint8 [d_in][d_out]
+ * (codes 0..15, row-major, host memory) into the row layout idx_wr of
+ * oasis_outlier_compensate_rows (host memory, d_in * ceil(d_out/8) words;
+ * the paper's own layout of the weight index matrix, one input channel per
+ * contiguous row).  Errors: NULL, SHAPE.
+ */
+int oasis_pack_weight_rows(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out);
 
 #ifdef __cplusplus
 }

@@ -406,6 +406,20 @@ def pack_weight_indices(w_idx: np.ndarray) -> np.ndarray:
     return out
 
 
+def pack_weight_rows(w_idx: np.ndarray) -> np.ndarray:
+    """[K][N] indices -> [K][ceil(N/8)] 32-bit words; column 8m+c of row p at
+    bits 4c..4c+3 of word (p, m), zero past N (one input channel per row)."""
+    w = np.asarray(w_idx, dtype=np.uint32)
+    K, N = w.shape
+    Np = (N + 7) // 8 * 8
+    wp = np.zeros((K, Np), dtype=np.uint32)
+    wp[:, :N] = w
+    out = np.zeros((K, Np // 8), dtype=np.uint32)
+    for c in range(8):
+        out |= wp[:, c::8] << np.uint32(4 * c)
+    return out
+
+
 # --------------------------------------------------------------------------
 # Table I / Sec. II-B: closed-form cost of the LUT schemes
 # --------------------------------------------------------------------------

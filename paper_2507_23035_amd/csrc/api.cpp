@@ -171,6 +171,27 @@ int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, con
   return launched(oasis::launch_compensate(a, stream));
 }
 
+int oasis_outlier_compensate_rows(const int32_t* max_idx, const int32_t* min_idx,
+                                  const float* residual, int n, int k, const uint32_t* idx_wr,
+                                  const oasis_lut_block* lut, int b_w, const float* w_scale,
+                                  int d_in, int d_out, float* y, int accumulate,
+                                  hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!lut || !w_scale || !y) return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual || !idx_wr)) return OASIS_ERR_NULL;
+  if (!aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4) ||
+      !aligned(idx_wr, 4) || !aligned(lut, 16) || !aligned(w_scale, 4) || !aligned(y, 4))
+    return OASIS_ERR_ALIGN;
+  // byte offsets into the codes are 32-bit
+  if ((uint64_t)d_in * (uint64_t)((d_out + 7) / 8) * 4u >= (1ull << 31)) return OASIS_ERR_TOO_LARGE;
+  oasis::CompArgs a{max_idx, min_idx, residual, n, k, idx_wr, lut, b_w, w_scale, d_in, d_out, y,
+                    accumulate ? 1 : 0};
+  return launched(oasis::launch_compensate_wr(a, stream));
+}
+
 int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
                                const uint32_t* idx_w, const float* w_scale, int d_out,
                                const oasis_lut_block* lut, int b_a, int b_w,
@@ -217,6 +238,22 @@ int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_
     for (int e = 0; e < 8; ++e) {
       const uint8_t* src = w_idx + (size_t)(8 * b + e) * d_out;
       for (int j = 0; j < d_out; ++j) row[j] |= (uint32_t)(src[j] & 15u) << (4 * e);
+    }
+  }
+  return OASIS_OK;
+}
+
+int oasis_pack_weight_rows(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out) {
+  if (!w_idx || !out) return OASIS_ERR_NULL;
+  if (d_in < 0 || d_out < 0) return OASIS_ERR_SHAPE;
+  const int wn = (d_out + 7) / 8;
+  for (int p = 0; p < d_in; ++p) {
+    const uint8_t* src = w_idx + (size_t)p * d_out;
+    uint32_t* row = out + (size_t)p * wn;
+    for (int m = 0; m < wn; ++m) {
+      uint32_t w = 0;
+      for (int c = 0; c < 8 && 8 * m + c < d_out; ++c) w |= (uint32_t)(src[8 * m + c] & 15u) << (4 * c);
+      row[m] = w;
     }
   }
   return OASIS_OK;

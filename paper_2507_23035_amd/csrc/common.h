@@ -135,6 +135,8 @@ hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s);
 // Y (+)= Y* + Y' in one launch when a.n <= kFusedMaxTokens.
 constexpr int kFusedMaxTokens = 32;
 hipError_t launch_compensate(const CompArgs& a, hipStream_t s);
+// Same, with idx_w in the row layout (uint32 [d_in][ceil(d_out / 8)]).
+hipError_t launch_compensate_wr(const CompArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* y, size_t count, hipStream_t s);
 
 }  // namespace oasis

@@ -270,8 +270,8 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
     for (int d = 0; d < ROW_PF; ++d) {
       const uint32_t j = base + d;
       const uint32_t row = (uint32_t)__builtin_amdgcn_readlane((int)lw_row, (int)(j - lw0));
-      // rows past the list read past the buffer: zeros, no branch
-      const int soff = j < nrow ? (int)(row * row_bytes) : (int)0x80000000u;
+      // rows past the list read row 0 (in bounds) and are never used
+      const int soff = j < nrow ? (int)(row * row_bytes) : 0;
       if constexpr (CPL % 4 == 0) {
 #pragma unroll
         for (int h = 0; h < CPL / 4; ++h) {
@@ -365,6 +365,224 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
       }
     }
   }
+}
+
+// ----------------------------------------------------------------------------
+// Compensation from the row layout: idx_wr uint32 [d_in][wn], wn =
+// ceil(d_out / 8), word m of row p holds the codes of input channel p for
+// output columns 8m .. 8m + 7 (column 8m + c in bits 4c .. 4c + 3).  One
+// listed outlier reads exactly its own row, d_out / 2 bytes.
+//
+// Workgroup = 4 waves over a slab of 64 words (512 columns) and a tile of
+// WR_TT tokens; wave w takes tokens w, w + 4, ... of the tile.  Lane l owns
+// word 64 * slab + l and 8 fp32 accumulators per token.  A token's listed
+// entries are wave-uniform: lane e holds entry e, readlane hands them out in
+// list order, and each entry fetches one word per lane (one contiguous
+// 256-byte piece of row p per wave, 3 * WR_U entries in flight).  A word's four
+// bytes become four pairs of weight centroids through a 64 KiB LDS table -
+// row `byte` holds 32 copies of pair(C_W, byte), so the offset is one
+// v_perm_b32 and the read is conflict free - and each centroid meets the
+// residual in one fp32 FMA.
+// ----------------------------------------------------------------------------
+constexpr int WR_TT = 32;   // tokens per workgroup tile
+constexpr int WR_U = 16;    // entries per unit of word loads
+constexpr int WR_C = 512;   // list entries per wave held in LDS at a time
+
+__global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int nslab,
+                                                        int ntile) {
+  // the pair table (bytes [0, 128) of each 256-byte row used) at a fixed LDS
+  // address; dynamic LDS: per wave WR_C channels and WR_C residuals of its lists
+  __shared__ uint32_t tab[256 * 64];
+  extern __shared__ __align__(16) unsigned char smem_wr[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int* lp = reinterpret_cast<int*>(smem_wr) + wave * WR_C;
+  float* lr = reinterpret_cast<float*>(smem_wr + 4 * 4 * WR_C) + wave * WR_C;
+  const int r = xcd_tile(blockIdx.x, nslab * ntile);
+  const int slab = r / ntile, tile = r % ntile;  // token tiles of a slab on one XCD
+  const int k = A.k, E = 2 * k, d_in = A.d_in, d_out = A.d_out;
+
+  // ---- this wave's tokens, in units of WR_U entries
+  const int tok0 = tile * WR_TT;
+  const int tw = tok0 + wave;  // first token of this wave; then every fourth
+  const int tend = min(A.n, tok0 + WR_TT);
+  const int ntw = tw < tend ? (tend - tw + 3) / 4 : 0;
+  const int nch = (E + WR_U - 1) / WR_U;  // units per token
+  const int U = ntw * nch;
+  // copy the lists of units [c0, c1) into this wave's LDS area, validated:
+  // dead entries (past the lists, duplicates with residual 0, channels out of
+  // range) get channel -1 and residual 0.  LDS operations of one wave run in
+  // order, so the wave reads its area without a barrier.
+  auto fill = [&](int c0, int c1) {
+    constexpr int PER = WR_C / 64;
+    int pv[PER];
+    float rv[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {  // every load first, then the checks
+      const int f = lane + 64 * j;
+      const int u = c0 + f / WR_U;
+      const int i = tw + 4 * (u / nch), e = WR_U * (u % nch) + f % WR_U;
+      pv[j] = -1;
+      rv[j] = 0.0f;
+      if (f < (c1 - c0) * WR_U && e < E) {
+        const int32_t* src = e < k ? A.max_idx + (size_t)i * k + e : A.min_idx + (size_t)i * k + (e - k);
+        pv[j] = *src;
+        rv[j] = A.residual[(size_t)i * E + e];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const bool live = pv[j] >= 0 && pv[j] < d_in && rv[j] != 0.0f;
+      lp[lane + 64 * j] = live ? pv[j] : -1;
+      lr[lane + 64 * j] = live ? rv[j] : 0.0f;
+    }
+  };
+  fill(0, min(U, WR_C / WR_U));  // the first chunk's loads overlap the table build
+
+  // pair table: thread t writes chunks c = t + 256 s (s < 8) of 16 bytes:
+  // row c / 8 (low code (t / 8) mod 16, high code t / 128 + 2 s), copies
+  // 4 (c mod 8) .. 4 (c mod 8) + 3
+  {
+    const uint16_t* cb = A.lut->cb_wgt;
+    const uint32_t lo = cb[(tid >> 3) & 15];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const uint32_t v = lo | ((uint32_t)cb[(tid >> 7) + 2 * s] << 16);
+      const uint32_t c = (uint32_t)tid + 256u * (uint32_t)s;
+      *reinterpret_cast<uint4_t*>(&tab[(c >> 3) * 64u + (c & 7u) * 4u]) = uint4_t{v, v, v, v};
+    }
+  }
+
+  const uint32_t m = (uint32_t)slab * 64u + (uint32_t)lane;  // this lane's word
+  const uint32_t voff = m * 4u;
+  const uint32_t row_bytes = (uint32_t)wn * 4u;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(A.idx_w), 0, (int)((uint32_t)d_in * row_bytes), 0x00020000);
+  const uint32_t lane4 = (uint32_t)(lane & 31) * 4u;
+  const char* tb = reinterpret_cast<const char*>(tab);
+  float sw[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const uint32_t j = 8u * m + (uint32_t)c;
+    sw[c] = j < (uint32_t)d_out ? A.w_scale[j] : 0.0f;
+  }
+  const bool vec = (d_out & 3) == 0 && ((reinterpret_cast<uintptr_t>(A.y) & 15u) == 0) &&
+                   8u * m + 8u <= (uint32_t)d_out;
+  __syncthreads();  // pair table
+
+  // ---- chunks of WR_C entries; inside a chunk three units of word loads
+  // stay in flight: step v reads the lists of unit v + 2 from LDS, requests
+  // its words (one per lane per entry), then consumes unit v.  Only word
+  // loads are in flight, and they retire in order, so each wait covers just
+  // the unit consumed.
+  auto issue = [&](int pl, uint32_t (&w)[WR_U]) {
+#pragma unroll
+    for (int e = 0; e < WR_U; ++e) {
+      const int pe = __builtin_amdgcn_readlane(pl, e);
+      // a dead entry reads row 0 (in bounds); its residual is 0
+      const int soff = pe >= 0 ? (int)((uint32_t)pe * row_bytes) : 0;
+      w[e] = __builtin_amdgcn_raw_buffer_load_b32(rw, (int)voff, soff, 0);
+    }
+  };
+  float acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
+  auto consume = [&](int u, float rl, const uint32_t (&w)[WR_U]) {
+#pragma unroll
+    for (int e = 0; e < WR_U; ++e) {
+      const float re = __builtin_bit_cast(float,
+                                          __builtin_amdgcn_readlane(__builtin_bit_cast(int, rl), e));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const uint32_t off = __builtin_amdgcn_perm(w[e], lane4, 0x0C0C0000u | ((4u + b) << 8));
+        const uint32_t pr = *reinterpret_cast<const uint32_t*>(tb + off);
+        acc[2 * b] = fmaf(re, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * b]);
+        acc[2 * b + 1] = fmaf(re, h2f((uint16_t)(pr >> 16)), acc[2 * b + 1]);
+      }
+    }
+    if (u % nch != nch - 1) return;
+    // the token's last unit: y (+)= s_j * acc
+    const int i = tw + 4 * (u / nch);
+    float* dst = A.y + (size_t)i * d_out + 8u * m;
+    if (vec) {
+      float4* d4 = reinterpret_cast<float4*>(dst);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float4 o = make_float4(sw[4 * h] * acc[4 * h], sw[4 * h + 1] * acc[4 * h + 1],
+                               sw[4 * h + 2] * acc[4 * h + 2], sw[4 * h + 3] * acc[4 * h + 3]);
+        if (A.accumulate) {
+          const float4 y0 = d4[h];
+          o.x += y0.x;
+          o.y += y0.y;
+          o.z += y0.z;
+          o.w += y0.w;
+        }
+        d4[h] = o;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        if (8u * m + (uint32_t)c < (uint32_t)d_out) {
+          const float v = sw[c] * acc[c];
+          dst[c] = A.accumulate ? dst[c] + v : v;
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
+  };
+
+  for (int c0 = 0; c0 < U; c0 += WR_C / WR_U) {
+    const int c1 = min(U, c0 + WR_C / WR_U), V = c1 - c0;
+    if (c0 > 0) fill(c0, c1);
+    __builtin_amdgcn_wave_barrier();
+    // lane e < WR_U: entry e of chunk unit v
+    auto rd = [&](int v, int& pl, float& rl) {
+      pl = -1;
+      rl = 0.0f;
+      if (v < V && lane < WR_U) {
+        pl = lp[v * WR_U + lane];
+        rl = lr[v * WR_U + lane];
+      }
+    };
+    int p0, p1, p2;
+    float r0, r1, r2;
+    uint32_t w0[WR_U], w1[WR_U], w2[WR_U];
+    rd(0, p0, r0);
+    rd(1, p1, r1);
+    issue(p0, w0);
+    if (V > 1) issue(p1, w1);
+    // (ra, wa): unit v; unit v + 2's lists go to (pc, rc), its words to wc
+    auto step = [&](int v, float& ra, uint32_t (&wa)[WR_U], int& pc, float& rc,
+                    uint32_t (&wc)[WR_U]) {
+      const float ru = ra;
+      rd(v + 2, pc, rc);
+      if (v + 2 < V) issue(pc, wc);
+      consume(c0 + v, ru, wa);
+    };
+    for (int v = 0; v < V; v += 3) {
+      step(v, r0, w0, p2, r2, w2);
+      if (v + 1 < V) step(v + 1, r1, w1, p0, r0, w0);
+      if (v + 2 < V) step(v + 2, r2, w2, p1, r1, w1);
+    }
+    __builtin_amdgcn_wave_barrier();  // the next fill overwrites the area
+  }
+}
+
+hipError_t launch_compensate_wr(const CompArgs& a, hipStream_t s) {
+  if (a.n == 0 || a.d_out == 0) return hipSuccess;
+  if (a.k == 0) {
+    if (a.accumulate) return hipSuccess;
+    return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
+  }
+  const int wn = (a.d_out + 7) / 8;
+  const int nslab = (wn + 63) / 64, ntile = (a.n + WR_TT - 1) / WR_TT;
+  const size_t lds = 4 * 8 * WR_C;  // dynamic part: the lists
+  hipError_t e = hipFuncSetAttribute((const void*)k_compensate_wr,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_compensate_wr, dim3(nslab * ntile), dim3(256), lds, s, a, wn, nslab, ntile);
+  return hipGetLastError();
 }
 
 hipError_t launch_compensate(const CompArgs& a, hipStream_t s) {

@@ -23,8 +23,8 @@ LUT_BLOCK_BYTES = 256 * 4 + 16 * 2 + 16 * 2
 
 EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quantize_act",
            "oasis_cluster_act", "oasis_detect_outliers",
-           "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_lut_gemm_compensated",
-           "oasis_pack_weight_indices")
+           "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_outlier_compensate_rows",
+           "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows")
 
 
 class OasisError(RuntimeError):
@@ -63,8 +63,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_outlier_compensate.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
     lib.oasis_lut_gemm_compensated.restype = I
     lib.oasis_lut_gemm_compensated.argtypes = [P, P, I, I, P, P, I, P, I, I, P, P, P, I, P, I, P]
+    lib.oasis_outlier_compensate_rows.restype = I
+    lib.oasis_outlier_compensate_rows.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
     lib.oasis_pack_weight_indices.restype = I
     lib.oasis_pack_weight_indices.argtypes = [P, I, I, P]
+    lib.oasis_pack_weight_rows.restype = I
+    lib.oasis_pack_weight_rows.argtypes = [P, I, I, P]
     _lib = lib
     return lib
 
@@ -99,6 +103,16 @@ def pack_weight_indices(w_idx: np.ndarray) -> np.ndarray:
     out = np.empty((d_in // 8, d_out), dtype=np.uint32)
     _check("oasis_pack_weight_indices",
            load().oasis_pack_weight_indices(w.ctypes.data, d_in, d_out, out.ctypes.data))
+    return out
+
+
+def pack_weight_rows(w_idx: np.ndarray) -> np.ndarray:
+    """uint8 [d_in][d_out] codes -> uint32 [d_in][ceil(d_out/8)] row-layout words (host)."""
+    w = np.ascontiguousarray(w_idx, dtype=np.uint8)
+    d_in, d_out = w.shape
+    out = np.empty((d_in, (d_out + 7) // 8), dtype=np.uint32)
+    _check("oasis_pack_weight_rows",
+           load().oasis_pack_weight_rows(w.ctypes.data, d_in, d_out, out.ctypes.data))
     return out
 
 
@@ -192,6 +206,21 @@ def outlier_compensate(max_idx, min_idx, residual, idx_w, lut, b_w: int, w_scale
     _check("oasis_outlier_compensate", load().oasis_outlier_compensate(
         _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
         _ptr(residual) if k else None, n, k, _ptr(idx_w), _ptr(lut), b_w, _ptr(w_scale), d_in,
+        d_out, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def outlier_compensate_rows(max_idx, min_idx, residual, idx_wr, lut, b_w: int, w_scale,
+                            d_in: int, y=None, accumulate: bool = True, stream=None):
+    """Outlier branch Y' from the row-layout codes (y += Y' with accumulate, else y = Y')."""
+    import torch
+    n, k = max_idx.shape
+    d_out = w_scale.shape[0]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=max_idx.device)
+    _check("oasis_outlier_compensate_rows", load().oasis_outlier_compensate_rows(
+        _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
+        _ptr(residual) if k else None, n, k, _ptr(idx_wr), _ptr(lut), b_w, _ptr(w_scale), d_in,
         d_out, _ptr(y), 1 if accumulate else 0, _stream(stream)))
     return y
 

@@ -31,7 +31,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for fn in ("oasis_build_lut", "oasis_quantize_act", "oasis_lut_gemm",
-               "oasis_outlier_compensate"):
+               "oasis_outlier_compensate", "oasis_outlier_compensate_rows"):
         assert fn in names
 
 
@@ -137,6 +137,31 @@ def test_compensate_errors(lib):
     assert c(None, P, P, 4, 3, P, P, 4, P, 16, 8, P, 1, None) == -1
     assert c(P, P, P, 4, 3, P, P, 4, P, 16, 8, MIS, 1, None) == -6
     assert c(P, P, P, 0, 3, P, P, 4, P, 16, 8, P, 1, None) == 0
+
+
+def test_compensate_rows_errors(lib):
+    c = lib.oasis_outlier_compensate_rows
+    assert c(P, P, P, 4, 3, P, P, 4, P, 20, 8, P, 1, None) == -2
+    assert c(P, P, P, 4, 17, P, P, 4, P, 16, 8, P, 1, None) == -4
+    assert c(P, P, P, 4, 3, P, P, 5, P, 16, 8, P, 1, None) == -3
+    assert c(None, P, P, 4, 3, P, P, 4, P, 16, 8, P, 1, None) == -1
+    assert c(P, P, P, 4, 3, P, P, 4, P, 16, 8, MIS, 1, None) == -6
+    assert c(P, P, P, 4, 3, P, P, 4, P, 65536, 65536, P, 1, None) == -9  # 2^31 bytes of codes
+    assert c(P, P, P, 0, 3, P, P, 4, P, 16, 8, P, 1, None) == 0
+
+
+def test_pack_weight_rows_matches_oracle_packing():
+    from oracle import oasis_oracle as O
+    rng = np.random.default_rng(6)
+    for shape in [(24, 13), (8, 16), (5, 1), (3, 40)]:
+        w = rng.integers(0, 16, shape).astype(np.uint8)
+        got = oasis.pack_weight_rows(w)
+        assert got.shape == (shape[0], (shape[1] + 7) // 8)
+        assert np.array_equal(got, O.pack_weight_rows(w))
+        # every nibble back in place, zeros past the last column
+        cols = np.arange(8 * got.shape[1])
+        nib = (got[:, cols // 8] >> (4 * (cols % 8)).astype(np.uint32)) & 15
+        assert np.array_equal(nib[:, :shape[1]], w) and not nib[:, shape[1]:].any()
 
 
 def test_pack_weight_indices_matches_oracle_packing():

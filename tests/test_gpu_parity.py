@@ -79,6 +79,16 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
                                   s_w, L.spec.d_in, accumulate=False)
     torch.cuda.synchronize()
     assert_close(yc.cpu().numpy()[rows], ref["y_comp"], "Y'")
+    idx_wr = torch.from_numpy(oasis.pack_weight_rows(L.w_idx).view(np.int32)).to(dev())
+    yr = oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr, lut,
+                                       b_w, s_w, L.spec.d_in, accumulate=False)
+    torch.cuda.synchronize()
+    assert_close(yr.cpu().numpy()[rows], ref["y_comp"], "Y' (row layout)")
+    ym = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
+    oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr, lut, b_w,
+                                  s_w, L.spec.d_in, y=ym, accumulate=True)
+    torch.cuda.synchronize()
+    assert_close(ym.cpu().numpy()[rows], ref["y"], "Y (gemm then row-layout compensation)")
     for algo in algos:
         r = oasis.forward(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode, algo)
         torch.cuda.synchronize()
