@@ -374,25 +374,25 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
 // listed outlier reads exactly its own row, d_out / 2 bytes.
 //
 // Workgroup = 4 waves over a slab of 64 words (512 columns) and a tile of
-// WR_TT tokens; wave w takes tokens w, w + 4, ... of the tile.  Lane l owns
+// tt tokens; wave w takes tokens w, w + 4, ... of the tile.  Lane l owns
 // word 64 * slab + l and 8 fp32 accumulators per token.  A token's listed
 // entries are wave-uniform: lane e holds entry e, readlane hands them out in
 // list order, and each entry fetches one word per lane (one contiguous
 // 256-byte piece of row p per wave, 3 * WR_U entries in flight).  A word's four
-// bytes become four pairs of weight centroids through a 64 KiB LDS table -
-// row `byte` holds 32 copies of pair(C_W, byte), so the offset is one
-// v_perm_b32 and the read is conflict free - and each centroid meets the
-// residual in one fp32 FMA.
+// bytes become four pairs of weight centroids through a 32 KiB LDS table -
+// row `byte` holds 32 copies of pair(C_W, byte), lane l reads copy l mod 32,
+// so the reads are conflict free - and each centroid meets the residual in
+// one fp32 FMA (v_fma_mix_f32 takes the fp16 half directly).  48 KiB of LDS
+// per workgroup keeps three workgroups on a CU to hide the row loads.
 // ----------------------------------------------------------------------------
-constexpr int WR_TT = 32;   // tokens per workgroup tile
 constexpr int WR_U = 16;    // entries per unit of word loads
 constexpr int WR_C = 512;   // list entries per wave held in LDS at a time
 
 __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int nslab,
-                                                        int ntile) {
-  // the pair table (bytes [0, 128) of each 256-byte row used) at a fixed LDS
-  // address; dynamic LDS: per wave WR_C channels and WR_C residuals of its lists
-  __shared__ uint32_t tab[256 * 64];
+                                                        int ntile, int tt) {
+  // the pair table at a fixed LDS address; dynamic LDS: per wave WR_C
+  // channels and WR_C residuals of its lists
+  __shared__ uint32_t tab[256 * 32];
   extern __shared__ __align__(16) unsigned char smem_wr[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -403,9 +403,9 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   const int k = A.k, E = 2 * k, d_in = A.d_in, d_out = A.d_out;
 
   // ---- this wave's tokens, in units of WR_U entries
-  const int tok0 = tile * WR_TT;
+  const int tok0 = tile * tt;
   const int tw = tok0 + wave;  // first token of this wave; then every fourth
-  const int tend = min(A.n, tok0 + WR_TT);
+  const int tend = min(A.n, tok0 + tt);
   const int ntw = tw < tend ? (tend - tw + 3) / 4 : 0;
   const int nch = (E + WR_U - 1) / WR_U;  // units per token
   const int U = ntw * nch;
@@ -439,9 +439,10 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   };
   fill(0, min(U, WR_C / WR_U));  // the first chunk's loads overlap the table build
 
-  // pair table: thread t writes chunks c = t + 256 s (s < 8) of 16 bytes:
-  // row c / 8 (low code (t / 8) mod 16, high code t / 128 + 2 s), copies
-  // 4 (c mod 8) .. 4 (c mod 8) + 3
+  // pair table, 32 KiB: row `byte` holds 32 copies of pair(C_W, byte).
+  // Thread t writes chunks c = t + 256 s (s < 8) of 16 bytes: row c / 8 (low
+  // code (t / 8) mod 16, high code t / 128 + 2 s), copies 4 (c mod 8) ..
+  // 4 (c mod 8) + 3
   {
     const uint16_t* cb = A.lut->cb_wgt;
     const uint32_t lo = cb[(tid >> 3) & 15];
@@ -449,7 +450,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
     for (int s = 0; s < 8; ++s) {
       const uint32_t v = lo | ((uint32_t)cb[(tid >> 7) + 2 * s] << 16);
       const uint32_t c = (uint32_t)tid + 256u * (uint32_t)s;
-      *reinterpret_cast<uint4_t*>(&tab[(c >> 3) * 64u + (c & 7u) * 4u]) = uint4_t{v, v, v, v};
+      *reinterpret_cast<uint4_t*>(&tab[(c >> 3) * 32u + (c & 7u) * 4u]) = uint4_t{v, v, v, v};
     }
   }
 
@@ -458,7 +459,9 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   const uint32_t row_bytes = (uint32_t)wn * 4u;
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(A.idx_w), 0, (int)((uint32_t)d_in * row_bytes), 0x00020000);
-  const uint32_t lane4 = (uint32_t)(lane & 31) * 4u;
+  // the offset of byte b's entry, b * 128 + (lane mod 32) * 4, is one
+  // v_perm_b32 (b << 8 | (lane mod 32) * 8) and one shift
+  const uint32_t lane8 = (uint32_t)(lane & 31) * 8u;
   const char* tb = reinterpret_cast<const char*>(tab);
   float sw[8];
 #pragma unroll
@@ -494,7 +497,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
                                           __builtin_amdgcn_readlane(__builtin_bit_cast(int, rl), e));
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const uint32_t off = __builtin_amdgcn_perm(w[e], lane4, 0x0C0C0000u | ((4u + b) << 8));
+        const uint32_t off = __builtin_amdgcn_perm(w[e], lane8, 0x0C0C0000u | ((4u + b) << 8)) >> 1;
         const uint32_t pr = *reinterpret_cast<const uint32_t*>(tb + off);
         acc[2 * b] = fmaf(re, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * b]);
         acc[2 * b + 1] = fmaf(re, h2f((uint16_t)(pr >> 16)), acc[2 * b + 1]);
@@ -576,12 +579,17 @@ hipError_t launch_compensate_wr(const CompArgs& a, hipStream_t s) {
     return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
   }
   const int wn = (a.d_out + 7) / 8;
-  const int nslab = (wn + 63) / 64, ntile = (a.n + WR_TT - 1) / WR_TT;
+  // tokens per tile: every wave's lists fit its LDS area at once (one copy,
+  // no pipeline drain) when 2k <= WR_C / 4 ... WR_C; at most 32
+  const int E = 2 * a.k;
+  const int tt = 4 * max(1, min(8, WR_C / E));
+  const int nslab = (wn + 63) / 64, ntile = (a.n + tt - 1) / tt;
   const size_t lds = 4 * 8 * WR_C;  // dynamic part: the lists
   hipError_t e = hipFuncSetAttribute((const void*)k_compensate_wr,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_compensate_wr, dim3(nslab * ntile), dim3(256), lds, s, a, wn, nslab, ntile);
+  hipLaunchKernelGGL(k_compensate_wr, dim3(nslab * ntile), dim3(256), lds, s, a, wn, nslab, ntile,
+                     tt);
   return hipGetLastError();
 }
 
