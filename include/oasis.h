@@ -125,6 +125,24 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
                        int32_t* max_idx, int32_t* min_idx, float* residual, hipStream_t stream);
 
 /*
+ * oasis_build_lut_quantize_act - oasis_build_lut followed by
+ * oasis_quantize_act, in one launch: the first workgroup of the quantize
+ * kernel also writes the LUT block, and every workgroup takes C_A from the
+ * codebook arguments, so a caller that rebuilds the LUT with every batch pays
+ * no extra launch (the paper builds it once per layer, Sec. IV-A).
+ *   cb_act, b_a, cb_wgt, b_w, lut : as in oasis_build_lut (lut is written;
+ *            the other calls of the step read it after this one).
+ *   x, n, d_in, k, scale_mode and the outputs : as in oasis_quantize_act.
+ *   n == 0 builds the LUT alone.
+ * Errors: those of both calls.
+ */
+int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                                 oasis_lut_block* lut, const uint16_t* x, int n, int d_in, int k,
+                                 int scale_mode, uint8_t* idx_act, float* act_scale,
+                                 int32_t* max_idx, int32_t* min_idx, float* residual,
+                                 hipStream_t stream);
+
+/*
  * oasis_cluster_act - the main branch's share of oasis_quantize_act: scale
  * and cluster index of every channel (Sec. III-C1: the whole token is
  * clustered, outliers included), without outlier detection.  Same arguments

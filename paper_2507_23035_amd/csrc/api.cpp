@@ -90,7 +90,39 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
       !aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4))
     return OASIS_ERR_ALIGN;
   oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
-                     max_idx, min_idx, residual};
+                     max_idx, min_idx, residual, nullptr, {}, 0};
+  return launched(oasis::launch_quantize(a, stream));
+}
+
+int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                                 oasis_lut_block* lut, const uint16_t* x, int n, int d_in, int k,
+                                 int scale_mode, uint8_t* idx_act, float* act_scale,
+                                 int32_t* max_idx, int32_t* min_idx, float* residual,
+                                 hipStream_t stream) {
+  if (!cb_act || !cb_wgt || !lut) return OASIS_ERR_NULL;
+  if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  for (int i = 0; i < (1 << b_a); ++i) {
+    const float v = half_bits_to_float(cb_act[i]);
+    if (!std::isfinite(v)) return OASIS_ERR_CODEBOOK;
+    if (i > 0 && !(v > half_bits_to_float(cb_act[i - 1]))) return OASIS_ERR_CODEBOOK;
+  }
+  for (int i = 0; i < (1 << b_w); ++i)
+    if (!std::isfinite(half_bits_to_float(cb_wgt[i]))) return OASIS_ERR_CODEBOOK;
+  if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
+  if (oasis::quantize_lds_bytes(d_in, k) > kMaxLds) return OASIS_ERR_TOO_LARGE;
+  if (n > 0 && (!x || !act_scale || (d_in > 0 && !idx_act))) return OASIS_ERR_NULL;
+  if (n > 0 && k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(lut, 16) || !aligned(idx_act, 16) || !aligned(act_scale, 4) ||
+      !aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4))
+    return OASIS_ERR_ALIGN;
+  if (n == 0) return launched(oasis::launch_build_lut(cb_act, b_a, cb_wgt, b_w, lut, stream));
+  oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
+                     max_idx, min_idx, residual, lut, {}, b_w};
+  for (int i = 0; i < (1 << b_a); ++i) a.cb.act[i] = cb_act[i];
+  for (int i = 0; i < (1 << b_w); ++i) a.cb.wgt[i] = cb_wgt[i];
   return launched(oasis::launch_quantize(a, stream));
 }
 
@@ -105,7 +137,7 @@ int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block*
   if (!aligned(x, 16) || !aligned(lut, 16) || !aligned(idx_act, 16) || !aligned(act_scale, 4))
     return OASIS_ERR_ALIGN;
   oasis::QuantArgs a{x, n, d_in, b_a, 0, scale_mode, lut, idx_act, act_scale,
-                     nullptr, nullptr, nullptr};
+                     nullptr, nullptr, nullptr, nullptr, {}, 0};
   return launched(oasis::launch_cluster(a, stream));
 }
 
@@ -124,7 +156,7 @@ int oasis_detect_outliers(const uint16_t* x, int n, int d_in, const oasis_lut_bl
       !aligned(residual, 4))
     return OASIS_ERR_ALIGN;
   oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, nullptr, nullptr,
-                     max_idx, min_idx, residual};
+                     max_idx, min_idx, residual, nullptr, {}, 0};
   return launched(oasis::launch_outliers(a, stream));
 }
 

@@ -78,6 +78,27 @@ __device__ __forceinline__ uint64_t block_scan64(uint64_t v, uint64_t* tmp) {
   return v + base;
 }
 // Everything the host launchers need; argument checking happens in api.cpp.
+// Codebooks by value (fp16 bits; entries past 2^b are 0).
+struct Codebooks {
+  uint16_t act[16];
+  uint16_t wgt[16];
+};
+
+// Entry e (< 256) of the LUT block: lut[e] = fp32(C_A[e >> b_w]) *
+// fp32(C_W[e mod 2^b_w]), 0 past 2^(b_a + b_w); for e < 16 also both
+// codebook entries.  A product of two fp16 values has at most 22 significant
+// bits, so it is exact in fp32.
+__device__ __forceinline__ void write_lut_entry(const Codebooks& cb, int b_a, int b_w, int e,
+                                                oasis_lut_block* out) {
+  float v = 0.0f;
+  if (e < (1 << (b_a + b_w))) v = h2f(cb.act[e >> b_w]) * h2f(cb.wgt[e & ((1 << b_w) - 1)]);
+  out->lut[e] = v;
+  if (e < 16) {
+    out->cb_act[e] = e < (1 << b_a) ? cb.act[e] : (uint16_t)0;
+    out->cb_wgt[e] = e < (1 << b_w) ? cb.wgt[e] : (uint16_t)0;
+  }
+}
+
 struct QuantArgs {
   const uint16_t* x;
   int n, d_in, b_a, k, scale_mode;
@@ -87,6 +108,11 @@ struct QuantArgs {
   int32_t* max_idx;
   int32_t* min_idx;
   float* residual;
+  // LUT build in the same launch: when lut_out is set, C_A comes from cb and
+  // workgroup 0 also writes the LUT block (lut is not read)
+  oasis_lut_block* lut_out;
+  Codebooks cb;
+  int b_w;
 };
 
 struct GemmArgs {

@@ -5,26 +5,9 @@
 
 namespace oasis {
 
-struct Codebooks {
-  uint16_t act[16];
-  uint16_t wgt[16];
-};
-
 __global__ void __launch_bounds__(256) k_build_lut(Codebooks cb, int b_a, int b_w,
                                                    oasis_lut_block* __restrict__ out) {
-  const int e = threadIdx.x;  // one entry per thread, 256 threads
-  const int a = e >> b_w;
-  const int w = e & ((1 << b_w) - 1);
-  float v = 0.0f;
-  if (e < (1 << (b_a + b_w))) {
-    // fp16 x fp16 has at most 22 significant bits: exact in fp32.
-    v = h2f(cb.act[a]) * h2f(cb.wgt[w]);
-  }
-  out->lut[e] = v;
-  if (e < 16) {
-    out->cb_act[e] = e < (1 << b_a) ? cb.act[e] : (uint16_t)0;
-    out->cb_wgt[e] = e < (1 << b_w) ? cb.wgt[e] : (uint16_t)0;
-  }
+  write_lut_entry(cb, b_a, b_w, threadIdx.x, out);  // one entry per thread, 256 threads
 }
 
 hipError_t launch_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,

@@ -104,7 +104,12 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     S.hist2[0][tid] = 0;
     S.hist2[1][tid] = 0;
   }
-  if (tid < 16) S.ca[tid] = h2f(A.lut->cb_act[tid]);
+  if (A.lut_out) {  // uniform: the LUT is built in this launch
+    if (tid < 16) S.ca[tid] = h2f(A.cb.act[tid]);
+    if (i == 0 && tid < 256) write_lut_entry(A.cb, A.b_a, A.b_w, tid, A.lut_out);
+  } else if (tid < 16) {
+    S.ca[tid] = h2f(A.lut->cb_act[tid]);
+  }
   if (tid == 0) S.nalloc = 0;
   __syncthreads();  // histograms cleared, C_A staged
 

@@ -24,7 +24,8 @@ LUT_BLOCK_BYTES = 256 * 4 + 16 * 2 + 16 * 2
 EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quantize_act",
            "oasis_cluster_act", "oasis_detect_outliers",
            "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_outlier_compensate_rows",
-           "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows")
+           "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows",
+           "oasis_build_lut_quantize_act")
 
 
 class OasisError(RuntimeError):
@@ -53,6 +54,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_build_lut.argtypes = [P, I, P, I, P, P]
     lib.oasis_quantize_act.restype = I
     lib.oasis_quantize_act.argtypes = [P, I, I, P, I, I, I, P, P, P, P, P, P]
+    lib.oasis_build_lut_quantize_act.restype = I
+    lib.oasis_build_lut_quantize_act.argtypes = [P, I, P, I, P, P, I, I, I, I, P, P, P, P, P, P]
     lib.oasis_cluster_act.restype = I
     lib.oasis_cluster_act.argtypes = [P, I, I, P, I, I, P, P, P]
     lib.oasis_detect_outliers.restype = I
@@ -148,6 +151,33 @@ def quantize_act(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
         _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
         _stream(stream)))
     return out
+
+
+def build_lut_quantize_act(cb_act, b_a: int, cb_wgt, b_w: int, x, k: int,
+                           scale_mode: int = SCALE_ABSMAX, lut=None, out: Optional[Dict] = None,
+                           stream=None):
+    """build_lut then quantize_act in one launch; returns (lut, quantize outputs)."""
+    import torch
+    n, d_in = x.shape
+    dev = x.device
+    if lut is None:
+        lut = torch.empty(LUT_BLOCK_BYTES, dtype=torch.uint8, device=dev)
+    if out is None:
+        out = {
+            "idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=dev),
+            "act_scale": torch.empty(n, dtype=torch.float32, device=dev),
+            "max_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "min_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
+        }
+    ca = _fp16_bits(cb_act)
+    cw = _fp16_bits(cb_wgt)
+    _check("oasis_build_lut_quantize_act", load().oasis_build_lut_quantize_act(
+        ca.ctypes.data, b_a, cw.ctypes.data, b_w, _ptr(lut), _ptr(x), n, d_in, k, scale_mode,
+        _ptr(out["idx_act"]), _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
+        _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
+        _stream(stream)))
+    return lut, out
 
 
 def cluster_act(x, lut, b_a: int, scale_mode: int = SCALE_ABSMAX, out: Optional[Dict] = None,

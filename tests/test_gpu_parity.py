@@ -207,6 +207,36 @@ def test_crowded_boundary_buckets():
     run_full(L)
 
 
+@pytest.mark.parametrize("name,k", [("decode_8x4096x4096", 32), ("tiny_4x256x256", 4),
+                                    ("crowded", 16)])
+def test_build_lut_quantize_in_one_launch(name, k):
+    """The fused LUT build + quantize equals the two calls, bit for bit, and
+    the LUT block equals the oracle's."""
+    if name == "crowded":
+        L = synth.make_layer(synth.custom(5, 1024, 64, k, seed=18))
+        L.x[0, :] = np.float16(1.5)
+    else:
+        L = synth.make_layer(synth.config(name))
+    b_a, b_w = L.spec.b_a, L.spec.b_w
+    x = torch.from_numpy(L.x.view(np.int16).copy()).to(dev())
+    lut1 = oasis.build_lut(L.cb_a, b_a, L.cb_w, b_w)
+    q1 = oasis.quantize_act(x, lut1, b_a, k)
+    lut2 = torch.full_like(lut1, 0xAB)
+    lut2, q2 = oasis.build_lut_quantize_act(L.cb_a, b_a, L.cb_w, b_w, x, k, lut=lut2)
+    torch.cuda.synchronize()
+    assert torch.equal(lut1, lut2)
+    ref = np.zeros(256, dtype=np.float32)
+    ref[: 1 << (b_a + b_w)] = O.build_lut(L.cb_a, L.cb_w, b_a, b_w).astype(np.float32)
+    assert np.array_equal(lut2.cpu().numpy()[:1024].view(np.float32), ref)
+    for key in q1:
+        assert torch.equal(q1[key], q2[key]), key
+    # no tokens: the LUT alone
+    lut3 = torch.zeros_like(lut1)
+    oasis.build_lut_quantize_act(L.cb_a, b_a, L.cb_w, b_w, x[:0], k, lut=lut3)
+    torch.cuda.synchronize()
+    assert torch.equal(lut1, lut3)
+
+
 def test_empty_batch():
     L = synth.make_layer(synth.custom(2, 64, 32, 2, seed=13))
     x, idx_w, s_w, lut = upload(L)
