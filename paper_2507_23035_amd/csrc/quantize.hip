@@ -104,14 +104,29 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     S.hist2[0][tid] = 0;
     S.hist2[1][tid] = 0;
   }
-  if (A.lut_out) {  // uniform: the LUT is built in this launch
-    if (tid < 16) S.ca[tid] = h2f(A.cb.act[tid]);
-    if (i == 0 && tid < 256) write_lut_entry(A.cb, A.b_a, A.b_w, tid, A.lut_out);
-  } else if (tid < 16) {
-    S.ca[tid] = h2f(A.lut->cb_act[tid]);
+  // C_A[lane] and C_A[lane + 1] (the boundary mid-points need both) from the
+  // codebook arguments when the LUT is built in this launch, else from the
+  // LUT block; requested now, used after the keys are made
+  const bool build = A.lut_out != nullptr;  // uniform
+  uint32_t cal = 0, cah = 0;
+  if (lane < 16) cal = build ? A.cb.act[lane] : A.lut->cb_act[lane];
+  if (lane < 15) cah = build ? A.cb.act[lane + 1] : A.lut->cb_act[lane + 1];
+  // workgroup 0 of a building launch: the codebook entries of LUT entry tid
+  const bool lut_writer = build && i == 0 && tid < 256;
+  const int lut_e = tid, lut_a = tid >> A.b_w, lut_w = tid & ((1 << A.b_w) - 1);
+  uint32_t lua = 0, luw = 0, lcw = 0;
+  if (lut_writer && lut_e < (1 << (A.b_a + A.b_w))) {
+    lua = A.cb.act[lut_a];
+    luw = A.cb.wgt[lut_w];
+  }
+  if (lut_writer && tid < 16) lcw = A.cb.wgt[tid];
+  if (tid < 256) {
+    S.hist1[tid] = 0;
+    S.hist2[0][tid] = 0;
+    S.hist2[1][tid] = 0;
   }
   if (tid == 0) S.nalloc = 0;
-  __syncthreads();  // histograms cleared, C_A staged
+  __syncthreads();  // histograms cleared
 
   // keys, two per word (even channel low)
   uint32_t key[VR][4];
@@ -138,7 +153,18 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   // boundary mid-points b_c = fp32(C_A[c] + C_A[c+1]) * 0.5 in lane c (they
   // do not depend on the token)
   const int nb = (1 << A.b_a) - 1;
-  const float bc = lane < nb ? (S.ca[lane] + S.ca[lane + 1]) * 0.5f : 0.0f;
+  const float bc = lane < nb ? (h2f((uint16_t)cal) + h2f((uint16_t)cah)) * 0.5f : 0.0f;
+  if (tid < 16) S.ca[tid] = h2f((uint16_t)cal);  // read after later barriers
+  if (lut_writer) {
+    // the LUT block (the contents oasis_build_lut writes); a product of two
+    // fp16 values is exact in fp32
+    A.lut_out->lut[lut_e] = lut_e < (1 << (A.b_a + A.b_w)) ? h2f((uint16_t)lua) * h2f((uint16_t)luw)
+                                                          : 0.0f;
+    if (tid < 16) {  // entries past 2^b are 0 in the arguments
+      A.lut_out->cb_act[tid] = (uint16_t)cal;
+      A.lut_out->cb_wgt[tid] = (uint16_t)lcw;
+    }
+  }
   amax = wave_max(amax);
   if (lane == 0) S.wmax[wave] = amax;
   __syncthreads();  // absmax partials, level-1 histogram
