@@ -19,6 +19,7 @@ Prints ONE JSON line (rank 0).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -208,6 +209,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="decode_8x4096x4096")
     ap.add_argument("--algo", default="mfma", choices=["mfma", "lut"])
+    ap.add_argument("--bits-a", type=int, default=0, choices=[0, 1, 2, 3, 4],
+                    help="activation bits (0: the config's, 4); 3 is the paper's W4A3 point")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
     ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate", "lookahead"],
@@ -240,7 +243,10 @@ def main():
         return
     oasis.load()
     dev = torch.device("cuda:0")
-    layer = synth.make_layer(synth.config(args.config))
+    spec = synth.config(args.config)
+    if args.bits_a and args.bits_a != spec.b_a:
+        spec = dataclasses.replace(spec, b_a=args.bits_a, name=f"{spec.name}_a{args.bits_a}")
+    layer = synth.make_layer(spec)
     s = layer.spec
     n, d_in, d_out, k, b_a, b_w = s.n, s.d_in, s.d_out, s.k, s.b_a, s.b_w
     algo = oasis.ALGO_MFMA if args.algo == "mfma" else oasis.ALGO_LUT

@@ -5,6 +5,8 @@ and the residuals (one fp32 rounding on both sides) must match bit for bit.
 fp32 outputs must satisfy |y - y_ref| <= max(1e-3 * |y_ref|, 1e-2) for every
 entry, y_ref being the oracle's fp64 result.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -267,6 +269,16 @@ def test_repeated_calls_are_stable():
 # ----------------------------------------------------------------------------
 FULL = ["prefill_up_2048x4096x11008", "prefill_down_2048x11008x4096",
         "large_decode_16x8192x28672", "large_prefill_4096x8192x28672"]
+
+
+@pytest.mark.parametrize("name", ["decode_8x4096x4096", "prefill_up_2048x4096x11008"])
+def test_w4a3_layers(name):
+    """The paper's second precision point: 3-bit activations (8 centroids, a
+    128-entry LUT), codes still one per nibble."""
+    L = synth.make_layer(dataclasses.replace(synth.config(name), b_a=3, name=f"{name}_a3"))
+    n = L.spec.n
+    tokens = None if n <= 8 else sorted({0, n - 1, 777, 1500})
+    run_full(L, tokens=tokens)
 
 
 @pytest.mark.parametrize("name", FULL)
