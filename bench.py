@@ -67,6 +67,7 @@ def call_bytes(n, d_in, d_out, k, path):
         "build_lut": 2 * 32 + 1088,
         "quantize_act": x + codes + 4 * n + lists,
         "build_lut_quantize_act": x + codes + 4 * n + lists + 1088,
+        "quantize_act_static": x + codes + 4 * n + lists,
         "cluster_act": x + codes + 4 * n,
         "detect_outliers": x + lists,
         "outlier_compensate": comp,
@@ -78,7 +79,7 @@ def call_bytes(n, d_in, d_out, k, path):
 KERNEL_SOURCES = {
     "build_lut": ["lut.hip"],
     "quantize_act": ["quantize.hip"], "cluster_act": ["quantize.hip"],
-    "build_lut_quantize_act": ["quantize.hip"],
+    "build_lut_quantize_act": ["quantize.hip"], "quantize_act_static": ["quantize.hip"],
     "detect_outliers": ["quantize.hip"],
     "outlier_compensate": ["compensate.hip"],
     "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
@@ -110,7 +111,7 @@ def measured_traffic(call, workload):
 
 CALL_SYMBOLS = {   # kernel symbol fragment of each call's dominant kernel
     "build_lut": "k_build_lut", "quantize_act": "k_quantize<", "cluster_act": "k_quantize<",
-    "build_lut_quantize_act": "k_quantize<",
+    "build_lut_quantize_act": "k_quantize<", "quantize_act_static": "k_quantize<",
     "detect_outliers": "k_quantize<", "outlier_compensate": "k_compensate",
     "lut_gemm": "k_gemm_mfma", "lut_gemm_compensated": "k_gemm_mfma",
 }
@@ -209,6 +210,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="decode_8x4096x4096")
     ap.add_argument("--algo", default="mfma", choices=["mfma", "lut"])
+    ap.add_argument("--oasis-s", action="store_true",
+                    help="OASIS-S: outliers from fixed thresholds (the mean k-th extreme "
+                         "values of the calibration tokens), 2k places per side")
     ap.add_argument("--bits-a", type=int, default=0, choices=[0, 1, 2, 3, 4],
                     help="activation bits (0: the config's, 4); 3 is the paper's W4A3 point")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
@@ -246,9 +250,19 @@ def main():
     spec = synth.config(args.config)
     if args.bits_a and args.bits_a != spec.b_a:
         spec = dataclasses.replace(spec, b_a=args.bits_a, name=f"{spec.name}_a{args.bits_a}")
+    if args.oasis_s:
+        if args.path == "lookahead":
+            print("bench.py: --oasis-s has no look-ahead schedule (no top-k to overlap)",
+                  file=sys.stderr)
+            sys.exit(2)
+        spec = dataclasses.replace(spec, name=f"{spec.name}_oasis_s")
     layer = synth.make_layer(spec)
     s = layer.spec
     n, d_in, d_out, k, b_a, b_w = s.n, s.d_in, s.d_out, s.k, s.b_a, s.b_w
+    thr = None
+    if args.oasis_s:   # thresholds at the k-th extremes; twice the places per side
+        thr = synth.static_thresholds(layer, k)
+        k = 2 * k
     algo = oasis.ALGO_MFMA if args.algo == "mfma" else oasis.ALGO_LUT
 
     wbytes = d_in * d_out // 2
@@ -284,6 +298,8 @@ def main():
         "quantize_act": lambda c: oasis.quantize_act(x, lut, b_a, k, out=q),
         "build_lut_quantize_act": lambda c: oasis.build_lut_quantize_act(
             cb_a, b_a, cb_w, b_w, x, k, lut=lut, out=q),
+        "quantize_act_static": lambda c: oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1],
+                                                                   out=q),
         "cluster_act": lambda c: oasis.cluster_act(x, lut, b_a, out=q),
         "detect_outliers": lambda c: oasis.detect_outliers(x, lut, b_a, k, out=q),
         "outlier_compensate": lambda c: oasis.outlier_compensate_rows(
@@ -296,14 +312,24 @@ def main():
             q["min_idx"], q["residual"], y=y),
     }
     if path == "fused":
-        names = ["build_lut_quantize_act", "lut_gemm_compensated"]
+        names = (["build_lut", "quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
+            ["lut_gemm_compensated"]
         gemm_name = "lut_gemm_compensated"
     elif path == "lookahead":
         names = ["build_lut", "cluster_act", "detect_outliers", "lut_gemm", "outlier_compensate"]
         gemm_name = "lut_gemm"
     else:
-        names = ["build_lut_quantize_act", "outlier_compensate", "lut_gemm"]
+        names = (["build_lut", "quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
+            ["outlier_compensate", "lut_gemm"]
         gemm_name = "lut_gemm"
+
+    def quantize(L):
+        """LUT block + quantization: one launch, or two for OASIS-S."""
+        if thr:
+            oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
+            oasis.quantize_act_static(x, L, b_a, k, thr[0], thr[1], out=q)
+        else:
+            oasis.build_lut_quantize_act(cb_a, b_a, cb_w, b_w, x, k, lut=L, out=q)
 
     def step(i):
         """Step i (weight copy i mod copies)."""
@@ -313,7 +339,7 @@ def main():
         if path == "fused":
             # the LUT block is rebuilt with every step (Sec. IV-A builds it once
             # per layer), inside the quantize launch
-            oasis.build_lut_quantize_act(cb_a, b_a, cb_w, b_w, x, k, lut=L, out=q)
+            quantize(L)
             oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w,
                                        q["max_idx"], q["min_idx"], q["residual"], y=y)
         elif path == "lookahead":
@@ -329,7 +355,7 @@ def main():
             oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr[c],
                                           L, b_w, s_w, d_in, y=y, accumulate=True)
         else:
-            oasis.build_lut_quantize_act(cb_a, b_a, cb_w, b_w, x, k, lut=L, out=q)
+            quantize(L)
             oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr[c],
                                           L, b_w, s_w, d_in, y=y, accumulate=False)
             oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo, y=y,
@@ -386,10 +412,13 @@ def main():
     last = args.warmup + nsteps - 1
     c_last = last % copies
     oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
+    q1 = oasis.quantize_act(x, lut, b_a, k) if not thr else \
+        oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1])
     if path == "fused":
-        y_ref = oasis.forward(x, lut, idx_w[c_last], s_w, b_a, b_w, k, algo=algo, fused=True)["y"]
+        y_ref = oasis.lut_gemm_compensated(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w,
+                                           lut, b_a, b_w, q1["max_idx"], q1["min_idx"],
+                                           q1["residual"])
     else:
-        q1 = oasis.quantize_act(x, lut, b_a, k)
         if path == "lookahead":
             y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a,
                                    b_w, algo)
@@ -467,7 +496,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "n": n, "d_in": d_in, "d_out": d_out, "k_per_side": k,
                    "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
-                   "path": path,
+                   "path": path, "outliers": "static" if thr else "top-k",
                    "weight_copies": copies},
         "schedule_check": schedule_ok,
         "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),

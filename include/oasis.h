@@ -125,6 +125,23 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
                        int32_t* max_idx, int32_t* min_idx, float* residual, hipStream_t stream);
 
 /*
+ * oasis_quantize_act_static - OASIS-S (Sec. V-A): the outliers are found with
+ * fixed thresholds learned offline instead of the per-token top-k.
+ *   Scale and codes as in oasis_quantize_act.  The max list holds the
+ *   channels with x >= thr_hi, the min list those with x <= thr_lo, each in
+ *   channel order and at most k of them (k = places per side); the places
+ *   left hold channel -1 and residual 0 (the compensation calls skip them).
+ *   Residuals as in oasis_quantize_act.  thr_lo < thr_hi, neither NaN
+ *   (+-inf allowed).
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, MODE (scale mode or thresholds),
+ * TOO_LARGE, LAUNCH.
+ */
+int oasis_quantize_act_static(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut,
+                              int b_a, int k, int scale_mode, float thr_hi, float thr_lo,
+                              uint8_t* idx_act, float* act_scale, int32_t* max_idx,
+                              int32_t* min_idx, float* residual, hipStream_t stream);
+
+/*
  * oasis_build_lut_quantize_act - oasis_build_lut followed by
  * oasis_quantize_act, in one launch: the first workgroup of the quantize
  * kernel also writes the LUT block, and every workgroup takes C_A from the

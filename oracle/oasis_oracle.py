@@ -35,6 +35,10 @@ design notes of the repository):
   R8  Residual r = fp32(x - fp32(t * C_A[a])), one fp32 rounding (the
       Error Calculation Unit of Sec. IV-A, in fp32 instead of fp16).
   R9  Accumulation is exact-ish (fp64 here); the GPU accumulates in fp32.
+  R11 OASIS-S (Sec. V-A: thresholds reused from the offline calibration):
+      the max list holds the channels with x >= thr_hi, the min list those
+      with x <= thr_lo, in channel order, at most k each; unused places hold
+      channel -1 and residual 0.
 """
 from __future__ import annotations
 
@@ -257,13 +261,15 @@ def residuals(x: np.ndarray, t: np.ndarray, a: np.ndarray, cb_a: np.ndarray,
     xh = dequant_act(a, t, cb_a)
     r = np.zeros((n, 2 * k), dtype=np.float32)
     for i in range(n):
-        in_max = set(int(p) for p in max_idx[i])
+        in_max = set(int(p) for p in max_idx[i] if p >= 0)
         for e in range(k):
             p = int(max_idx[i, e])
-            r[i, e] = np.float32(x32[i, p] - xh[i, p])
+            if p >= 0:                      # -1: an unused place (R11)
+                r[i, e] = np.float32(x32[i, p] - xh[i, p])
         for e in range(k):
             p = int(min_idx[i, e])
-            r[i, k + e] = np.float32(0.0) if p in in_max else np.float32(x32[i, p] - xh[i, p])
+            if p >= 0:
+                r[i, k + e] = np.float32(0.0) if p in in_max else np.float32(x32[i, p] - xh[i, p])
     return r
 
 
@@ -367,10 +373,39 @@ def quantize_act(x: np.ndarray, cb_a: np.ndarray, b_a: int, k: int,
     return {"t": t, "a": a, "max_idx": mx, "min_idx": mn, "residual": r}
 
 
+def static_lists(x: np.ndarray, thr_hi: float, thr_lo: float,
+                 k: int) -> Tuple[np.ndarray, np.ndarray]:
+    """OASIS-S outlier lists (R11): channels at or beyond the fixed thresholds,
+    in channel order, at most k per side, -1 in the places left."""
+    xv = np.asarray(x, dtype=np.float16).astype(np.float64)
+    hi, lo = float(np.float32(thr_hi)), float(np.float32(thr_lo))
+    n = xv.shape[0]
+    mx = np.full((n, k), -1, dtype=np.int32)
+    mn = np.full((n, k), -1, dtype=np.int32)
+    for i in range(n):
+        up = [p for p in range(xv.shape[1]) if xv[i, p] >= hi][:k]
+        dn = [p for p in range(xv.shape[1]) if xv[i, p] <= lo][:k]
+        mx[i, :len(up)] = up
+        mn[i, :len(dn)] = dn
+    return mx, mn
+
+
+def quantize_act_static(x: np.ndarray, cb_a: np.ndarray, b_a: int, k: int, thr_hi: float,
+                        thr_lo: float, mode: int = SCALE_ABSMAX) -> Dict[str, np.ndarray]:
+    """OASIS-S: scale and indices as in quantize_act, lists from fixed thresholds."""
+    t = act_scale(x, mode)
+    a = cluster(x, t, cb_a, b_a)
+    mx, mn = static_lists(x, thr_hi, thr_lo, k)
+    r = residuals(x, t, a, cb_a, mx, mn)
+    return {"t": t, "a": a, "max_idx": mx, "min_idx": mn, "residual": r}
+
+
 def forward(x, w_idx, cb_w, s_w, cb_a, b_a: int, b_w: int, k: int,
-            mode: int = SCALE_ABSMAX, tokens=None) -> Dict[str, np.ndarray]:
-    """Look-ahead LUT-GEMM plus error compensation: Y = Y* + Y' (Sec. III-C)."""
-    q = quantize_act(x, cb_a, b_a, k, mode)
+            mode: int = SCALE_ABSMAX, tokens=None, thresholds=None) -> Dict[str, np.ndarray]:
+    """Look-ahead LUT-GEMM plus error compensation: Y = Y* + Y' (Sec. III-C);
+    thresholds = (thr_hi, thr_lo) selects OASIS-S lists (R11)."""
+    q = quantize_act(x, cb_a, b_a, k, mode) if thresholds is None else \
+        quantize_act_static(x, cb_a, b_a, k, thresholds[0], thresholds[1], mode)
     lut = build_lut(cb_a, cb_w, b_a, b_w)
     ys = lut_gemm(q["a"], w_idx, lut, q["t"], s_w, b_w, tokens=tokens)
     yc = outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], w_idx, cb_w, s_w,

@@ -94,6 +94,28 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
   return launched(oasis::launch_quantize(a, stream));
 }
 
+int oasis_quantize_act_static(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut,
+                              int b_a, int k, int scale_mode, float thr_hi, float thr_lo,
+                              uint8_t* idx_act, float* act_scale, int32_t* max_idx,
+                              int32_t* min_idx, float* residual, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (std::isnan(thr_hi) || std::isnan(thr_lo) || !(thr_lo < thr_hi)) return OASIS_ERR_MODE;
+  if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
+  if (oasis::quantize_lds_bytes(d_in, k) > kMaxLds) return OASIS_ERR_TOO_LARGE;
+  if (n == 0) return OASIS_OK;
+  if (!x || !lut || !act_scale || (d_in > 0 && !idx_act)) return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(lut, 16) || !aligned(idx_act, 16) || !aligned(act_scale, 4) ||
+      !aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4))
+    return OASIS_ERR_ALIGN;
+  oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
+                     max_idx, min_idx, residual, nullptr, {}, 0, 1, thr_hi, thr_lo};
+  return launched(oasis::launch_quantize(a, stream));
+}
+
 int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
                                  oasis_lut_block* lut, const uint16_t* x, int n, int d_in, int k,
                                  int scale_mode, uint8_t* idx_act, float* act_scale,

@@ -113,6 +113,9 @@ struct QuantArgs {
   oasis_lut_block* lut_out;
   Codebooks cb;
   int b_w;
+  // OASIS-S: outliers are x >= thr_hi and x <= thr_lo (k = places per side)
+  int static_thr;
+  float thr_hi, thr_lo;
 };
 
 struct GemmArgs {

@@ -143,10 +143,12 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     }
     if (topk && live) {
       reinterpret_cast<uint4*>(xs)[tid * VR + u] = xv[u];
+      if (!A.static_thr) {  // uniform: fixed thresholds need no histogram
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        atomicAdd(&S.hist1[(key[u][q] >> 8) & 0xFFu], 1u);
-        atomicAdd(&S.hist1[key[u][q] >> 24], 1u);
+        for (int q = 0; q < 4; ++q) {
+          atomicAdd(&S.hist1[(key[u][q] >> 8) & 0xFFu], 1u);
+          atomicAdd(&S.hist1[key[u][q] >> 24], 1u);
+        }
       }
     }
   }
@@ -249,6 +251,95 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
       __syncthreads();  // bucket table
       make_codes();
       store_codes();
+    }
+    return;
+  }
+  const size_t krow = (size_t)i * k;
+  const size_t rrow = (size_t)i * 2 * k;
+  // one bit per channel of the thread: 32-bit masks while they suffice
+  using mask_t = typename std::conditional<(8 * VR <= 32), uint32_t, uint64_t>::type;
+
+  if (A.static_thr) {  // uniform
+    // ---- OASIS-S: the outliers are the channels at or beyond two fixed
+    // thresholds, listed in channel order, at most k per side; the places
+    // left are padded with channel -1 and residual 0.  x >= thr_hi exactly
+    // when key(x) >= key(Q), Q the smallest fp16 (or +inf) not below thr_hi;
+    // x <= thr_lo when key(x) <= key(Q'), Q' the largest fp16 not above it.
+    const _Float16 fh = (_Float16)A.thr_hi, fl = (_Float16)A.thr_lo;  // nearest even
+    const uint32_t KH = ord_key(__builtin_bit_cast(uint16_t, fh)) + ((float)fh < A.thr_hi ? 1u : 0u);
+    const uint32_t KL = ord_key(__builtin_bit_cast(uint16_t, fl)) - ((float)fl > A.thr_lo ? 1u : 0u);
+    __syncthreads();  // bucket table
+    make_codes();
+    if (CLUSTER) store_codes();
+    mask_t mmax = 0, mmin = 0;
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      if (tid * VR + u < nvec) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t kk = (key[u][q] >> (16 * hh)) & 0xFFFFu;
+            mmax |= (mask_t)(kk >= KH ? 1u : 0u) << (8 * u + 2 * q + hh);
+            mmin |= (mask_t)(kk <= KL ? 1u : 0u) << (8 * u + 2 * q + hh);
+          }
+        }
+      }
+    }
+    // channel-order ranks: block exclusive scans of the per-thread counts
+    // (two scans: a side may hold all 65536 channels)
+    const uint32_t cmx = (uint32_t)__builtin_popcountll((uint64_t)mmax);
+    const uint32_t cmn = (uint32_t)__builtin_popcountll((uint64_t)mmin);
+    const uint32_t imx = wave_incl_scan(cmx), imn = wave_incl_scan(cmn);
+    uint32_t* wtot_min = S.hist2[0];  // the level-2 histograms are unused here
+    if (lane == 63) {
+      S.wtot[wave] = imx;
+      wtot_min[wave] = imn;
+    }
+    __syncthreads();  // wave totals
+    uint32_t smax = imx - cmx, smin = imn - cmn, totmax = 0, totmin = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t a = S.wtot[w], b = wtot_min[w];
+      smax += w < wave ? a : 0u;
+      smin += w < wave ? b : 0u;
+      totmax += a;
+      totmin += b;
+    }
+    mask_t m = mmax | mmin;
+    const uint32_t p0 = 8u * (uint32_t)(tid * VR);
+    while (m) {
+      const int e = __builtin_ctzll((uint64_t)m);
+      m &= m - 1;
+      uint32_t cw = codes[0];
+#pragma unroll
+      for (int u = 1; u < VR; ++u) cw = (e >> 3) == u ? codes[u] : cw;
+      const uint32_t a = (cw >> (4 * (e & 7))) & 15u;
+      const uint32_t p = p0 + (uint32_t)e;
+      // t * C_A[a] is exact, a product of two fp16 values
+      const float r = h2f(xs[p]) - t * S.ca[a];
+      const bool im = ((mmax >> e) & 1u) != 0u, in = ((mmin >> e) & 1u) != 0u;
+      const bool listed_max = im && smax < (uint32_t)k;
+      if (listed_max) {
+        A.max_idx[krow + smax] = (int)p;
+        A.residual[rrow + smax] = r;
+      }
+      if (in && smin < (uint32_t)k) {
+        A.min_idx[krow + smin] = (int)p;
+        A.residual[rrow + k + smin] = listed_max ? 0.0f : r;  // compensated once
+      }
+      smax += im ? 1u : 0u;
+      smin += in ? 1u : 0u;
+    }
+    for (int e = tid; e < k; e += NT) {
+      if ((uint32_t)e >= totmax) {
+        A.max_idx[krow + e] = -1;
+        A.residual[rrow + e] = 0.0f;
+      }
+      if ((uint32_t)e >= totmin) {
+        A.min_idx[krow + e] = -1;
+        A.residual[rrow + k + e] = 0.0f;
+      }
     }
     return;
   }
@@ -382,8 +473,6 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   if (CLUSTER) store_codes();
 
   // ---- list membership, one bit per channel
-  // one bit per channel of the thread: 32-bit masks while they suffice
-  using mask_t = typename std::conditional<(8 * VR <= 32), uint32_t, uint64_t>::type;
   mask_t mmax = 0, mmin = 0;
   if (!cut) {
 #pragma unroll
@@ -496,8 +585,6 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   // min list.  P lanes share an entry, each counting the entries that pop
   // before it over every P-th quad; a DPP sum combines the P counts.  Sort
   // keys (key, channel) are distinct, so the ranks are the list positions.
-  const size_t krow = (size_t)i * k;
-  const size_t rrow = (size_t)i * 2 * k;
   {
     constexpr int HALF = NT / 2;
     const bool is_max = wave < NW / 2;  // uniform

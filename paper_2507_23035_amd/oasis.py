@@ -25,7 +25,7 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_cluster_act", "oasis_detect_outliers",
            "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_outlier_compensate_rows",
            "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows",
-           "oasis_build_lut_quantize_act")
+           "oasis_build_lut_quantize_act", "oasis_quantize_act_static")
 
 
 class OasisError(RuntimeError):
@@ -54,6 +54,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_build_lut.argtypes = [P, I, P, I, P, P]
     lib.oasis_quantize_act.restype = I
     lib.oasis_quantize_act.argtypes = [P, I, I, P, I, I, I, P, P, P, P, P, P]
+    F = ctypes.c_float
+    lib.oasis_quantize_act_static.restype = I
+    lib.oasis_quantize_act_static.argtypes = [P, I, I, P, I, I, I, F, F, P, P, P, P, P, P]
     lib.oasis_build_lut_quantize_act.restype = I
     lib.oasis_build_lut_quantize_act.argtypes = [P, I, P, I, P, P, I, I, I, I, P, P, P, P, P, P]
     lib.oasis_cluster_act.restype = I
@@ -148,6 +151,30 @@ def quantize_act(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
     _check("oasis_quantize_act", load().oasis_quantize_act(
         _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode, _ptr(out["idx_act"]),
         _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
+        _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
+        _stream(stream)))
+    return out
+
+
+def quantize_act_static(x, lut, b_a: int, k: int, thr_hi: float, thr_lo: float,
+                        scale_mode: int = SCALE_ABSMAX, out: Optional[Dict] = None,
+                        stream=None) -> Dict:
+    """OASIS-S: scale and codes, outlier lists from fixed thresholds (k places
+    per side, channel -1 / residual 0 where unused)."""
+    import torch
+    n, d_in = x.shape
+    dev = x.device
+    if out is None:
+        out = {
+            "idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=dev),
+            "act_scale": torch.empty(n, dtype=torch.float32, device=dev),
+            "max_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "min_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
+        }
+    _check("oasis_quantize_act_static", load().oasis_quantize_act_static(
+        _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode, float(thr_hi), float(thr_lo),
+        _ptr(out["idx_act"]), _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
         _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
         _stream(stream)))
     return out

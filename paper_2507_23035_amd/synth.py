@@ -197,6 +197,17 @@ def make_layer(spec: LayerSpec) -> Layer:
     return Layer(spec, x, w_idx, cb_w, s_w, cb_a, heavy, clipped)
 
 
+def static_thresholds(layer: Layer, k: int):
+    """Offline outlier thresholds for OASIS-S (Sec. V-A): the mean over the
+    layer's calibration tokens of the k-th largest and the k-th smallest
+    value, as fp32 (thr_hi, thr_lo)."""
+    spec = layer.spec
+    _, _, _, rng_cal = _streams(spec.seed)
+    cal = to_fp16_saturating(_draw_tokens(rng_cal, spec, spec.calib_tokens, layer.heavy))
+    srt = np.sort(cal.astype(np.float64), axis=1)
+    return float(np.float32(srt[:, -k].mean())), float(np.float32(srt[:, k - 1].mean()))
+
+
 def config(name: str, **overrides) -> LayerSpec:
     spec = CONFIGS[name]
     return replace(spec, **overrides) if overrides else spec

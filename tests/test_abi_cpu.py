@@ -115,6 +115,21 @@ def test_build_lut_quantize_errors(lib):
     assert f(A, 4, W, 4, P, None, 4, 16, 1, 0, P, P, P, P, P, None) == -1
 
 
+def test_quantize_static_errors(lib):
+    f = lib.oasis_quantize_act_static
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                  ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float] + \
+        [ctypes.c_void_p] * 5 + [ctypes.c_void_p]
+    assert f(P, 4, 12, P, 4, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -2
+    assert f(P, 4, 16, P, 5, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -3
+    assert f(P, 4, 16, P, 4, 17, 0, 2.0, -2.0, P, P, P, P, P, None) == -4
+    assert f(P, 4, 16, P, 4, 1, 0, -2.0, 2.0, P, P, P, P, P, None) == -7     # lo >= hi
+    assert f(P, 4, 16, P, 4, 1, 0, float("nan"), -2.0, P, P, P, P, P, None) == -7
+    assert f(None, 4, 16, P, 4, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -1
+    assert f(MIS, 4, 16, P, 4, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -6
+    assert f(P, 0, 16, None, 4, 1, 0, 2.0, -2.0, None, None, None, None, None, None) == 0
+
+
 def test_cluster_and_detect_errors(lib):
     c = lib.oasis_cluster_act
     assert c(P, 4, 12, P, 4, 0, P, P, None) == -2

@@ -239,6 +239,35 @@ def test_build_lut_quantize_in_one_launch(name, k):
     assert torch.equal(lut1, lut3)
 
 
+@pytest.mark.parametrize("name,k,thr", [
+    ("decode_8x4096x4096", 64, None),          # thresholds from calibration tokens
+    ("custom", 8, (1.25, -1.25)),              # capped lists and unused places
+    ("custom", 40, (0.0, -0.0625)),            # thresholds at and next to zero
+])
+def test_static_thresholds(name, k, thr):
+    """OASIS-S lists, residuals and the whole layer against the oracle."""
+    if name == "custom":
+        L = synth.make_layer(synth.custom(6, 520, 72, k, seed=21))
+    else:
+        L = synth.make_layer(synth.config(name))
+    if thr is None:   # offline: mean of the calibration tokens' k/2-th extreme values
+        thr = synth.static_thresholds(L, k // 2)
+    b_a, b_w = L.spec.b_a, L.spec.b_w
+    x, idx_w, s_w, lut = upload(L)
+    ref = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, b_a, b_w, k, thresholds=thr)
+    q = oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1])
+    check_quant(q, ref, k)
+    y = oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w,
+                                   q["max_idx"], q["min_idx"], q["residual"])
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy(), ref["y"], "Y (static thresholds, fused)")
+    idx_wr = torch.from_numpy(oasis.pack_weight_rows(L.w_idx).view(np.int32)).to(dev())
+    yc = oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr, lut,
+                                       b_w, s_w, L.spec.d_in, accumulate=False)
+    torch.cuda.synchronize()
+    assert_close(yc.cpu().numpy(), ref["y_comp"], "Y' (static thresholds, row layout)")
+
+
 def test_empty_batch():
     L = synth.make_layer(synth.custom(2, 64, 32, 2, seed=13))
     x, idx_w, s_w, lut = upload(L)

@@ -236,6 +236,54 @@ def test_duplicate_channels_compensated_once():
     assert np.all(q["residual"][0, :4] != 0)
 
 
+# ---------------------------------------------------------------- Sec. V-A, OASIS-S
+def test_static_lists_by_hand():
+    """Fixed thresholds: the channels at or beyond them, in channel order,
+    capped at k per side, -1 in the places left (read by hand)."""
+    x = np.array([[0.5, 3.0, -4.0, 2.5, -0.125, 7.0, -1.0, 2.0]], dtype=np.float16)
+    mx, mn = O.static_lists(x, 2.5, -1.0, 4)
+    assert mx.tolist() == [[1, 3, 5, -1]]
+    assert mn.tolist() == [[2, 6, -1, -1]]
+    mx, mn = O.static_lists(x, 2.5, -1.0, 2)
+    assert mx.tolist() == [[1, 3]] and mn.tolist() == [[2, 6]]
+    # a threshold between two fp16 values: 2.4 keeps 2.5 and drops 2.0
+    mx, _ = O.static_lists(x, 2.4, -9.0, 8)
+    assert mx[0, :3].tolist() == [1, 3, 5] and mx[0, 3] == -1
+
+
+def test_static_lists_equal_topk_sets_at_the_kth_values():
+    """With the thresholds at a token's k-th largest and k-th smallest value
+    (distinct values) the static lists hold exactly the top-k sets."""
+    rng = np.random.default_rng(4)
+    for k in (1, 3, 10):
+        x = rng.permutation(np.arange(-50, 50)).astype(np.float16)[None, :] / np.float16(8)
+        x = x.astype(np.float16)
+        srt = np.sort(x[0].astype(np.float64))
+        mx, mn = O.static_lists(x, srt[-k], srt[k - 1], k)
+        tmx, tmn = O.topk_lists(x, k)
+        assert set(mx[0].tolist()) == set(tmx[0].tolist())
+        assert set(mn[0].tolist()) == set(tmn[0].tolist())
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_static_forward_equals_conventional_scheme(seed):
+    """OASIS-S still gives quantized inliers plus fp16 outliers (Sec. II-C),
+    unused places adding nothing."""
+    L = small_layer(n=6, d_in=24, d_out=10, k=3, seed=seed)
+    r = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, 4, 4, 3, thresholds=(1.5, -1.5))
+    what = L.cb_w.astype(np.float64)[L.w_idx] * L.s_w.astype(np.float64)[None, :]
+    mixed = r["t"].astype(np.float64)[:, None] * L.cb_a.astype(np.float64)[r["a"]]
+    for i in range(L.x.shape[0]):
+        for p in set(r["max_idx"][i]) | set(r["min_idx"][i]):
+            if p >= 0:
+                mixed[i, p] = float(L.x[i, p])
+    assert (r["max_idx"] == -1).any()        # some places unused
+    ref = mixed @ what
+    scale = np.abs(mixed) @ np.abs(what)
+    assert np.all(np.abs(r["y"] - ref) <= 2.0 ** -22 * scale + 1e-12)
+    assert np.all(r["residual"][:, :3][r["max_idx"] == -1] == 0)
+
+
 # ---------------------------------------------------------------- Table I
 def test_cost_model_closed_forms():
     c = O.cost_model(4096, 4096, 4, 4)
