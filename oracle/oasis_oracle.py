@@ -35,7 +35,7 @@ design notes of the repository):
   R8  Residual r = fp32(x - fp32(t * C_A[a])), one fp32 rounding (the
       Error Calculation Unit of Sec. IV-A, in fp32 instead of fp16).
   R9  Accumulation is exact-ish (fp64 here); the GPU accumulates in fp32.
-  R11 OASIS-S (Sec. V-A: thresholds reused from the offline calibration):
+  R12 OASIS-S (Sec. V-A: thresholds reused from the offline calibration):
       the max list holds the channels with x >= thr_hi, the min list those
       with x <= thr_lo, in channel order, at most k each; unused places hold
       channel -1 and residual 0.
@@ -264,7 +264,7 @@ def residuals(x: np.ndarray, t: np.ndarray, a: np.ndarray, cb_a: np.ndarray,
         in_max = set(int(p) for p in max_idx[i] if p >= 0)
         for e in range(k):
             p = int(max_idx[i, e])
-            if p >= 0:                      # -1: an unused place (R11)
+            if p >= 0:                      # -1: an unused place (R12)
                 r[i, e] = np.float32(x32[i, p] - xh[i, p])
         for e in range(k):
             p = int(min_idx[i, e])
@@ -375,7 +375,7 @@ def quantize_act(x: np.ndarray, cb_a: np.ndarray, b_a: int, k: int,
 
 def static_lists(x: np.ndarray, thr_hi: float, thr_lo: float,
                  k: int) -> Tuple[np.ndarray, np.ndarray]:
-    """OASIS-S outlier lists (R11): channels at or beyond the fixed thresholds,
+    """OASIS-S outlier lists (R12): channels at or beyond the fixed thresholds,
     in channel order, at most k per side, -1 in the places left."""
     xv = np.asarray(x, dtype=np.float16).astype(np.float64)
     hi, lo = float(np.float32(thr_hi)), float(np.float32(thr_lo))
@@ -403,7 +403,7 @@ def quantize_act_static(x: np.ndarray, cb_a: np.ndarray, b_a: int, k: int, thr_h
 def forward(x, w_idx, cb_w, s_w, cb_a, b_a: int, b_w: int, k: int,
             mode: int = SCALE_ABSMAX, tokens=None, thresholds=None) -> Dict[str, np.ndarray]:
     """Look-ahead LUT-GEMM plus error compensation: Y = Y* + Y' (Sec. III-C);
-    thresholds = (thr_hi, thr_lo) selects OASIS-S lists (R11)."""
+    thresholds = (thr_hi, thr_lo) selects OASIS-S lists (R12)."""
     q = quantize_act(x, cb_a, b_a, k, mode) if thresholds is None else \
         quantize_act_static(x, cb_a, b_a, k, thresholds[0], thresholds[1], mode)
     lut = build_lut(cb_a, cb_w, b_a, b_w)
