@@ -73,6 +73,9 @@ def call_bytes(n, d_in, d_out, k, path):
         "outlier_compensate": comp,
         "lut_gemm": gemm_bytes(n, d_in, d_out, merge=path == "separate"),
         "lut_gemm_compensated": gemm_bytes(n, d_in, d_out, k, merge=False),
+        # the row-layout copy of a listed channel, where the launch reads it,
+        # duplicates codes the operation needs once: not counted
+        "lut_gemm_compensated_rows": gemm_bytes(n, d_in, d_out, k, merge=False),
     }
 
 
@@ -83,6 +86,7 @@ KERNEL_SOURCES = {
     "detect_outliers": ["quantize.hip"],
     "outlier_compensate": ["compensate.hip"],
     "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
+    "lut_gemm_compensated_rows": ["lut_gemm.hip", "compensate.hip"],
 }
 
 
@@ -114,6 +118,7 @@ CALL_SYMBOLS = {   # kernel symbol fragment of each call's dominant kernel
     "build_lut_quantize_act": "k_quantize<", "quantize_act_static": "k_quantize<",
     "detect_outliers": "k_quantize<", "outlier_compensate": "k_compensate",
     "lut_gemm": "k_gemm_mfma", "lut_gemm_compensated": "k_gemm_mfma",
+    "lut_gemm_compensated_rows": "k_gemm_mfma",
 }
 
 
@@ -138,7 +143,7 @@ def summarize_pmc(root, workload, path):
     db = json.load(open(out_path)) if os.path.exists(out_path) else {}
     lines = [f"| call | kernel | dispatches | FETCH_SIZE | WRITE_SIZE | HBM bytes/launch |",
              "|---|---|---|---|---|---|"]
-    names = {"fused": ["build_lut_quantize_act", "lut_gemm_compensated"],
+    names = {"fused": ["build_lut_quantize_act", "lut_gemm_compensated_rows"],
              "separate": ["build_lut_quantize_act", "outlier_compensate", "lut_gemm"],
              "lookahead": ["cluster_act", "detect_outliers", "lut_gemm",
                            "outlier_compensate"]}[path]
@@ -285,12 +290,10 @@ def main():
     if path == "auto":
         path = "fused" if (n <= 32 and algo == oasis.ALGO_MFMA) else "separate"
     side = torch.cuda.Stream()
-    # the outlier branch of the separate and look-ahead schedules reads the
-    # codes in the row layout (one input channel = d_out/2 contiguous bytes)
-    idx_wr = []
-    if path != "fused":
-        rows = oasis.pack_weight_rows(layer.w_idx).view(np.int32)
-        idx_wr = [torch.from_numpy(rows).to(dev) for _ in range(copies)]
+    # the outlier branch reads the codes in the row layout (one input channel
+    # = d_out/2 contiguous bytes); the main branch streams idx_w
+    rows = oasis.pack_weight_rows(layer.w_idx).view(np.int32)
+    idx_wr = [torch.from_numpy(rows).to(dev) for _ in range(copies)]
 
     # Every call of the path, with the arguments the step uses (c = weight copy).
     calls = {
@@ -310,11 +313,14 @@ def main():
         "lut_gemm_compensated": lambda c: oasis.lut_gemm_compensated(
             q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, q["max_idx"],
             q["min_idx"], q["residual"], y=y),
+        "lut_gemm_compensated_rows": lambda c: oasis.lut_gemm_compensated_rows(
+            q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c], s_w, lut, b_a, b_w, q["max_idx"],
+            q["min_idx"], q["residual"], y=y),
     }
     if path == "fused":
         names = (["build_lut", "quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
-            ["lut_gemm_compensated"]
-        gemm_name = "lut_gemm_compensated"
+            ["lut_gemm_compensated_rows"]
+        gemm_name = "lut_gemm_compensated_rows"
     elif path == "lookahead":
         names = ["build_lut", "cluster_act", "detect_outliers", "lut_gemm", "outlier_compensate"]
         gemm_name = "lut_gemm"
@@ -340,8 +346,9 @@ def main():
             # the LUT block is rebuilt with every step (Sec. IV-A builds it once
             # per layer), inside the quantize launch
             quantize(L)
-            oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w,
-                                       q["max_idx"], q["min_idx"], q["residual"], y=y)
+            oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c],
+                                            s_w, L, b_a, b_w, q["max_idx"], q["min_idx"],
+                                            q["residual"], y=y)
         elif path == "lookahead":
             oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
             # main branch and outlier detection run concurrently (Sec. III-C)
@@ -415,9 +422,9 @@ def main():
     q1 = oasis.quantize_act(x, lut, b_a, k) if not thr else \
         oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1])
     if path == "fused":
-        y_ref = oasis.lut_gemm_compensated(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w,
-                                           lut, b_a, b_w, q1["max_idx"], q1["min_idx"],
-                                           q1["residual"])
+        y_ref = oasis.lut_gemm_compensated_rows(q1["idx_act"], q1["act_scale"], idx_w[c_last],
+                                                idx_wr[c_last], s_w, lut, b_a, b_w,
+                                                q1["max_idx"], q1["min_idx"], q1["residual"])
     else:
         if path == "lookahead":
             y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a,
@@ -464,7 +471,7 @@ def main():
 
     def roof(nm):
         us = kern_us[nm]
-        if nm in ("lut_gemm", "lut_gemm_compensated") and n > 32:
+        if nm in ("lut_gemm", "lut_gemm_compensated", "lut_gemm_compensated_rows") and n > 32:
             tflops = ops / (us * 1e-6) / 1e12
             r = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
                  "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),

@@ -265,6 +265,24 @@ int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, i
                                hipStream_t stream);
 
 /*
+ * oasis_lut_gemm_compensated_rows - oasis_lut_gemm_compensated with the
+ * outlier branch reading the codes in the row layout idx_wr (see
+ * oasis_pack_weight_rows) while the main branch streams idx_w: a listed
+ * outlier costs 0.5 B per output column instead of 4 B.  For few tokens the
+ * call reads idx_wr only when 8 * n * k >= d_in (below that the GEMM layout's
+ * rows, which the same launch streams, are cheaper).  Same arguments,
+ * results and errors as oasis_lut_gemm_compensated, plus idx_wr (DEVICE,
+ * 4-byte aligned; NULL only when k == 0) and TOO_LARGE when
+ * d_in * ceil(d_out/8) * 4 >= 2^31.
+ */
+int oasis_lut_gemm_compensated_rows(const uint8_t* idx_act, const float* act_scale, int n,
+                                    int d_in, const uint32_t* idx_w, const uint32_t* idx_wr,
+                                    const float* w_scale, int d_out, const oasis_lut_block* lut,
+                                    int b_a, int b_w, const int32_t* max_idx,
+                                    const int32_t* min_idx, const float* residual, int k,
+                                    float* y, int accumulate, hipStream_t stream);
+
+/*
  * oasis_pack_weight_indices - HOST helper: pack w_idx uint8 [d_in][d_out]
  * (codes 0..15, row-major, host memory) into the idx_w layout above
  * (host memory, d_in/8 * d_out words).  Errors: NULL, SHAPE.

@@ -246,12 +246,12 @@ int oasis_outlier_compensate_rows(const int32_t* max_idx, const int32_t* min_idx
   return launched(oasis::launch_compensate_wr(a, stream));
 }
 
-int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
-                               const uint32_t* idx_w, const float* w_scale, int d_out,
-                               const oasis_lut_block* lut, int b_a, int b_w,
-                               const int32_t* max_idx, const int32_t* min_idx,
-                               const float* residual, int k, float* y, int accumulate,
-                               hipStream_t stream) {
+static int gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
+                            const uint32_t* idx_w, const uint32_t* idx_wr, const float* w_scale,
+                            int d_out, const oasis_lut_block* lut, int b_a, int b_w,
+                            const int32_t* max_idx, const int32_t* min_idx,
+                            const float* residual, int k, float* y, int accumulate,
+                            hipStream_t stream) {
   if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
   if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
   if (k < 0 || k > d_in) return OASIS_ERR_K;
@@ -261,26 +261,51 @@ int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, i
   if (k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
   if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
       !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
-      !aligned(min_idx, 4) || !aligned(residual, 4))
+      !aligned(min_idx, 4) || !aligned(residual, 4) || !aligned(idx_wr, 4))
     return OASIS_ERR_ALIGN;
   if ((size_t)(d_in / 8) * d_out * 4 >= (1ull << 31) || (size_t)n * d_in / 2 >= (1ull << 31))
     return OASIS_ERR_TOO_LARGE;  // 32-bit buffer offsets
+  if (idx_wr && (uint64_t)d_in * (uint64_t)((d_out + 7) / 8) * 4u >= (1ull << 31))
+    return OASIS_ERR_TOO_LARGE;
   if (d_in == 0) {  // no channels: Y* = Y' = 0
     if (accumulate) return OASIS_OK;
     return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
   }
   if (n <= oasis::kFusedMaxTokens) {
     oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
-                      accumulate ? 1 : 0, max_idx, min_idx, residual, k};
+                      accumulate ? 1 : 0, max_idx, min_idx, residual, k, idx_wr};
     return launched(oasis::launch_gemm_mfma(a, stream));
   }
   // many tokens: main branch into y, then the compensation merged into it
   oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
-                    accumulate ? 1 : 0, nullptr, nullptr, nullptr, 0};
+                    accumulate ? 1 : 0, nullptr, nullptr, nullptr, 0, nullptr};
   hipError_t e = oasis::launch_gemm_mfma(a, stream);
   if (e != hipSuccess || k == 0) return launched(e);
-  oasis::CompArgs c{max_idx, min_idx, residual, n, k, idx_w, lut, b_w, w_scale, d_in, d_out, y, 1};
-  return launched(oasis::launch_compensate(c, stream));
+  oasis::CompArgs c{max_idx, min_idx, residual, n, k, idx_wr ? idx_wr : idx_w, lut, b_w,
+                    w_scale, d_in, d_out, y, 1};
+  return launched(idx_wr ? oasis::launch_compensate_wr(c, stream)
+                         : oasis::launch_compensate(c, stream));
+}
+
+int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
+                               const uint32_t* idx_w, const float* w_scale, int d_out,
+                               const oasis_lut_block* lut, int b_a, int b_w,
+                               const int32_t* max_idx, const int32_t* min_idx,
+                               const float* residual, int k, float* y, int accumulate,
+                               hipStream_t stream) {
+  return gemm_compensated(idx_act, act_scale, n, d_in, idx_w, nullptr, w_scale, d_out, lut, b_a,
+                          b_w, max_idx, min_idx, residual, k, y, accumulate, stream);
+}
+
+int oasis_lut_gemm_compensated_rows(const uint8_t* idx_act, const float* act_scale, int n,
+                                    int d_in, const uint32_t* idx_w, const uint32_t* idx_wr,
+                                    const float* w_scale, int d_out, const oasis_lut_block* lut,
+                                    int b_a, int b_w, const int32_t* max_idx,
+                                    const int32_t* min_idx, const float* residual, int k,
+                                    float* y, int accumulate, hipStream_t stream) {
+  if (k > 0 && n > 0 && d_out > 0 && d_in > 0 && !idx_wr) return OASIS_ERR_NULL;
+  return gemm_compensated(idx_act, act_scale, n, d_in, idx_w, idx_wr, w_scale, d_out, lut, b_a,
+                          b_w, max_idx, min_idx, residual, k, y, accumulate, stream);
 }
 
 int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out) {

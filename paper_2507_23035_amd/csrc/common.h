@@ -134,6 +134,9 @@ struct GemmArgs {
   const int32_t* min_idx;
   const float* residual;
   int k;
+  // optional: the codes in the row layout ([d_in][ceil(d_out/8)] words); when
+  // set, the compensation reads its rows from here (0.5 B per outlier and column)
+  const uint32_t* idx_wr;
 };
 
 struct CompArgs {

@@ -329,6 +329,56 @@ __device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvA
   }
 }
 
+// The same from the row layout: thread owns 8 consecutive columns (one word
+// of each row), so an entry costs one 4-byte load, four pair lookups in the
+// weight half of the decode table (row `byte` holds pair(C_W, byte)) and
+// eight FMAs.
+template <int B>
+__device__ __forceinline__ void comp_rows_wr(__amdgpu_buffer_rsrc_t rwr, uint32_t row_bytes,
+                                             uint32_t woff, const CompEntries<B>& ce,
+                                             uint32_t (&w)[B]) {
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const uint32_t pp = ce.p[b] >= 0 ? (uint32_t)ce.p[b] : 0u;
+    w[b] = __builtin_amdgcn_raw_buffer_load_b32(rwr, (int)(pp * row_bytes + woff), 0, 0);
+  }
+}
+
+template <int B, bool PRE>
+__device__ __forceinline__ void tile_compensation_wr(const GemmArgs& A,
+                                                     __amdgpu_buffer_rsrc_t rwr,
+                                                     uint32_t row_bytes, uint32_t woff,
+                                                     const char* tab, int nslices, int i,
+                                                     int slice, const CompEntries<B>& first,
+                                                     const uint32_t (&first_rows)[B],
+                                                     float (&acc)[8]) {
+  const int E = 2 * A.k;
+  const uint32_t l4 = (uint32_t)(threadIdx.x & 31) * 4u;
+  for (int e0 = slice; e0 < E; e0 += B * nslices) {
+    CompEntries<B> ce;
+    uint32_t w[B];
+    if (PRE && e0 == slice) {
+      ce = first;
+#pragma unroll
+      for (int b = 0; b < B; ++b) w[b] = first_rows[b];
+    } else {
+      comp_entries<B>(A, i, e0, nslices, ce);
+      comp_rows_wr<B>(rwr, row_bytes, woff, ce, w);
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const float r = ce.p[b] >= 0 ? ce.r[b] : 0.0f;
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        const uint32_t off = __builtin_amdgcn_perm(w[b], l4, 0x0C0C0000u | ((4u + bb) << 8));
+        const uint32_t pr = *reinterpret_cast<const uint32_t*>(tab + off);
+        acc[2 * bb] = fmaf(r, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * bb]);
+        acc[2 * bb + 1] = fmaf(r, h2f((uint16_t)(pr >> 16)), acc[2 * bb + 1]);
+      }
+    }
+  }
+}
+
 // ----------------------------------------------------------------------------
 // MFMA kernel, few tokens (GEMV-like): one workgroup per 16*CW output
 // columns, its NW waves interleave the K blocks and are summed through LDS,
@@ -340,12 +390,13 @@ __device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvA
 // entries, then the weight codes; building the table waits only for the
 // codebooks while the weight stream is in flight.
 // ----------------------------------------------------------------------------
-template <int CW, int TF, int NW, int PF, bool FULLK, int B>
+template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
   constexpr int NT = NW * 64;
   constexpr int SLOTS = 16 * TF, COLS = 16 * CW;
-  constexpr int NSLICES = (NT / SLOTS) / (COLS / 4) > 0 ? (NT / SLOTS) / (COLS / 4) : 1;
-  static_assert((NT / SLOTS) % (COLS / 4) == 0, "threads per token must cover the columns");
+  constexpr int CG = ROWS ? 8 : 4;  // columns per compensation thread
+  constexpr int NSLICES = (NT / SLOTS) / (COLS / CG) > 0 ? (NT / SLOTS) / (COLS / CG) : 1;
+  static_assert((NT / SLOTS) % (COLS / CG) == 0, "threads per token must cover the columns");
   constexpr int RED_FLOATS = 4 * NW * CW * TF * 64;
   constexpr int PART_FLOATS = SLOTS * NSLICES * COLS;
   static_assert(4 * (RED_FLOATS + PART_FLOATS) <= 64 * 1024, "reduction buffers fit in the table");
@@ -373,7 +424,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   }
   const int T = NT / SLOTS;  // compensation threads per token
   const int ci = tid / T, cu = tid - ci * T;
-  const int cquad = cu % (COLS / 4), cslice = cu / (COLS / 4);
+  const int cquad = cu % (COLS / CG), cslice = cu / (COLS / CG);  // column group, slice
   // a few entries are worth holding through the main loop, many are not
   constexpr bool PRE = B <= 4 && TF == 1 && CW <= 2;
   CompEntries<B> ce0;
@@ -397,17 +448,35 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   const char* tb = reinterpret_cast<const char*>(tab);
   const uint32_t l4w = (uint32_t)(lane & 31) * 4u, l4a = l4w + 128u;
   // the preloaded entries' row words, in flight during the main loop
-  const uint32_t ccol4 = (uint32_t)(j0 + 4 * cquad) * 4u;
-  uint4_t crow0[B];
-  if (PRE && fused && ci < A.n) comp_rows<B>(A, ad, ccol4, ce0, crow0);
+  const uint32_t ccol4 = (uint32_t)(j0 + CG * cquad) * 4u;
+  // row layout: word (j0 + 8 cquad) / 8 of each row
+  const uint32_t wr_row = (uint32_t)((A.d_out + 7) / 8) * 4u;
+  const uint32_t wr_off = (uint32_t)(j0 / 8 + cquad) * 4u;
+  __amdgpu_buffer_rsrc_t rwr = ad.rw;
+  if constexpr (ROWS)
+    rwr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(A.idx_wr), 0,
+                                            (int)((uint32_t)A.d_in * wr_row), 0x00020000);
+  uint4_t crow0[ROWS ? 1 : B];
+  uint32_t crw0[ROWS ? B : 1];
+  if (PRE && fused && ci < A.n) {
+    if constexpr (ROWS) comp_rows_wr<B>(rwr, wr_row, wr_off, ce0, crw0);
+    else comp_rows<B>(A, ad, ccol4, ce0, crow0);
+  }
   if (wave < nblk)
     gemv_blocks<CW, TF, PF, FULLK>(KB, ad, wave, nblk, NW, buf, tb, l4w, l4a, tok_ok, acc);
 
   // outlier branch: reads only rows 0..15 of the table (weight centroids),
   // which nothing overwrites before the next barrier
-  float cacc[4] = {0.f, 0.f, 0.f, 0.f};
-  if (fused && ci < A.n)
-    tile_compensation<COLS, B, PRE>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0, cacc);
+  float cacc[CG];
+#pragma unroll
+  for (int c = 0; c < CG; ++c) cacc[c] = 0.0f;
+  if (fused && ci < A.n) {
+    if constexpr (ROWS)
+      tile_compensation_wr<B, PRE>(A, rwr, wr_row, wr_off, tb, NSLICES, ci, cslice, ce0, crw0,
+                                   cacc);
+    else
+      tile_compensation<COLS, B, PRE>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0, cacc);
+  }
   __syncthreads();  // every wave is done with the table: reuse it for the reduction
   float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tab);
   float* part = reinterpret_cast<float*>(tab) + RED_FLOATS;  // compensation partials
@@ -417,7 +486,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
     for (int f = 0; f < TF; ++f) red[wave][c * TF + f][lane] = acc[c][f];
   if (fused && ci < SLOTS) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) part[(ci * NSLICES + cslice) * COLS + 4 * cquad + c] = cacc[c];
+    for (int c = 0; c < CG; ++c) part[(ci * NSLICES + cslice) * COLS + CG * cquad + c] = cacc[c];
   }
   __syncthreads();
 
@@ -612,27 +681,39 @@ static void launch_prefill(const GemmArgs& a, hipStream_t s) {
                        dim3(WX * WY * 64), 0, s, a, ncx, nty);
 }
 
-template <int CW, int TF, int NW, int B>
+template <int CW, int TF, int NW, int B, bool ROWS>
 static void launch_gemv_b(const GemmArgs& a, hipStream_t s) {
   const int ntiles = (a.d_out + 16 * CW - 1) / (16 * CW);
   constexpr int PF = 2;  // blocks in flight per wave
   if ((a.d_in / 8) % 16 == 0)
-    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true, B>), dim3(ntiles), dim3(NW * 64),
-                       0, s, a, ntiles);
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true, B, ROWS>), dim3(ntiles),
+                       dim3(NW * 64), 0, s, a, ntiles);
   else
-    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false, B>), dim3(ntiles),
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false, B, ROWS>), dim3(ntiles),
                        dim3(NW * 64), 0, s, a, ntiles);
 }
 
 // Outlier entries in flight per compensation thread: about a token's share of
 // one slice, at most 8.
+template <int CW, int TF, int NW, bool ROWS>
+static void launch_gemv_r(const GemmArgs& a, hipStream_t s) {
+  constexpr int NSLICES = (NW * 64 / (16 * TF)) / (16 * CW / (ROWS ? 8 : 4));
+  if (2 * a.k <= 4 * NSLICES)
+    launch_gemv_b<CW, TF, NW, 4, ROWS>(a, s);
+  else
+    launch_gemv_b<CW, TF, NW, 8, ROWS>(a, s);
+}
+
+// The fused compensation reads the row layout when the GEMM layout would cost
+// at least twice the tile's own weight stream (n * 2k words of 4 B per
+// column against d_in / 8): those row words are L2 hits while the tile
+// streams them, the row layout's are separate (cold) reads of 0.5 B.
 template <int CW, int TF, int NW>
 static void launch_gemv(const GemmArgs& a, hipStream_t s) {
-  constexpr int NSLICES = (NW * 64 / (16 * TF)) / (4 * CW);
-  if (2 * a.k <= 4 * NSLICES)
-    launch_gemv_b<CW, TF, NW, 4>(a, s);
+  if (a.k > 0 && a.idx_wr && 8ll * a.n * a.k >= (long long)a.d_in)
+    launch_gemv_r<CW, TF, NW, true>(a, s);
   else
-    launch_gemv_b<CW, TF, NW, 8>(a, s);
+    launch_gemv_r<CW, TF, NW, false>(a, s);
 }
 
 template <int TF>

@@ -25,7 +25,8 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_cluster_act", "oasis_detect_outliers",
            "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_outlier_compensate_rows",
            "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows",
-           "oasis_build_lut_quantize_act", "oasis_quantize_act_static")
+           "oasis_build_lut_quantize_act", "oasis_quantize_act_static",
+           "oasis_lut_gemm_compensated_rows")
 
 
 class OasisError(RuntimeError):
@@ -69,6 +70,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_outlier_compensate.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
     lib.oasis_lut_gemm_compensated.restype = I
     lib.oasis_lut_gemm_compensated.argtypes = [P, P, I, I, P, P, I, P, I, I, P, P, P, I, P, I, P]
+    lib.oasis_lut_gemm_compensated_rows.restype = I
+    lib.oasis_lut_gemm_compensated_rows.argtypes = [P, P, I, I, P, P, P, I, P, I, I, P, P, P, I,
+                                                    P, I, P]
     lib.oasis_outlier_compensate_rows.restype = I
     lib.oasis_outlier_compensate_rows.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
     lib.oasis_pack_weight_indices.restype = I
@@ -296,6 +300,25 @@ def lut_gemm_compensated(idx_act, act_scale, idx_w, w_scale, lut, b_a: int, b_w:
         _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
         b_a, b_w, _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
         _ptr(residual) if k else None, k, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def lut_gemm_compensated_rows(idx_act, act_scale, idx_w, idx_wr, w_scale, lut, b_a: int,
+                              b_w: int, max_idx, min_idx, residual, y=None,
+                              accumulate: bool = False, stream=None):
+    """lut_gemm_compensated with the outlier branch reading the row-layout codes."""
+    import torch
+    n = idx_act.shape[0]
+    d_in = idx_act.shape[1] * 2
+    d_out = idx_w.shape[1]
+    k = max_idx.shape[1]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
+    _check("oasis_lut_gemm_compensated_rows", load().oasis_lut_gemm_compensated_rows(
+        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(idx_wr) if k else None,
+        _ptr(w_scale), d_out, _ptr(lut), b_a, b_w, _ptr(max_idx) if k else None,
+        _ptr(min_idx) if k else None, _ptr(residual) if k else None, k, _ptr(y),
+        1 if accumulate else 0, _stream(stream)))
     return y
 
 

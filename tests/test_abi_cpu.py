@@ -198,6 +198,14 @@ def test_pack_weight_rows_matches_oracle_packing():
         assert np.array_equal(nib[:, :shape[1]], w) and not nib[:, shape[1]:].any()
 
 
+def test_fused_rows_errors(lib):
+    g = lib.oasis_lut_gemm_compensated_rows
+    assert g(P, P, 4, 12, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, None) == -2
+    assert g(P, P, 4, 16, P, None, P, 8, P, 4, 4, P, P, P, 2, P, 0, None) == -1   # rows needed
+    assert g(P, P, 4, 16, P, MIS, P, 8, P, 4, 4, P, P, P, 2, P, 0, None) == -6
+    assert g(P, P, 4, 16, P, P, P, 8, P, 4, 4, P, P, P, 17, P, 0, None) == -4
+
+
 def test_pack_weight_indices_matches_oracle_packing():
     from oracle import oasis_oracle as O
     rng = np.random.default_rng(5)

@@ -86,6 +86,16 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
                                        b_w, s_w, L.spec.d_in, accumulate=False)
     torch.cuda.synchronize()
     assert_close(yr.cpu().numpy()[rows], ref["y_comp"], "Y' (row layout)")
+    yf = oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut,
+                                         b_a, b_w, q["max_idx"], q["min_idx"], q["residual"])
+    torch.cuda.synchronize()
+    assert_close(yf.cpu().numpy()[rows], ref["y"], "Y fused (row-layout compensation)")
+    yf.fill_(0.5)
+    oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut, b_a,
+                                    b_w, q["max_idx"], q["min_idx"], q["residual"], y=yf,
+                                    accumulate=True)
+    torch.cuda.synchronize()
+    assert_close(yf.cpu().numpy()[rows] - 0.5, ref["y"], "Y fused rows, accumulate")
     ym = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
     oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr, lut, b_w,
                                   s_w, L.spec.d_in, y=ym, accumulate=True)
@@ -266,6 +276,10 @@ def test_static_thresholds(name, k, thr):
                                        b_w, s_w, L.spec.d_in, accumulate=False)
     torch.cuda.synchronize()
     assert_close(yc.cpu().numpy(), ref["y_comp"], "Y' (static thresholds, row layout)")
+    yr = oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut,
+                                         b_a, b_w, q["max_idx"], q["min_idx"], q["residual"])
+    torch.cuda.synchronize()
+    assert_close(yr.cpu().numpy(), ref["y"], "Y (static thresholds, fused rows)")
 
 
 def test_empty_batch():
