@@ -32,6 +32,12 @@ float half_bits_to_float(uint16_t h) {
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool bits_ok(int b) { return b >= 1 && b <= 4; }
+// The GEMM kernels address codes with 32-bit buffer offsets, up to one block
+// of 16 weight rows past the last (partial) block.
+bool offsets_fit(int n, int d_in, int d_out) {
+  const uint64_t kb = (uint64_t)(d_in / 8) + 31;
+  return kb * (uint64_t)d_out * 4u < (1ull << 31) && (uint64_t)(n + 1) * kb * 4u < (1ull << 31);
+}
 
 constexpr size_t kMaxLds = 160 * 1024;
 
@@ -195,8 +201,7 @@ int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_
   if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
       !aligned(act_scale, 4) || !aligned(w_scale, 4))
     return OASIS_ERR_ALIGN;
-  if ((size_t)(d_in / 8) * d_out * 4 >= (1ull << 31) || (size_t)n * d_in / 2 >= (1ull << 31))
-    return OASIS_ERR_TOO_LARGE;  // 32-bit buffer offsets
+  if (!offsets_fit(n, d_in, d_out)) return OASIS_ERR_TOO_LARGE;
   if (d_in == 0) {  // empty reduction: Y* = 0
     if (accumulate) return OASIS_OK;
     return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
@@ -263,8 +268,7 @@ static int gemm_compensated(const uint8_t* idx_act, const float* act_scale, int 
       !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
       !aligned(min_idx, 4) || !aligned(residual, 4) || !aligned(idx_wr, 4))
     return OASIS_ERR_ALIGN;
-  if ((size_t)(d_in / 8) * d_out * 4 >= (1ull << 31) || (size_t)n * d_in / 2 >= (1ull << 31))
-    return OASIS_ERR_TOO_LARGE;  // 32-bit buffer offsets
+  if (!offsets_fit(n, d_in, d_out)) return OASIS_ERR_TOO_LARGE;
   if (idx_wr && (uint64_t)d_in * (uint64_t)((d_out + 7) / 8) * 4u >= (1ull << 31))
     return OASIS_ERR_TOO_LARGE;
   if (d_in == 0) {  // no channels: Y* = Y' = 0

@@ -259,7 +259,9 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
   auto window = [&](const uint32_t* src, uint32_t first, uint32_t count, uint32_t fill) {
     return first + lane < count ? src[first + lane] : fill;
   };
-  // load stream: rows [lw0, lw0 + 64) of the list in lanes
+  // load stream: rows [lw0, lw0 + 64) of the list in lanes.  The row's offset
+  // is added to the lane's (the descriptor's size check then covers the whole
+  // offset: columns past d_out in the last row read zeros)
   uint32_t lw0 = 0, lw_row = window(rowlist, 0, nrow, 0u);
   auto load_batch = [&](uint32_t base, uint32_t (&w)[ROW_PF][CPL]) {
     if (base >= lw0 + 64) {  // batches are 64-aligned: slide the window
@@ -271,16 +273,16 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
       const uint32_t j = base + d;
       const uint32_t row = (uint32_t)__builtin_amdgcn_readlane((int)lw_row, (int)(j - lw0));
       // rows past the list read row 0 (in bounds) and are never used
-      const int soff = j < nrow ? (int)(row * row_bytes) : 0;
+      const uint32_t roff = j < nrow ? row * row_bytes : 0u;
       if constexpr (CPL % 4 == 0) {
 #pragma unroll
         for (int h = 0; h < CPL / 4; ++h) {
           const uint4_t v = __builtin_bit_cast(
-              uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(voff + 16u * h), soff, 0));
+              uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(roff + voff + 16u * h), 0, 0));
           w[d][4 * h] = v[0]; w[d][4 * h + 1] = v[1]; w[d][4 * h + 2] = v[2]; w[d][4 * h + 3] = v[3];
         }
       } else {
-        w[d][0] = __builtin_amdgcn_raw_buffer_load_b32(rw, (int)voff, soff, 0);
+        w[d][0] = __builtin_amdgcn_raw_buffer_load_b32(rw, (int)(roff + voff), 0, 0);
       }
     }
   };
@@ -455,7 +457,9 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   }
 
   const uint32_t m = (uint32_t)slab * 64u + (uint32_t)lane;  // this lane's word
-  const uint32_t voff = m * 4u;
+  // lanes past the row end read its last word (never stored), so a load stays
+  // inside its row whatever part of the offset the size check covers
+  const uint32_t voff = min(m, (uint32_t)wn - 1u) * 4u;
   const uint32_t row_bytes = (uint32_t)wn * 4u;
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(A.idx_w), 0, (int)((uint32_t)d_in * row_bytes), 0x00020000);

@@ -48,17 +48,23 @@ struct DualTableLoader {
   uint32_t hw[2], ha[2];  // the pairs holding codes 4w .. 4w + 3
   // wave < 4 only
   __device__ __forceinline__ void load(const oasis_lut_block* lut, uint32_t wave) {
-    const uint32_t* w32 = reinterpret_cast<const uint32_t*>(lut->cb_wgt);
-    const uint32_t* a32 = reinterpret_cast<const uint32_t*>(lut->cb_act);
+    // constant address space: scalar loads, also through a pointer the compiler
+    // cannot trace back to a kernel argument
+    using cu32 = const __attribute__((address_space(4))) uint32_t;
+    cu32* w32 = (cu32*)reinterpret_cast<const uint32_t*>(lut->cb_wgt);
+    cu32* a32 = (cu32*)reinterpret_cast<const uint32_t*>(lut->cb_act);
+    // readfirstlane keeps every value a scalar load: without it the compiler
+    // may turn the per-lane choice between the two codebooks into a choice of
+    // address, i.e. a vector load that waits behind the weight stream
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      cw[q] = w32[q];
-      ca[q] = a32[q];
+      cw[q] = __builtin_amdgcn_readfirstlane(w32[q]);
+      ca[q] = __builtin_amdgcn_readfirstlane(a32[q]);
     }
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      hw[q] = w32[2 * wave + q];
-      ha[q] = a32[2 * wave + q];
+      hw[q] = __builtin_amdgcn_readfirstlane(w32[2 * wave + q]);
+      ha[q] = __builtin_amdgcn_readfirstlane(a32[2 * wave + q]);
     }
   }
   __device__ __forceinline__ void store(uint32_t* tab, uint32_t wave, int lane) const {
@@ -117,17 +123,19 @@ struct BlockCodes {
 };
 
 // Buffer loads of a block of codes for the GEMV kernel.  Per-lane byte offsets
-// are computed once; the block's offset travels in an SGPR.  The buffer
-// descriptors carry the tensors' sizes, so a read past the end returns 0
-// instead of faulting: columns past d_out or tokens past n only feed outputs
-// that are never stored, and the words of a last, partial K block are masked
-// in mma_block.
+// are computed once and the block's offset is added to them, so the whole
+// offset is in the per-lane operand that the descriptor's size check covers:
+// a read past the end returns 0 instead of faulting.  Columns past d_out or
+// tokens past n only feed outputs that are never stored, the words of a last,
+// partial K block are masked in mma_block, and a block past the last one
+// (index clamped to nblk) reads zeros.
 struct GemvAddr {
   __amdgpu_buffer_rsrc_t rw, ra;
   uint32_t woff[4];  // byte offset of (row 4g + s, column j0 + CW*m) in block 0
   uint32_t aoff;     // byte offset of (token m, word 4g) in block 0
   uint32_t wblk;     // bytes per block of 16 weight rows
   uint32_t astride;  // bytes between token tiles (16 tokens)
+  uint32_t nblk;     // blocks of 16 weight rows (the last may be partial)
 };
 
 template <int CW>
@@ -145,29 +153,31 @@ __device__ __forceinline__ GemvAddr gemv_addr(const GemmArgs& A, int j0) {
   ad.aoff = ((uint32_t)m * KB + 4u * g) * 4u;
   ad.wblk = 16u * (uint32_t)A.d_out * 4u;
   ad.astride = 16u * KB * 4u;
+  ad.nblk = (KB + 15u) / 16u;
   return ad;
 }
 
 template <int CW, int TF>
 __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
                                                BlockCodes<CW, TF>& bc) {
-  const int sw = (int)((uint32_t)blk * ad.wblk);
-  const int sa = blk * 64;
+  const uint32_t b = min((uint32_t)blk, ad.nblk);
+  const uint32_t wb = b * ad.wblk, ab = b * 64u;
 #pragma unroll
   for (int f = 0; f < TF; ++f)
-    bc.av[f] = __builtin_bit_cast(
-        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.ra, (int)(ad.aoff + f * ad.astride), sa, 0));
+    bc.av[f] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                               ad.ra, (int)(ad.aoff + f * ad.astride + ab), 0, 0));
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
+    const int o = (int)(ad.woff[s] + wb);
     if constexpr (CW == 4) {
-      const uint4_t v = __builtin_bit_cast(
-          uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)ad.woff[s], sw, 0));
+      const uint4_t v =
+          __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, o, 0, 0));
       bc.wv[s][0] = v[0]; bc.wv[s][1] = v[1]; bc.wv[s][2] = v[2]; bc.wv[s][3] = v[3];
     } else if constexpr (CW == 2) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b64(ad.rw, (int)ad.woff[s], sw, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(ad.rw, o, 0, 0);
       bc.wv[s][0] = v[0]; bc.wv[s][CW - 1] = v[1];
     } else {
-      bc.wv[s][0] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)ad.woff[s], sw, 0);
+      bc.wv[s][0] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, o, 0, 0);
     }
   }
 }
@@ -224,21 +234,30 @@ __device__ __forceinline__ void mma_block(int KB, int blk, const BlockCodes<CW, 
 // PF blocks' codes in flight (buffer loads): after a block is expanded and
 // multiplied its registers are refilled with the block PF strides ahead.
 // `buf` holds the codes of the first PF blocks (loaded before the table was
-// built).
+// built).  The refills are unconditional (past the end they read zeros
+// through the buffer descriptors): a conditional load would make the compiler
+// count it as absent on one path and wait for every load before using a block.
 template <int CW, int TF, int PF, bool FULLK>
 __device__ __forceinline__ void gemv_blocks(int KB, const GemvAddr& ad, int blk_begin,
                                             int blk_end, int blk_stride,
                                             BlockCodes<CW, TF> (&buf)[PF], const char* tab,
                                             uint32_t l4w, uint32_t l4a, const bool (&tok_ok)[TF],
                                             float4_t (&acc)[CW][TF]) {
+  if (blk_end <= blk_begin + PF * blk_stride) {  // the preloaded blocks are all: no refills
+#pragma unroll
+    for (int d = 0; d < PF; ++d)
+      if (blk_begin + d * blk_stride < blk_end)
+        mma_block<CW, TF, !FULLK>(KB, blk_begin + d * blk_stride, buf[d], tab, l4w, l4a, tok_ok,
+                                  acc);
+    return;
+  }
   for (int blk = blk_begin; blk < blk_end; blk += PF * blk_stride) {
 #pragma unroll
     for (int d = 0; d < PF; ++d) {
       const int b = blk + d * blk_stride;
       if (b < blk_end) {
         mma_block<CW, TF, !FULLK>(KB, b, buf[d], tab, l4w, l4a, tok_ok, acc);
-        const int nb = b + PF * blk_stride;
-        if (nb < blk_end) load_block_buf<CW, TF>(ad, nb, buf[d]);
+        load_block_buf<CW, TF>(ad, b + PF * blk_stride, buf[d]);
       }
     }
   }
@@ -287,17 +306,16 @@ __device__ __forceinline__ void comp_entries(const GemmArgs& A, int i, int e0, i
 }
 
 // Row words of the tile's columns for B entries (buffer loads; entries with
-// p < 0 read row 0 and are given a zero residual).
+// p < 0 get an offset past the buffer, which reads zeros without a memory
+// access, and a zero residual).
 template <int B>
 __device__ __forceinline__ void comp_rows(const GemmArgs& A, const GemvAddr& ad, uint32_t col4,
                                           const CompEntries<B>& ce, uint4_t (&w)[B]) {
   const uint32_t d_out = (uint32_t)A.d_out;
 #pragma unroll
   for (int b = 0; b < B; ++b) {
-    const uint32_t pp = ce.p[b] >= 0 ? (uint32_t)ce.p[b] : 0u;
-    w[b] = __builtin_bit_cast(
-        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)((pp >> 3) * d_out * 4u + col4),
-                                                       0, 0));
+    const uint32_t o = ce.p[b] >= 0 ? ((uint32_t)ce.p[b] >> 3) * d_out * 4u + col4 : 0xFFFFFFF0u;
+    w[b] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, (int)o, 0, 0));
   }
 }
 
@@ -339,8 +357,8 @@ __device__ __forceinline__ void comp_rows_wr(__amdgpu_buffer_rsrc_t rwr, uint32_
                                              uint32_t (&w)[B]) {
 #pragma unroll
   for (int b = 0; b < B; ++b) {
-    const uint32_t pp = ce.p[b] >= 0 ? (uint32_t)ce.p[b] : 0u;
-    w[b] = __builtin_amdgcn_raw_buffer_load_b32(rwr, (int)(pp * row_bytes + woff), 0, 0);
+    const uint32_t o = ce.p[b] >= 0 ? (uint32_t)ce.p[b] * row_bytes + woff : 0xFFFFFFF0u;
+    w[b] = __builtin_amdgcn_raw_buffer_load_b32(rwr, (int)o, 0, 0);
   }
 }
 
@@ -383,12 +401,14 @@ __device__ __forceinline__ void tile_compensation_wr(const GemmArgs& A,
 // MFMA kernel, few tokens (GEMV-like): one workgroup per 16*CW output
 // columns, its NW waves interleave the K blocks and are summed through LDS,
 // so every output is written once, without atomics.  With outlier lists
-// (A.k > 0) the workgroup also adds the compensation of its columns; each
+// (B > 0, k > 0) the workgroup also adds the compensation of its columns; each
 // wave starts its share as soon as its own blocks are done.
 //
-// Prologue: the codebooks (scalar loads), the scales and the first outlier
-// entries, then the weight codes; building the table waits only for the
-// codebooks while the weight stream is in flight.
+// Prologue: the scales and the first outlier entries, then the weight codes,
+// then the codebooks (scalar loads, issued after the vector loads so that no
+// wait for them delays the weight stream); building the table waits only for
+// the codebooks, and the entries are checked after the table barrier, behind
+// the weight loads in flight.
 // ----------------------------------------------------------------------------
 template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
@@ -408,32 +428,50 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   const int j0 = xcd_tile(blockIdx.x, ntiles) * COLS;
   const int KB = A.d_in >> 3;
   const int nblk = (KB + 15) / 16;
-  const bool fused = A.k > 0;
+  constexpr bool fused = B > 0;  // B = 0: no outlier lists (k = 0)
+  constexpr int BE = B > 0 ? B : 1;
 
-  // ---- prologue: codebook entries, scales, outlier entries, weight codes
+  // ---- prologue: codebooks (scalar loads), scales, outlier entries, weight
+  // codes.  Without outlier lists every kernel argument the vector loads need
+  // is made resident in SGPRs first (the empty asm, on which the codebook
+  // address depends): a scalar-load wait cannot single out one load, so none
+  // is fetched after the codebook loads and no weight load waits for them;
+  // the weight loads are unconditional (a block past the end reads zeros), so
+  // the wait before each block covers that block only.  With lists the
+  // entries are loaded and checked first and only the blocks that exist are
+  // requested: measured, that order is the faster one there (the list wait
+  // is short, and the row words that follow would otherwise queue behind
+  // the whole weight stream).
+  const GemvAddr ad = gemv_addr<CW>(A, j0);
+  const oasis_lut_block* lutp = A.lut;
+  if constexpr (!fused)
+    asm("" : "+s"(lutp)
+        : "s"(A.idx_w), "s"(A.idx_act), "s"(A.w_scale), "s"(A.act_scale), "s"(A.n),
+          "s"(A.d_in), "s"(A.d_out));
   DualTableLoader dt;
-  if (wave < 4) dt.load(A.lut, (uint32_t)wave);
-  float sc[EPT];  // s_j * t_i of this thread's epilogue outputs (s_j alone for the compensation)
-  float swj[EPT];
+  if (wave < 4) dt.load(lutp, (uint32_t)wave);
+  if constexpr (!fused) __builtin_amdgcn_sched_barrier(0);
+  float ts[EPT];   // t_i of this thread's epilogue outputs
+  float swj[EPT];  // s_j of the same
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
     const int o = tid + NT * q;
     const int tok = min(o / COLS, A.n - 1), j = min(j0 + o % COLS, A.d_out - 1);
     swj[q] = A.w_scale[j];
-    sc[q] = A.act_scale[tok] * swj[q];
+    ts[q] = A.act_scale[tok];
   }
   const int T = NT / SLOTS;  // compensation threads per token
   const int ci = tid / T, cu = tid - ci * T;
   const int cquad = cu % (COLS / CG), cslice = cu / (COLS / CG);  // column group, slice
   // a few entries are worth holding through the main loop, many are not
-  constexpr bool PRE = B <= 4 && TF == 1 && CW <= 2;
-  CompEntries<B> ce0;
-  if (PRE && fused && ci < A.n) comp_entries<B>(A, ci, cslice, NSLICES, ce0);
-  const GemvAddr ad = gemv_addr<CW>(A, j0);
+  constexpr bool PRE = fused && B <= 4 && TF == 1 && CW <= 2;
+  CompEntries<BE> ce0;
+  if (PRE && ci < A.n) comp_entries<BE>(A, ci, cslice, NSLICES, ce0);
   BlockCodes<CW, TF> buf[PF];
 #pragma unroll
   for (int d = 0; d < PF; ++d)
-    if (wave + d * NW < nblk) load_block_buf<CW, TF>(ad, wave + d * NW, buf[d]);
+    if (!fused || wave + d * NW < nblk) load_block_buf<CW, TF>(ad, wave + d * NW, buf[d]);
+  if constexpr (!fused) __builtin_amdgcn_sched_barrier(0);
   if (wave < 4) dt.store(tab, (uint32_t)wave, lane);
   __syncthreads();  // decode table
 
@@ -456,11 +494,11 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   if constexpr (ROWS)
     rwr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(A.idx_wr), 0,
                                             (int)((uint32_t)A.d_in * wr_row), 0x00020000);
-  uint4_t crow0[ROWS ? 1 : B];
-  uint32_t crw0[ROWS ? B : 1];
-  if (PRE && fused && ci < A.n) {
-    if constexpr (ROWS) comp_rows_wr<B>(rwr, wr_row, wr_off, ce0, crw0);
-    else comp_rows<B>(A, ad, ccol4, ce0, crow0);
+  uint4_t crow0[ROWS ? 1 : BE];
+  uint32_t crw0[ROWS ? BE : 1];
+  if (PRE && ci < A.n) {
+    if constexpr (ROWS) comp_rows_wr<BE>(rwr, wr_row, wr_off, ce0, crw0);
+    else comp_rows<BE>(A, ad, ccol4, ce0, crow0);
   }
   if (wave < nblk)
     gemv_blocks<CW, TF, PF, FULLK>(KB, ad, wave, nblk, NW, buf, tb, l4w, l4a, tok_ok, acc);
@@ -472,10 +510,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   for (int c = 0; c < CG; ++c) cacc[c] = 0.0f;
   if (fused && ci < A.n) {
     if constexpr (ROWS)
-      tile_compensation_wr<B, PRE>(A, rwr, wr_row, wr_off, tb, NSLICES, ci, cslice, ce0, crw0,
+      tile_compensation_wr<BE, PRE>(A, rwr, wr_row, wr_off, tb, NSLICES, ci, cslice, ce0, crw0,
                                    cacc);
     else
-      tile_compensation<COLS, B, PRE>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0, cacc);
+      tile_compensation<COLS, BE, PRE>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0, cacc);
   }
   __syncthreads();  // every wave is done with the table: reuse it for the reduction
   float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tab);
@@ -504,7 +542,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
     float v = 0.0f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) v += redf[((w * CW * TF + t) * 64 + ln) * 4 + (mrow & 3)];
-    float val = sc[q] * v;
+    float val = ts[q] * swj[q] * v;
     if (fused) {
       float cs = 0.0f;
       for (int sl = 0; sl < NSLICES; ++sl) cs += part[(tok * NSLICES + sl) * COLS + jl];
@@ -527,7 +565,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 // ----------------------------------------------------------------------------
 
 // Per-lane byte offsets of the codes of one wave (block 0); a block's offset
-// travels in an SGPR.  Reads past either tensor return 0.  Weight lane m of
+// is added to them (the descriptor's size check covers the whole offset), so
+// reads past either tensor return 0.  Weight lane m of
 // column tile c holds column j0 + 16c + m, so the MFMA's output rows 4g..4g+3
 // are 4 consecutive columns: each lane stores 16 contiguous bytes.
 template <int CW, int TF>
@@ -541,17 +580,17 @@ struct PrefillAddr {
 template <int CW, int TF>
 __device__ __forceinline__ void load_block_pf(const PrefillAddr<CW, TF>& ad, int blk,
                                               BlockCodes<CW, TF>& bc) {
-  const int sw = (int)((uint32_t)blk * ad.wblk);
-  const int sa = blk * 64;
+  const uint32_t wb = (uint32_t)blk * ad.wblk, ab = (uint32_t)blk * 64u;
 #pragma unroll
   for (int f = 0; f < TF; ++f)
     bc.av[f] = __builtin_bit_cast(
-        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.ra, (int)ad.aoff[f], sa, 0));
+        uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.ra, (int)(ad.aoff[f] + ab), 0, 0));
 #pragma unroll
   for (int s = 0; s < 4; ++s)
 #pragma unroll
     for (int c = 0; c < CW; ++c)
-      bc.wv[s][c] = __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)(ad.woff[s] + 64u * c), sw, 0);
+      bc.wv[s][c] =
+          __builtin_amdgcn_raw_buffer_load_b32(ad.rw, (int)(ad.woff[s] + wb + 64u * c), 0, 0);
 }
 
 // KMASK: zero the activation operand of words past the end of the reduction
@@ -708,9 +747,12 @@ static void launch_gemv_r(const GemmArgs& a, hipStream_t s) {
 // at least twice the tile's own weight stream (n * 2k words of 4 B per
 // column against d_in / 8): those row words are L2 hits while the tile
 // streams them, the row layout's are separate (cold) reads of 0.5 B.
+// No lists (k = 0): B = 0, a kernel without the outlier branch.
 template <int CW, int TF, int NW>
 static void launch_gemv(const GemmArgs& a, hipStream_t s) {
-  if (a.k > 0 && a.idx_wr && 8ll * a.n * a.k >= (long long)a.d_in)
+  if (a.k == 0)
+    launch_gemv_b<CW, TF, NW, 0, false>(a, s);
+  else if (a.idx_wr && 8ll * a.n * a.k >= (long long)a.d_in)
     launch_gemv_r<CW, TF, NW, true>(a, s);
   else
     launch_gemv_r<CW, TF, NW, false>(a, s);
