@@ -39,6 +39,11 @@ design notes of the repository):
       the max list holds the channels with x >= thr_hi, the min list those
       with x <= thr_lo, in channel order, at most k each; unused places hold
       channel -1 and residual 0.
+  R13 Inlier scale ("inlier"): t_i = max |x_ip| over the channels in neither
+      list, so the main branch's centroids span only the values it keeps
+      (the outliers are compensated exactly, Sec. III-A, III-C); t_i = 0 when
+      every channel is listed (the outlier branch then carries the whole
+      product).  The lists come first, so this mode has no look-ahead split.
 """
 from __future__ import annotations
 
@@ -49,6 +54,7 @@ import numpy as np
 
 SCALE_ABSMAX = 0
 SCALE_NONE = 1
+SCALE_INLIER = 2
 
 
 # --------------------------------------------------------------------------
@@ -242,6 +248,19 @@ class Orizuru:
 # --------------------------------------------------------------------------
 # Sec. III-C: look-ahead residuals of the outliers
 # --------------------------------------------------------------------------
+def inlier_scale(x: np.ndarray, max_idx: np.ndarray, min_idx: np.ndarray) -> np.ndarray:
+    """R13: t_i = max |x_ip| over the channels in neither list (0 if none)."""
+    xv = np.asarray(x, dtype=np.float16).astype(np.float64)
+    n, K = xv.shape
+    t = np.zeros(n, dtype=np.float32)
+    for i in range(n):
+        listed = set(int(p) for p in max_idx[i] if p >= 0) | \
+            set(int(p) for p in min_idx[i] if p >= 0)
+        rest = [abs(xv[i, p]) for p in range(K) if p not in listed]
+        t[i] = np.float32(max(rest)) if rest else np.float32(0.0)
+    return t
+
+
 def dequant_act(a: np.ndarray, t: np.ndarray, cb_a: np.ndarray) -> np.ndarray:
     """x_hat = fp32(t * C_A[a]): exact, the product of two fp16 values."""
     ca = np.asarray(cb_a, dtype=np.float16).astype(np.float32)
@@ -366,9 +385,9 @@ def outlier_compensate(max_idx: np.ndarray, min_idx: np.ndarray, r: np.ndarray,
 def quantize_act(x: np.ndarray, cb_a: np.ndarray, b_a: int, k: int,
                  mode: int = SCALE_ABSMAX) -> Dict[str, np.ndarray]:
     """Per-token scale, activation indices, outlier lists and residuals."""
-    t = act_scale(x, mode)
-    a = cluster(x, t, cb_a, b_a)
     mx, mn = topk_lists(x, k)
+    t = inlier_scale(x, mx, mn) if mode == SCALE_INLIER else act_scale(x, mode)
+    a = cluster(x, t, cb_a, b_a)
     r = residuals(x, t, a, cb_a, mx, mn)
     return {"t": t, "a": a, "max_idx": mx, "min_idx": mn, "residual": r}
 
@@ -393,9 +412,9 @@ def static_lists(x: np.ndarray, thr_hi: float, thr_lo: float,
 def quantize_act_static(x: np.ndarray, cb_a: np.ndarray, b_a: int, k: int, thr_hi: float,
                         thr_lo: float, mode: int = SCALE_ABSMAX) -> Dict[str, np.ndarray]:
     """OASIS-S: scale and indices as in quantize_act, lists from fixed thresholds."""
-    t = act_scale(x, mode)
-    a = cluster(x, t, cb_a, b_a)
     mx, mn = static_lists(x, thr_hi, thr_lo, k)
+    t = inlier_scale(x, mx, mn) if mode == SCALE_INLIER else act_scale(x, mode)
+    a = cluster(x, t, cb_a, b_a)
     r = residuals(x, t, a, cb_a, mx, mn)
     return {"t": t, "a": a, "max_idx": mx, "min_idx": mn, "residual": r}
 

@@ -236,6 +236,57 @@ def test_duplicate_channels_compensated_once():
     assert np.all(q["residual"][0, :4] != 0)
 
 
+# ---------------------------------------------------------------- inlier scale (R13)
+def test_inlier_scale_by_hand():
+    """k = 1: the max list takes 10, the min list -2; the inliers' absmax is 3.
+    Boundaries of C_A = (-1, -0.5, 0.25, 0.75) are (-0.75, -0.125, 0.5), scaled
+    by t = 3: (-2.25, -0.375, 1.5)."""
+    x = np.array([[10, 1, -2, 0.5, -0.25, 3]], dtype=np.float16)
+    cb = np.array([-1, -0.5, 0.25, 0.75], dtype=np.float16)
+    q = O.quantize_act(x, cb, 2, 1, mode=O.SCALE_INLIER)
+    assert q["t"][0] == np.float32(3.0)
+    assert list(q["a"][0]) == [3, 2, 1, 2, 2, 3]
+    assert list(q["max_idx"][0]) == [0] and list(q["min_idx"][0]) == [2]
+    assert list(q["residual"][0]) == [np.float32(10 - 3 * 0.75), np.float32(-2 - 3 * -0.5)]
+
+
+def test_inlier_scale_is_the_absmax_of_the_unlisted():
+    L = small_layer(n=6, d_in=96, k=5, seed=7)
+    q = O.quantize_act(L.x, L.cb_a, 4, 5, mode=O.SCALE_INLIER)
+    ta = O.act_scale(L.x)
+    for i in range(L.spec.n):
+        listed = set(q["max_idx"][i]) | set(q["min_idx"][i])
+        rest = np.abs(np.delete(L.x[i].astype(np.float64), sorted(listed)))
+        assert q["t"][i] == np.float32(rest.max()) <= ta[i]
+    q0 = O.quantize_act(L.x, L.cb_a, 4, 0, mode=O.SCALE_INLIER)
+    assert np.array_equal(q0["t"], ta)               # no outliers: the absmax
+
+
+def test_inlier_scale_all_channels_listed():
+    """Every channel listed: t = 0, the main branch vanishes and the outlier
+    branch alone gives the GEMM of the fp16 activations."""
+    L = small_layer(n=3, d_in=16, d_out=12, k=16)
+    r = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, 4, 4, 16, mode=O.SCALE_INLIER)
+    assert np.all(r["t"] == 0) and np.all(r["y_star"] == 0)
+    what = L.cb_w.astype(np.float64)[L.w_idx] * L.s_w.astype(np.float64)[None, :]
+    ref = L.x.astype(np.float64) @ what
+    np.testing.assert_allclose(r["y"], ref, rtol=1e-12, atol=1e-9)
+
+
+@pytest.mark.parametrize("seed,k", [(4, 2), (5, 6)])
+def test_inlier_lookahead_equals_conventional_scheme(seed, k):
+    L = small_layer(n=5, d_in=32, d_out=9, k=k, seed=seed)
+    r = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, 4, 4, k, mode=O.SCALE_INLIER)
+    what = L.cb_w.astype(np.float64)[L.w_idx] * L.s_w.astype(np.float64)[None, :]
+    mixed = r["t"].astype(np.float64)[:, None] * L.cb_a.astype(np.float64)[r["a"]]
+    for i in range(L.spec.n):
+        for p in set(r["max_idx"][i]) | set(r["min_idx"][i]):
+            mixed[i, p] = float(L.x[i, p])
+    ref = mixed @ what
+    scale = np.abs(mixed) @ np.abs(what)
+    assert np.all(np.abs(r["y"] - ref) <= 2.0 ** -22 * scale + 1e-12)
+
+
 # ---------------------------------------------------------------- Sec. V-A, OASIS-S
 def test_static_lists_by_hand():
     """Fixed thresholds: the channels at or beyond them, in channel order,
