@@ -190,13 +190,14 @@ def calibrate_copy(mib):
                       "bytes_written_per_copy": nbytes, "copies": 10}), flush=True)
 
 
-def cpu_baseline(layer, budget_s=12.0):
+def cpu_baseline(layer, budget_s=12.0, mode=0):
     """Time the oracle's whole-layer forward on the host (single-threaded numpy)."""
     from oracle import oasis_oracle as O
     s = layer.spec
     reps, t0 = 0, time.perf_counter()
     while True:
-        O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w, s.k)
+        O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w, s.k,
+                  mode=mode)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 50:
@@ -220,6 +221,9 @@ def main():
                          "values of the calibration tokens), 2k places per side")
     ap.add_argument("--bits-a", type=int, default=0, choices=[0, 1, 2, 3, 4],
                     help="activation bits (0: the config's, 4); 3 is the paper's W4A3 point")
+    ap.add_argument("--scale", default="absmax", choices=["absmax", "inlier"],
+                    help="per-token scale: absmax of all channels, or of the channels in "
+                         "neither outlier list (a second quantize launch; no look-ahead)")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
     ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate", "lookahead"],
@@ -255,6 +259,13 @@ def main():
     spec = synth.config(args.config)
     if args.bits_a and args.bits_a != spec.b_a:
         spec = dataclasses.replace(spec, b_a=args.bits_a, name=f"{spec.name}_a{args.bits_a}")
+    scale = oasis.SCALE_INLIER if args.scale == "inlier" else oasis.SCALE_ABSMAX
+    if args.scale == "inlier":
+        if args.path == "lookahead":
+            print("bench.py: --scale inlier has no look-ahead schedule (the scale needs the lists)",
+                  file=sys.stderr)
+            sys.exit(2)
+        spec = dataclasses.replace(spec, name=f"{spec.name}_inlier")
     if args.oasis_s:
         if args.path == "lookahead":
             print("bench.py: --oasis-s has no look-ahead schedule (no top-k to overlap)",
@@ -298,11 +309,11 @@ def main():
     # Every call of the path, with the arguments the step uses (c = weight copy).
     calls = {
         "build_lut": lambda c: oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut),
-        "quantize_act": lambda c: oasis.quantize_act(x, lut, b_a, k, out=q),
+        "quantize_act": lambda c: oasis.quantize_act(x, lut, b_a, k, scale, out=q),
         "build_lut_quantize_act": lambda c: oasis.build_lut_quantize_act(
-            cb_a, b_a, cb_w, b_w, x, k, lut=lut, out=q),
+            cb_a, b_a, cb_w, b_w, x, k, scale, lut=lut, out=q),
         "quantize_act_static": lambda c: oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1],
-                                                                   out=q),
+                                                                   scale, out=q),
         "cluster_act": lambda c: oasis.cluster_act(x, lut, b_a, out=q),
         "detect_outliers": lambda c: oasis.detect_outliers(x, lut, b_a, k, out=q),
         "outlier_compensate": lambda c: oasis.outlier_compensate_rows(
@@ -333,9 +344,9 @@ def main():
         """LUT block + quantization: one launch, or two for OASIS-S."""
         if thr:
             oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
-            oasis.quantize_act_static(x, L, b_a, k, thr[0], thr[1], out=q)
+            oasis.quantize_act_static(x, L, b_a, k, thr[0], thr[1], scale, out=q)
         else:
-            oasis.build_lut_quantize_act(cb_a, b_a, cb_w, b_w, x, k, lut=L, out=q)
+            oasis.build_lut_quantize_act(cb_a, b_a, cb_w, b_w, x, k, scale, lut=L, out=q)
 
     def step(i):
         """Step i (weight copy i mod copies)."""
@@ -419,8 +430,8 @@ def main():
     last = args.warmup + nsteps - 1
     c_last = last % copies
     oasis.build_lut(cb_a, b_a, cb_w, b_w, out=lut)
-    q1 = oasis.quantize_act(x, lut, b_a, k) if not thr else \
-        oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1])
+    q1 = oasis.quantize_act(x, lut, b_a, k, scale) if not thr else \
+        oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1], scale)
     if path == "fused":
         y_ref = oasis.lut_gemm_compensated_rows(q1["idx_act"], q1["act_scale"], idx_w[c_last],
                                                 idx_wr[c_last], s_w, lut, b_a, b_w,
@@ -504,6 +515,7 @@ def main():
         "config": {"workload": s.name, "n": n, "d_in": d_in, "d_out": d_out, "k_per_side": k,
                    "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
                    "path": path, "outliers": "static" if thr else "top-k",
+                   "scale": args.scale,
                    "weight_copies": copies},
         "schedule_check": schedule_ok,
         "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),
@@ -512,7 +524,7 @@ def main():
         "roofline_main_branch": main_branch,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layer)
+        out["cpu_baseline"] = cpu_baseline(layer, mode=scale)
     print(json.dumps(out), flush=True)
 
 

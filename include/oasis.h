@@ -61,7 +61,11 @@ enum oasis_status {
 
 enum oasis_scale_mode {
   OASIS_SCALE_ABSMAX = 0,     /* t_i = max_p |x_ip| (outliers included)            */
-  OASIS_SCALE_NONE = 1        /* t_i = 1                                           */
+  OASIS_SCALE_NONE = 1,       /* t_i = 1                                           */
+  OASIS_SCALE_INLIER = 2      /* t_i = max |x_ip| over the channels in neither
+                                 outlier list (0 if every channel is listed); the
+                                 lists come first, so there is no look-ahead split:
+                                 a second launch computes t, codes and residuals */
 };
 
 enum oasis_gemm_algo {
@@ -103,7 +107,7 @@ int oasis_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int
  *   x         : DEVICE fp16 [n][d_in], 16-byte aligned.
  *   lut       : DEVICE LUT block built with the same b_a (its C_A is used).
  *   k         : outliers per side per token, 0 <= k <= d_in.
- *   scale_mode: OASIS_SCALE_ABSMAX or OASIS_SCALE_NONE.
+ *   scale_mode: OASIS_SCALE_ABSMAX, OASIS_SCALE_NONE or OASIS_SCALE_INLIER.
  * Outputs (DEVICE, fully overwritten):
  *   idx_act   : uint8 [n][d_in/2] cluster index of EVERY channel, outliers
  *               included: #{c : x >= fp32(t * b_c)} with
@@ -132,7 +136,8 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
  *   channel order and at most k of them (k = places per side); the places
  *   left hold channel -1 and residual 0 (the compensation calls skip them).
  *   Residuals as in oasis_quantize_act.  thr_lo < thr_hi, neither NaN
- *   (+-inf allowed).
+ *   (+-inf allowed).  With OASIS_SCALE_INLIER, t excludes the listed
+ *   channels (unused places excluded nothing).
  * Errors: NULL, SHAPE, BITS, K, ALIGN, MODE (scale mode or thresholds),
  * TOO_LARGE, LAUNCH.
  */
@@ -166,7 +171,8 @@ int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t
  * and outputs as oasis_quantize_act restricted to idx_act and act_scale.
  * With oasis_detect_outliers on a second stream this is the GPU form of the
  * look-ahead schedule: the main-branch GEMM needs only these outputs, so it
- * does not wait for outlier detection (Sec. II-C, III-C).
+ * does not wait for outlier detection (Sec. II-C, III-C).  OASIS_SCALE_INLIER
+ * needs the lists first and is refused (MODE).
  * Errors: NULL, SHAPE, BITS, ALIGN, MODE, TOO_LARGE, LAUNCH.
  */
 int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
@@ -177,7 +183,8 @@ int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block*
  * (Orizuru and the Error Calculation Unit, Sec. IV-A, IV-D): max_idx,
  * min_idx and residual exactly as oasis_quantize_act writes them (the scale
  * and the cluster index of each outlier are recomputed from x).  k == 0 is a
- * no-op.  Errors: NULL, SHAPE, BITS, K, ALIGN, MODE, TOO_LARGE, LAUNCH.
+ * no-op.  OASIS_SCALE_INLIER is refused (MODE), as in oasis_cluster_act.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, MODE, TOO_LARGE, LAUNCH.
  */
 int oasis_detect_outliers(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,
                           int k, int scale_mode, int32_t* max_idx, int32_t* min_idx,

@@ -65,6 +65,17 @@ const char* oasis_status_str(int status) {
 
 const char* oasis_version(void) { return "oasis 0.1 gfx950"; }
 
+// Inlier scale: the quantize launch (absmax scale) writes the lists, then a
+// second launch recomputes t, the codes and the residuals from them.
+static int quantize_launch(oasis::QuantArgs a, hipStream_t stream) {
+  const bool inlier = a.scale_mode == OASIS_SCALE_INLIER;
+  if (inlier) a.scale_mode = OASIS_SCALE_ABSMAX;
+  hipError_t e = oasis::launch_quantize(a, stream);
+  if (e != hipSuccess || !inlier) return launched(e);
+  if (a.lut_out) a.lut = a.lut_out;
+  return launched(oasis::launch_inlier_codes(a, stream));
+}
+
 int oasis_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
                     oasis_lut_block* out, hipStream_t stream) {
   if (!cb_act || !cb_wgt || !out) return OASIS_ERR_NULL;
@@ -86,7 +97,9 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
   if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
   if (!bits_ok(b_a)) return OASIS_ERR_BITS;
   if (k < 0 || k > d_in) return OASIS_ERR_K;
-  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE &&
+      scale_mode != OASIS_SCALE_INLIER)
+    return OASIS_ERR_MODE;
   if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
   if (oasis::quantize_lds_bytes(d_in, k) > kMaxLds) return OASIS_ERR_TOO_LARGE;
   if (n == 0) return OASIS_OK;
@@ -97,7 +110,7 @@ int oasis_quantize_act(const uint16_t* x, int n, int d_in, const oasis_lut_block
     return OASIS_ERR_ALIGN;
   oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
                      max_idx, min_idx, residual, nullptr, {}, 0};
-  return launched(oasis::launch_quantize(a, stream));
+  return quantize_launch(a, stream);
 }
 
 int oasis_quantize_act_static(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut,
@@ -107,7 +120,9 @@ int oasis_quantize_act_static(const uint16_t* x, int n, int d_in, const oasis_lu
   if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
   if (!bits_ok(b_a)) return OASIS_ERR_BITS;
   if (k < 0 || k > d_in) return OASIS_ERR_K;
-  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE &&
+      scale_mode != OASIS_SCALE_INLIER)
+    return OASIS_ERR_MODE;
   if (std::isnan(thr_hi) || std::isnan(thr_lo) || !(thr_lo < thr_hi)) return OASIS_ERR_MODE;
   if (d_in > 65536) return OASIS_ERR_TOO_LARGE;
   if (oasis::quantize_lds_bytes(d_in, k) > kMaxLds) return OASIS_ERR_TOO_LARGE;
@@ -119,7 +134,7 @@ int oasis_quantize_act_static(const uint16_t* x, int n, int d_in, const oasis_lu
     return OASIS_ERR_ALIGN;
   oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
                      max_idx, min_idx, residual, nullptr, {}, 0, 1, thr_hi, thr_lo};
-  return launched(oasis::launch_quantize(a, stream));
+  return quantize_launch(a, stream);
 }
 
 int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
@@ -131,7 +146,9 @@ int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t
   if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
   if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
   if (k < 0 || k > d_in) return OASIS_ERR_K;
-  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE) return OASIS_ERR_MODE;
+  if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE &&
+      scale_mode != OASIS_SCALE_INLIER)
+    return OASIS_ERR_MODE;
   for (int i = 0; i < (1 << b_a); ++i) {
     const float v = half_bits_to_float(cb_act[i]);
     if (!std::isfinite(v)) return OASIS_ERR_CODEBOOK;
@@ -151,7 +168,7 @@ int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t
                      max_idx, min_idx, residual, lut, {}, b_w};
   for (int i = 0; i < (1 << b_a); ++i) a.cb.act[i] = cb_act[i];
   for (int i = 0; i < (1 << b_w); ++i) a.cb.wgt[i] = cb_wgt[i];
-  return launched(oasis::launch_quantize(a, stream));
+  return quantize_launch(a, stream);
 }
 
 int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,

@@ -162,6 +162,9 @@ hipError_t launch_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
 hipError_t launch_cluster(const QuantArgs& a, hipStream_t s);   // scale + codes only
 hipError_t launch_outliers(const QuantArgs& a, hipStream_t s);  // lists + residuals only
+// inlier scale: t from the channels in neither list, then codes and residuals
+// (after a launch that wrote the lists; reads C_A from a.lut)
+hipError_t launch_inlier_codes(const QuantArgs& a, hipStream_t s);
 hipError_t launch_gemm_lut(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s);
 // Y (+)= Y* + Y' in one launch when a.n <= kFusedMaxTokens.

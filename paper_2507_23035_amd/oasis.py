@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "liboasis.so")
 
 SCALE_ABSMAX = 0
 SCALE_NONE = 1
+SCALE_INLIER = 2
 ALGO_LUT = 0
 ALGO_MFMA = 1
 LUT_BLOCK_BYTES = 256 * 4 + 16 * 2 + 16 * 2

@@ -87,7 +87,7 @@ def test_quantize_errors(lib):
     assert q(P, 4, 16, P, 0, 1, 0, P, P, P, P, P, None) == -3
     assert q(P, 4, 16, P, 4, 17, 0, P, P, P, P, P, None) == -4
     assert q(P, 4, 16, P, 4, -1, 0, P, P, P, P, P, None) == -4
-    assert q(P, 4, 16, P, 4, 1, 2, P, P, P, P, P, None) == -7
+    assert q(P, 4, 16, P, 4, 1, 3, P, P, P, P, P, None) == -7       # modes 0..2
     assert q(P, 4, 65544, P, 4, 1, 0, P, P, P, P, P, None) == -9
     assert q(P, 4, 32768, P, 4, 32768, 0, P, P, P, P, P, None) == -9   # LDS budget
     assert q(None, 4, 16, P, 4, 1, 0, P, P, P, P, P, None) == -1
@@ -110,7 +110,7 @@ def test_build_lut_quantize_errors(lib):
     assert f(desc.ctypes.data, 4, W, 4, P, P, 4, 16, 1, 0, P, P, P, P, P, None) == -5
     assert f(A, 4, W, 4, MIS, P, 4, 16, 1, 0, P, P, P, P, P, None) == -6
     assert f(A, 4, W, 4, P, MIS, 4, 16, 1, 0, P, P, P, P, P, None) == -6
-    assert f(A, 4, W, 4, P, P, 4, 16, 1, 2, P, P, P, P, P, None) == -7
+    assert f(A, 4, W, 4, P, P, 4, 16, 1, 3, P, P, P, P, P, None) == -7
     assert f(A, 4, W, 4, P, P, 4, 65544, 1, 0, P, P, P, P, P, None) == -9
     assert f(A, 4, W, 4, P, None, 4, 16, 1, 0, P, P, P, P, P, None) == -1
 
@@ -124,6 +124,7 @@ def test_quantize_static_errors(lib):
     assert f(P, 4, 16, P, 5, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -3
     assert f(P, 4, 16, P, 4, 17, 0, 2.0, -2.0, P, P, P, P, P, None) == -4
     assert f(P, 4, 16, P, 4, 1, 0, -2.0, 2.0, P, P, P, P, P, None) == -7     # lo >= hi
+    assert f(P, 4, 16, P, 4, 1, 3, 2.0, -2.0, P, P, P, P, P, None) == -7     # mode
     assert f(P, 4, 16, P, 4, 1, 0, float("nan"), -2.0, P, P, P, P, P, None) == -7
     assert f(None, 4, 16, P, 4, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -1
     assert f(MIS, 4, 16, P, 4, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -6
@@ -135,6 +136,7 @@ def test_cluster_and_detect_errors(lib):
     assert c(P, 4, 12, P, 4, 0, P, P, None) == -2
     assert c(P, 4, 16, P, 5, 0, P, P, None) == -3
     assert c(P, 4, 16, P, 4, 3, P, P, None) == -7
+    assert c(P, 4, 16, P, 4, 2, P, P, None) == -7   # the inlier scale needs the lists
     assert c(None, 4, 16, P, 4, 0, P, P, None) == -1
     assert c(P, 4, 16, P, 4, 0, MIS, P, None) == -6
     d = lib.oasis_detect_outliers
@@ -142,6 +144,7 @@ def test_cluster_and_detect_errors(lib):
     assert d(P, 4, 16, P, 4, 2, 0, None, P, P, None) == -1
     assert d(P, 4, 16, P, 4, 0, 0, None, None, None, None) == 0   # k = 0: nothing to do
     assert d(P, 4, 65544, P, 4, 1, 0, P, P, P, None) == -9
+    assert d(P, 4, 16, P, 4, 1, 2, P, P, P, None) == -7
 
 
 def test_fused_gemm_errors(lib):

@@ -113,13 +113,17 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
                                q["max_idx"], q["min_idx"], q["residual"], y=yf, accumulate=True)
     torch.cuda.synchronize()
     assert_close(yf.cpu().numpy()[rows] - 0.5, ref["y"], "Y fused, accumulate")
-    c = oasis.cluster_act(x, lut, b_a, scale_mode)
-    d = oasis.detect_outliers(x, lut, b_a, k, scale_mode)
-    check_quant({**c, **d}, ref, k)
-    r = oasis.forward_lookahead(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode)
-    torch.cuda.synchronize()
-    check_quant(r, ref, k)
-    assert_close(r["y"].cpu().numpy()[rows], ref["y"], "Y look-ahead")
+    if scale_mode == oasis.SCALE_INLIER:  # the scale needs the lists: no look-ahead split
+        with pytest.raises(oasis.OasisError):
+            oasis.cluster_act(x, lut, b_a, scale_mode)
+    else:
+        c = oasis.cluster_act(x, lut, b_a, scale_mode)
+        d = oasis.detect_outliers(x, lut, b_a, k, scale_mode)
+        check_quant({**c, **d}, ref, k)
+        r = oasis.forward_lookahead(x, lut, idx_w, s_w, b_a, b_w, k, scale_mode)
+        torch.cuda.synchronize()
+        check_quant(r, ref, k)
+        assert_close(r["y"].cpu().numpy()[rows], ref["y"], "Y look-ahead")
     # the other merge order: main branch first, compensation merged into it
     y = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
     oasis.outlier_compensate(q["max_idx"], q["min_idx"], q["residual"], idx_w, lut, b_w, s_w,
@@ -186,6 +190,41 @@ def test_scale_mode_none():
     spec = synth.custom(6, 256, 80, 4, seed=11, dist="normal", outlier_count=2,
                         outlier_scale=4.0)
     run_full(synth.make_layer(spec), scale_mode=oasis.SCALE_NONE)
+
+
+INLIER = [
+    # name or (n, d_in, d_out, k, seed)
+    "decode_8x4096x4096",
+    "tiny_4x256x256",
+    (17, 512, 257, 8, 41),       # ragged
+    (2, 128, 96, 128, 42),       # every channel listed: t = 0
+    (70, 1032, 130, 20, 43),     # many tokens, d_in not a multiple of 128
+]
+
+
+@pytest.mark.parametrize("case", INLIER, ids=str)
+def test_inlier_scale(case):
+    """Inlier scale (t from the unlisted channels): codes, scales, lists and
+    residuals bit for bit, every schedule's y within tolerance."""
+    if isinstance(case, str):
+        L = synth.make_layer(synth.config(case))
+    else:
+        n, d_in, d_out, k, seed = case
+        L = synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed))
+    run_full(L, scale_mode=oasis.SCALE_INLIER)
+    # fused LUT build and the OASIS-S lists take the same second pass
+    s = L.spec
+    x = torch.from_numpy(L.x.view(np.int16).copy()).to(dev())
+    ref = O.quantize_act(L.x, L.cb_a, s.b_a, s.k, mode=O.SCALE_INLIER)
+    _, q = oasis.build_lut_quantize_act(L.cb_a, s.b_a, L.cb_w, s.b_w, x, s.k,
+                                        scale_mode=oasis.SCALE_INLIER)
+    check_quant(q, ref, s.k)
+    thr = (1.5, -1.5)
+    ref_s = O.quantize_act_static(L.x, L.cb_a, s.b_a, s.k, thr[0], thr[1], mode=O.SCALE_INLIER)
+    lut = oasis.build_lut(L.cb_a, s.b_a, L.cb_w, s.b_w)
+    q_s = oasis.quantize_act_static(x, lut, s.b_a, s.k, thr[0], thr[1],
+                                    scale_mode=oasis.SCALE_INLIER)
+    check_quant(q_s, ref_s, s.k)
 
 
 @pytest.mark.parametrize("k", [6, 40])  # 40: compensation inside the GEMV main loop
