@@ -666,37 +666,88 @@ static hipError_t launch_parts(const QuantArgs& a, hipStream_t s) {
 // Inlier scale, a second pass once the lists exist: per token (one workgroup
 // of 256 threads), t = max |x| over the channels in neither list (0 when all
 // are listed), the cluster index of every channel under that t by the same
-// boundary rule, and the residuals of the listed channels.  LDS: two bitmaps
-// of d_in bits (listed; in the max list).
+// boundary rule, and the residuals of the listed channels.  The token (VR
+// vectors of 8 channels per thread), its list entries and C_A are requested
+// together at the start; the token is also staged in LDS for the residuals.
+// LDS: the token (2 B per channel), then two bitmaps of d_in bits (listed;
+// in the max list).
 // ----------------------------------------------------------------------------
+struct InlierBounds {
+  float p[15];  // P_c, +inf past the last boundary
+};
+
+struct InlierCb {
+  float c[16];  // C_A in fp32
+};
+
+__device__ __forceinline__ float inlier_centroid(const InlierCb cb, uint32_t a) {
+  float v = cb.c[0];
+#pragma unroll
+  for (int q = 1; q < 16; ++q) v = a == (uint32_t)q ? cb.c[q] : v;
+  return v;
+}
+
+__device__ __forceinline__ uint32_t inlier_code(const InlierBounds b, float xf) {
+  uint32_t a = 0;
+#pragma unroll
+  for (int c = 0; c < 15; ++c) a += xf >= b.p[c] ? 1u : 0u;
+  return a;
+}
+
+template <int VR>
 __global__ void __launch_bounds__(256) k_inlier_codes(QuantArgs A) {
 #pragma clang fp contract(off)
-  extern __shared__ uint32_t bits[];
+  extern __shared__ __align__(16) unsigned char ismem[];
   __shared__ uint32_t wmax[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i = blockIdx.x;
   const int d_in = A.d_in, k = A.k, nw = (d_in + 31) / 32, nvec = d_in / 8;
-  uint32_t* listed = bits;
-  uint32_t* inmax = bits + nw;
-  for (int w = tid; w < 2 * nw; w += 256) bits[w] = 0u;
-  __syncthreads();
+  uint16_t* xs = reinterpret_cast<uint16_t*>(ismem);
+  uint32_t* listed = reinterpret_cast<uint32_t*>(ismem + 2 * (size_t)d_in);
+  uint32_t* inmax = listed + nw;
+  // ---- requests: the token, the list entries, C_A
+  const uint4* xrow = reinterpret_cast<const uint4*>(A.x + (size_t)i * d_in);
+  uint4 xv[VR];
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    const int v = tid + 256 * u;
+    xv[u] = v < nvec ? xrow[v] : make_uint4(0u, 0u, 0u, 0u);
+  }
   const int32_t* mx = A.max_idx + (size_t)i * k;
   const int32_t* mn = A.min_idx + (size_t)i * k;
-  for (int e = tid; e < 2 * k; e += 256) {
-    const int p = e < k ? mx[e] : mn[e - k];
+  constexpr int EPT = 4;  // list entries per thread per pass
+  int pe[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int e = tid + 256 * u;
+    pe[u] = e < 2 * k ? (e < k ? mx[e] : mn[e - k]) : -1;
+  }
+  InlierCb ca;
+#pragma unroll
+  for (int c = 0; c < 16; ++c) ca.c[c] = h2f(A.lut->cb_act[c]);
+  for (int w = tid; w < 2 * nw; w += 256) listed[w] = 0u;
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    const int v = tid + 256 * u;
+    if (v < nvec) reinterpret_cast<uint4*>(xs)[v] = xv[u];
+  }
+  __syncthreads();
+  for (int e = tid, u = 0; e < 2 * k; e += 256, ++u) {
+    const int p = u < EPT ? pe[u < EPT ? u : 0] : (e < k ? mx[e] : mn[e - k]);
     if (p >= 0 && p < d_in) {
       atomicOr(&listed[p >> 5], 1u << (p & 31));
       if (e < k) atomicOr(&inmax[p >> 5], 1u << (p & 31));
     }
   }
   __syncthreads();
-  // |x| of finite fp16 values orders like its 15 low bits
-  const uint4* xrow = reinterpret_cast<const uint4*>(A.x + (size_t)i * d_in);
+  // ---- t: |x| of finite fp16 values orders like its 15 low bits
   uint32_t m = 0;
-  for (int v = tid; v < nvec; v += 256) {
-    const uint4 q = xrow[v];
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    const int v = tid + 256 * u;
+    if (v >= nvec) continue;
     const uint32_t lst = (listed[v >> 2] >> (8 * (v & 3))) & 0xFFu;  // channels 8v .. 8v + 7
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    const uint32_t w[4] = {xv[u].x, xv[u].y, xv[u].z, xv[u].w};
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       if (!((lst >> (2 * c)) & 1u)) m = max(m, w[c] & 0x7FFFu);
@@ -710,48 +761,56 @@ __global__ void __launch_bounds__(256) k_inlier_codes(QuantArgs A) {
   m = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
   const float t = h2f((uint16_t)m);
   if (tid == 0) A.act_scale[i] = t;
-  // scaled boundaries P_c = fp32(t * b_c), b_c = fp32(C_A[c] + C_A[c+1]) * 0.5
+  // ---- scaled boundaries P_c = fp32(t * b_c), b_c = fp32(C_A[c] + C_A[c+1]) * 0.5
   const int nb = (1 << A.b_a) - 1;
-  float P[15];
+  InlierBounds P;
 #pragma unroll
-  for (int c = 0; c < 15; ++c) {
-    const float bc = c < nb ? (h2f(A.lut->cb_act[c]) + h2f(A.lut->cb_act[c + 1])) * 0.5f : 0.0f;
-    P[c] = c < nb ? t * bc : __builtin_inff();
-  }
-  auto code_of = [&](float xv) {
-    uint32_t a = 0;
-#pragma unroll
-    for (int c = 0; c < 15; ++c) a += xv >= P[c] ? 1u : 0u;
-    return a;
-  };
+  for (int c = 0; c < 15; ++c)
+    P.p[c] = c < nb ? t * ((ca.c[c] + ca.c[c + 1]) * 0.5f) : __builtin_inff();
   uint32_t* arow = reinterpret_cast<uint32_t*>(A.idx_act + (size_t)i * (d_in / 2));
-  for (int v = tid; v < nvec; v += 256) {
-    const uint4 q = xrow[v];
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    const int v = tid + 256 * u;
+    if (v >= nvec) continue;
+    const uint32_t w[4] = {xv[u].x, xv[u].y, xv[u].z, xv[u].w};
     uint32_t packed = 0;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      packed |= code_of(h2f((uint16_t)(w[c] & 0xFFFFu))) << (8 * c);
-      packed |= code_of(h2f((uint16_t)(w[c] >> 16))) << (8 * c + 4);
+      packed |= inlier_code(P, h2f((uint16_t)(w[c] & 0xFFFFu))) << (8 * c);
+      packed |= inlier_code(P, h2f((uint16_t)(w[c] >> 16))) << (8 * c + 4);
     }
     arow[v] = packed;
   }
-  // residuals: r = fp32(x - fp32(t * C_A[a])); a min entry also in the max list gets 0
-  for (int e = tid; e < 2 * k; e += 256) {
-    const int p = e < k ? mx[e] : mn[e - k];
+  // ---- residuals: r = fp32(x - fp32(t * C_A[a])); a min entry also in the max list gets 0
+  for (int e = tid, u = 0; e < 2 * k; e += 256, ++u) {
+    const int p = u < EPT ? pe[u < EPT ? u : 0] : (e < k ? mx[e] : mn[e - k]);
     if (p < 0 || p >= d_in) continue;  // an unused place keeps its 0
-    const float xv = h2f(A.x[(size_t)i * d_in + p]);
-    const float xhat = t * h2f(A.lut->cb_act[code_of(xv)]);
+    const float xf = h2f(xs[p]);
+    const float c = inlier_centroid(ca, inlier_code(P, xf));
     const bool dup = e >= k && ((inmax[p >> 5] >> (p & 31)) & 1u);
-    A.residual[(size_t)i * 2 * k + e] = dup ? 0.0f : xv - xhat;
+    A.residual[(size_t)i * 2 * k + e] = dup ? 0.0f : xf - t * c;
   }
 }
 
 hipError_t launch_inlier_codes(const QuantArgs& a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
-  const size_t lds = 2 * (size_t)((a.d_in + 31) / 32) * 4;
-  hipLaunchKernelGGL(k_inlier_codes, dim3(a.n), dim3(256), lds, s, a);
-  return hipGetLastError();
+  const int nvec = a.d_in / 8;
+  const size_t lds = 2 * (size_t)a.d_in + 2 * (size_t)((a.d_in + 31) / 32) * 4;
+  auto go = [&](auto kern) {
+    if (lds > 64 * 1024) {
+      hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(a.n), dim3(256), lds, s, a);
+    return hipGetLastError();
+  };
+  if (nvec <= 256) return go(k_inlier_codes<1>);
+  if (nvec <= 512) return go(k_inlier_codes<2>);
+  if (nvec <= 1024) return go(k_inlier_codes<4>);
+  if (nvec <= 2048) return go(k_inlier_codes<8>);
+  if (nvec <= 4096) return go(k_inlier_codes<16>);
+  return go(k_inlier_codes<32>);
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s) { return launch_parts<true, true>(a, s); }
