@@ -685,7 +685,10 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
   // lane (g, tc) of tile (c, f): token tok0 + 16f + tc, columns
   // j0 + 16c + 4g .. + 3
   const int tc = lane & 15;
-  const bool vec = (A.d_out & 3) == 0;
+  // 16-byte loads and stores only where y and the scales allow them (the
+  // boundary promises 4-byte alignment)
+  const bool vec = (A.d_out & 3) == 0 && (reinterpret_cast<uintptr_t>(A.y) & 15u) == 0 &&
+                   (reinterpret_cast<uintptr_t>(A.w_scale) & 15u) == 0;
 #pragma unroll
   for (int c = 0; c < CW; ++c) {
     const int j = j0 + 16 * c + 4 * g;
