@@ -67,6 +67,7 @@ def call_bytes(n, d_in, d_out, k, path):
         "build_lut": 2 * 32 + 1088,
         "quantize_act": x + codes + 4 * n + lists,
         "build_lut_quantize_act": x + codes + 4 * n + lists + 1088,
+        "build_lut_quantize_act_static": x + codes + 4 * n + lists + 1088,
         "quantize_act_static": x + codes + 4 * n + lists,
         "cluster_act": x + codes + 4 * n,
         "detect_outliers": x + lists,
@@ -83,6 +84,7 @@ KERNEL_SOURCES = {
     "build_lut": ["lut.hip"],
     "quantize_act": ["quantize.hip"], "cluster_act": ["quantize.hip"],
     "build_lut_quantize_act": ["quantize.hip"], "quantize_act_static": ["quantize.hip"],
+    "build_lut_quantize_act_static": ["quantize.hip"],
     "detect_outliers": ["quantize.hip"],
     "outlier_compensate": ["compensate.hip"],
     "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
@@ -116,6 +118,7 @@ def measured_traffic(call, workload):
 CALL_SYMBOLS = {   # kernel symbol fragment of each call's dominant kernel
     "build_lut": "k_build_lut", "quantize_act": "k_quantize<", "cluster_act": "k_quantize<",
     "build_lut_quantize_act": "k_quantize<", "quantize_act_static": "k_quantize<",
+    "build_lut_quantize_act_static": "k_quantize<",
     "detect_outliers": "k_quantize<", "outlier_compensate": "k_compensate",
     "lut_gemm": "k_gemm_mfma", "lut_gemm_compensated": "k_gemm_mfma",
     "lut_gemm_compensated_rows": "k_gemm_mfma",
@@ -314,6 +317,8 @@ def main():
             cb_a, b_a, cb_w, b_w, x, k, scale, lut=lut, out=q),
         "quantize_act_static": lambda c: oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1],
                                                                    scale, out=q),
+        "build_lut_quantize_act_static": lambda c: oasis.build_lut_quantize_act_static(
+            cb_a, b_a, cb_w, b_w, x, k, thr[0], thr[1], scale, lut=lut, out=q),
         "cluster_act": lambda c: oasis.cluster_act(x, lut, b_a, out=q),
         "detect_outliers": lambda c: oasis.detect_outliers(x, lut, b_a, k, out=q),
         "outlier_compensate": lambda c: oasis.outlier_compensate_rows(
@@ -329,22 +334,22 @@ def main():
             q["min_idx"], q["residual"], y=y),
     }
     if path == "fused":
-        names = (["build_lut", "quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
+        names = (["build_lut_quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
             ["lut_gemm_compensated_rows"]
         gemm_name = "lut_gemm_compensated_rows"
     elif path == "lookahead":
         names = ["build_lut", "cluster_act", "detect_outliers", "lut_gemm", "outlier_compensate"]
         gemm_name = "lut_gemm"
     else:
-        names = (["build_lut", "quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
+        names = (["build_lut_quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
             ["outlier_compensate", "lut_gemm"]
         gemm_name = "lut_gemm"
 
     def quantize(L):
-        """LUT block + quantization: one launch, or two for OASIS-S."""
+        """LUT block + quantization in one launch (a second one for the inlier scale)."""
         if thr:
-            oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
-            oasis.quantize_act_static(x, L, b_a, k, thr[0], thr[1], scale, out=q)
+            oasis.build_lut_quantize_act_static(cb_a, b_a, cb_w, b_w, x, k, thr[0], thr[1], scale,
+                                                lut=L, out=q)
         else:
             oasis.build_lut_quantize_act(cb_a, b_a, cb_w, b_w, x, k, scale, lut=L, out=q)
 

@@ -165,6 +165,19 @@ int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t
                                  hipStream_t stream);
 
 /*
+ * oasis_build_lut_quantize_act_static - oasis_build_lut followed by
+ * oasis_quantize_act_static (OASIS-S, Sec. V-A), in one launch as in
+ * oasis_build_lut_quantize_act.  Arguments, outputs and errors: those of the
+ * two calls.
+ */
+int oasis_build_lut_quantize_act_static(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt,
+                                        int b_w, oasis_lut_block* lut, const uint16_t* x, int n,
+                                        int d_in, int k, int scale_mode, float thr_hi,
+                                        float thr_lo, uint8_t* idx_act, float* act_scale,
+                                        int32_t* max_idx, int32_t* min_idx, float* residual,
+                                        hipStream_t stream);
+
+/*
  * oasis_cluster_act - the main branch's share of oasis_quantize_act: scale
  * and cluster index of every channel (Sec. III-C1: the whole token is
  * clustered, outliers included), without outlier detection.  Same arguments

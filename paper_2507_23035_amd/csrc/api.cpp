@@ -137,17 +137,21 @@ int oasis_quantize_act_static(const uint16_t* x, int n, int d_in, const oasis_lu
   return quantize_launch(a, stream);
 }
 
-int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
-                                 oasis_lut_block* lut, const uint16_t* x, int n, int d_in, int k,
-                                 int scale_mode, uint8_t* idx_act, float* act_scale,
-                                 int32_t* max_idx, int32_t* min_idx, float* residual,
-                                 hipStream_t stream) {
+// oasis_build_lut_quantize_act and its OASIS-S form: every check, then one
+// launch whose first workgroup also writes the LUT block.
+static int build_lut_quantize(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                              oasis_lut_block* lut, const uint16_t* x, int n, int d_in, int k,
+                              int scale_mode, int static_thr, float thr_hi, float thr_lo,
+                              uint8_t* idx_act, float* act_scale, int32_t* max_idx,
+                              int32_t* min_idx, float* residual, hipStream_t stream) {
   if (!cb_act || !cb_wgt || !lut) return OASIS_ERR_NULL;
   if (n < 0 || d_in < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
   if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
   if (k < 0 || k > d_in) return OASIS_ERR_K;
   if (scale_mode != OASIS_SCALE_ABSMAX && scale_mode != OASIS_SCALE_NONE &&
       scale_mode != OASIS_SCALE_INLIER)
+    return OASIS_ERR_MODE;
+  if (static_thr && (std::isnan(thr_hi) || std::isnan(thr_lo) || !(thr_lo < thr_hi)))
     return OASIS_ERR_MODE;
   for (int i = 0; i < (1 << b_a); ++i) {
     const float v = half_bits_to_float(cb_act[i]);
@@ -165,10 +169,29 @@ int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t
     return OASIS_ERR_ALIGN;
   if (n == 0) return launched(oasis::launch_build_lut(cb_act, b_a, cb_wgt, b_w, lut, stream));
   oasis::QuantArgs a{x, n, d_in, b_a, k, scale_mode, lut, idx_act, act_scale,
-                     max_idx, min_idx, residual, lut, {}, b_w};
+                     max_idx, min_idx, residual, lut, {}, b_w, static_thr, thr_hi, thr_lo};
   for (int i = 0; i < (1 << b_a); ++i) a.cb.act[i] = cb_act[i];
   for (int i = 0; i < (1 << b_w); ++i) a.cb.wgt[i] = cb_wgt[i];
   return quantize_launch(a, stream);
+}
+
+int oasis_build_lut_quantize_act(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
+                                 oasis_lut_block* lut, const uint16_t* x, int n, int d_in, int k,
+                                 int scale_mode, uint8_t* idx_act, float* act_scale,
+                                 int32_t* max_idx, int32_t* min_idx, float* residual,
+                                 hipStream_t stream) {
+  return build_lut_quantize(cb_act, b_a, cb_wgt, b_w, lut, x, n, d_in, k, scale_mode, 0, 0.0f,
+                            0.0f, idx_act, act_scale, max_idx, min_idx, residual, stream);
+}
+
+int oasis_build_lut_quantize_act_static(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt,
+                                        int b_w, oasis_lut_block* lut, const uint16_t* x, int n,
+                                        int d_in, int k, int scale_mode, float thr_hi,
+                                        float thr_lo, uint8_t* idx_act, float* act_scale,
+                                        int32_t* max_idx, int32_t* min_idx, float* residual,
+                                        hipStream_t stream) {
+  return build_lut_quantize(cb_act, b_a, cb_wgt, b_w, lut, x, n, d_in, k, scale_mode, 1, thr_hi,
+                            thr_lo, idx_act, act_scale, max_idx, min_idx, residual, stream);
 }
 
 int oasis_cluster_act(const uint16_t* x, int n, int d_in, const oasis_lut_block* lut, int b_a,

@@ -27,6 +27,7 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_outlier_compensate_rows",
            "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows",
            "oasis_build_lut_quantize_act", "oasis_quantize_act_static",
+           "oasis_build_lut_quantize_act_static",
            "oasis_lut_gemm_compensated_rows")
 
 
@@ -59,6 +60,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     F = ctypes.c_float
     lib.oasis_quantize_act_static.restype = I
     lib.oasis_quantize_act_static.argtypes = [P, I, I, P, I, I, I, F, F, P, P, P, P, P, P]
+    lib.oasis_build_lut_quantize_act_static.restype = I
+    lib.oasis_build_lut_quantize_act_static.argtypes = [P, I, P, I, P, P, I, I, I, I, F, F, P, P,
+                                                        P, P, P, P]
     lib.oasis_build_lut_quantize_act.restype = I
     lib.oasis_build_lut_quantize_act.argtypes = [P, I, P, I, P, P, I, I, I, I, P, P, P, P, P, P]
     lib.oasis_cluster_act.restype = I
@@ -209,6 +213,33 @@ def build_lut_quantize_act(cb_act, b_a: int, cb_wgt, b_w: int, x, k: int,
         _ptr(out["idx_act"]), _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
         _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
         _stream(stream)))
+    return lut, out
+
+
+def build_lut_quantize_act_static(cb_act, b_a: int, cb_wgt, b_w: int, x, k: int, thr_hi: float,
+                                  thr_lo: float, scale_mode: int = SCALE_ABSMAX, lut=None,
+                                  out: Optional[Dict] = None, stream=None):
+    """build_lut then quantize_act_static (OASIS-S) in one launch; returns (lut, outputs)."""
+    import torch
+    n, d_in = x.shape
+    dev = x.device
+    if lut is None:
+        lut = torch.empty(LUT_BLOCK_BYTES, dtype=torch.uint8, device=dev)
+    if out is None:
+        out = {
+            "idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=dev),
+            "act_scale": torch.empty(n, dtype=torch.float32, device=dev),
+            "max_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "min_idx": torch.empty((n, k), dtype=torch.int32, device=dev),
+            "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
+        }
+    ca = _fp16_bits(cb_act)
+    cw = _fp16_bits(cb_wgt)
+    _check("oasis_build_lut_quantize_act_static", load().oasis_build_lut_quantize_act_static(
+        ca.ctypes.data, b_a, cw.ctypes.data, b_w, _ptr(lut), _ptr(x), n, d_in, k, scale_mode,
+        float(thr_hi), float(thr_lo), _ptr(out["idx_act"]), _ptr(out["act_scale"]),
+        _ptr(out["max_idx"]) if k else None, _ptr(out["min_idx"]) if k else None,
+        _ptr(out["residual"]) if k else None, _stream(stream)))
     return lut, out
 
 

@@ -131,6 +131,20 @@ def test_quantize_static_errors(lib):
     assert f(P, 0, 16, None, 4, 1, 0, 2.0, -2.0, None, None, None, None, None, None) == 0
 
 
+def test_build_lut_quantize_static_errors(lib):
+    f = lib.oasis_build_lut_quantize_act_static
+    ca = _cb(np.linspace(-1, 1, 16))
+    cw = _cb(np.linspace(-1, 1, 16))
+    A, W = ca.ctypes.data, cw.ctypes.data
+    assert f(None, 4, W, 4, P, P, 4, 16, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -1
+    assert f(A, 4, W, 4, P, P, 4, 12, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -2
+    assert f(A, 4, W, 5, P, P, 4, 16, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -3
+    assert f(A, 4, W, 4, P, P, 4, 16, 17, 0, 2.0, -2.0, P, P, P, P, P, None) == -4
+    assert f(A, 4, W, 4, P, P, 4, 16, 1, 0, -2.0, 2.0, P, P, P, P, P, None) == -7   # lo >= hi
+    assert f(A, 4, W, 4, P, P, 4, 16, 1, 3, 2.0, -2.0, P, P, P, P, P, None) == -7
+    assert f(A, 4, W, 4, MIS, P, 4, 16, 1, 0, 2.0, -2.0, P, P, P, P, P, None) == -6
+
+
 def test_cluster_and_detect_errors(lib):
     c = lib.oasis_cluster_act
     assert c(P, 4, 12, P, 4, 0, P, P, None) == -2

@@ -227,6 +227,28 @@ def test_inlier_scale(case):
     check_quant(q_s, ref_s, s.k)
 
 
+@pytest.mark.parametrize("n", [8, 40])   # GEMV and prefill epilogues
+def test_outputs_and_scales_4_byte_aligned(n):
+    """y and w_scale at 4-byte (not 16-byte) aligned addresses, as the
+    boundary allows: the prefill epilogue must not use 16-byte accesses."""
+    L = synth.make_layer(synth.custom(n, 256, 64, 4, seed=51))
+    s = L.spec
+    x, idx_w, _, lut = upload(L)
+    base = torch.zeros(s.d_out + 1, dtype=torch.float32, device=dev())
+    base[1:] = torch.from_numpy(L.s_w).to(dev())
+    s_w = base[1:]
+    ref = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, s.b_a, s.b_w, s.k)
+    q = oasis.quantize_act(x, lut, s.b_a, s.k)
+    ybuf = torch.zeros(s.n * s.d_out + 1, dtype=torch.float32, device=dev())
+    y = ybuf[1:].view(s.n, s.d_out)
+    assert s_w.data_ptr() % 16 != 0 and y.data_ptr() % 16 != 0
+    oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, s.b_a, s.b_w,
+                   oasis.ALGO_MFMA, y=y)
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy(), ref["y_star"], "Y* (4-byte aligned y and scales)")
+    assert ybuf[0].item() == 0.0
+
+
 @pytest.mark.parametrize("k", [6, 40])  # 40: compensation inside the GEMV main loop
 def test_degenerate_tokens(k):
     """Constant tokens, an all-zero token, signed zeros and heavy ties."""
@@ -319,6 +341,14 @@ def test_static_thresholds(name, k, thr):
                                          b_a, b_w, q["max_idx"], q["min_idx"], q["residual"])
     torch.cuda.synchronize()
     assert_close(yr.cpu().numpy(), ref["y"], "Y (static thresholds, fused rows)")
+    # the LUT block built in the same launch: both outputs bit for bit
+    lut2 = torch.full_like(lut, 0xAB)
+    lut2, q2 = oasis.build_lut_quantize_act_static(L.cb_a, b_a, L.cb_w, b_w, x, k, thr[0],
+                                                   thr[1], lut=lut2)
+    torch.cuda.synchronize()
+    assert torch.equal(lut2, lut)
+    for key in q:
+        assert torch.equal(q[key], q2[key]), key
 
 
 def test_empty_batch():
