@@ -495,16 +495,21 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
   auto consume = [&](int u, float rl, const uint32_t (&w)[WR_U]) {
+    // a unit without a live entry (the unused places of OASIS-S lists sit at
+    // the end of each list) adds nothing: skip its products
+    if (__ballot(rl != 0.0f) != 0) {
 #pragma unroll
-    for (int e = 0; e < WR_U; ++e) {
-      const float re = __builtin_bit_cast(float,
-                                          __builtin_amdgcn_readlane(__builtin_bit_cast(int, rl), e));
+      for (int e = 0; e < WR_U; ++e) {
+        const float re = __builtin_bit_cast(
+            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rl), e));
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const uint32_t off = __builtin_amdgcn_perm(w[e], lane8, 0x0C0C0000u | ((4u + b) << 8)) >> 1;
-        const uint32_t pr = *reinterpret_cast<const uint32_t*>(tb + off);
-        acc[2 * b] = fmaf(re, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * b]);
-        acc[2 * b + 1] = fmaf(re, h2f((uint16_t)(pr >> 16)), acc[2 * b + 1]);
+        for (int b = 0; b < 4; ++b) {
+          const uint32_t off =
+              __builtin_amdgcn_perm(w[e], lane8, 0x0C0C0000u | ((4u + b) << 8)) >> 1;
+          const uint32_t pr = *reinterpret_cast<const uint32_t*>(tb + off);
+          acc[2 * b] = fmaf(re, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * b]);
+          acc[2 * b + 1] = fmaf(re, h2f((uint16_t)(pr >> 16)), acc[2 * b + 1]);
+        }
       }
     }
     if (u % nch != nch - 1) return;
