@@ -44,6 +44,10 @@ design notes of the repository):
       (the outliers are compensated exactly, Sec. III-A, III-C); t_i = 0 when
       every channel is listed (the outlier branch then carries the whole
       product).  The lists come first, so this mode has no look-ahead split.
+  R14 Per-output-channel weight codebooks (an extension the paper leaves
+      open, Sec. III-A): column j has its own C_W[j], so each column has its
+      own LUT slice C_A (x) C_W[j], lut_j[(a << n_W) | w] = C_A[a] * C_W[j][w];
+      s_j still scales the column.  A shared codebook is the case of equal rows.
 """
 from __future__ import annotations
 
@@ -353,6 +357,76 @@ def dequant_weights(w_idx: np.ndarray, cb_w: np.ndarray, s_w: np.ndarray) -> np.
     """w_hat[p, j] = s_j * C_W[w_pj] (fp64)."""
     return np.asarray(cb_w, dtype=np.float16).astype(np.float64)[w_idx] * \
         np.asarray(s_w, dtype=np.float64)[None, :]
+
+
+# --------------------------------------------------------------------------
+# R14: per-output-channel weight codebooks
+# --------------------------------------------------------------------------
+def build_lut_percol(cb_a: np.ndarray, cb_w_cols: np.ndarray, b_a: int, b_w: int) -> np.ndarray:
+    """lut[j][(a << b_w) | w] = fp32(C_A[a]) * fp32(C_W[j][w]) for every column j."""
+    ca = np.asarray(cb_a, dtype=np.float16)[: 1 << b_a].astype(np.float32)
+    cw = np.asarray(cb_w_cols, dtype=np.float16)[:, : 1 << b_w].astype(np.float32)
+    out = np.zeros((cw.shape[0], 1 << (b_a + b_w)), dtype=np.float32)
+    for j in range(cw.shape[0]):
+        for a_ in range(1 << b_a):
+            for w in range(1 << b_w):
+                out[j, (a_ << b_w) | w] = ca[a_] * cw[j, w]
+    return out
+
+
+def lut_gemm_percol(a: np.ndarray, w_idx: np.ndarray, lut_cols: np.ndarray, t: np.ndarray,
+                    s_w: np.ndarray, b_w: int, tokens=None) -> np.ndarray:
+    """Y*[i, j] = t_i * s_j * sum_p lut_j[(a_ip << b_w) | w_pj]: every column
+    looks its concatenated indices up in its own LUT slice (fp64 sum)."""
+    rows = range(a.shape[0]) if tokens is None else tokens
+    lut64 = np.asarray(lut_cols, dtype=np.float32).astype(np.float64)
+    w = np.asarray(w_idx, dtype=np.intp)
+    cols = np.arange(w.shape[1])
+    out = np.zeros((len(rows), w.shape[1]), dtype=np.float64)
+    for r, i in enumerate(rows):
+        acc = np.zeros(w.shape[1], dtype=np.float64)
+        for p in range(w.shape[0]):
+            acc += lut64[cols, (int(a[i, p]) << b_w) | w[p]]
+        out[r] = float(t[i]) * np.asarray(s_w, dtype=np.float64) * acc
+    return out
+
+
+def dequant_weights_percol(w_idx: np.ndarray, cb_w_cols: np.ndarray,
+                           s_w: np.ndarray) -> np.ndarray:
+    """w_hat[p, j] = s_j * C_W[j][w_pj] (fp64)."""
+    cw = np.asarray(cb_w_cols, dtype=np.float16).astype(np.float64)
+    w = np.asarray(w_idx, dtype=np.intp)
+    return cw[np.arange(w.shape[1])[None, :], w] * np.asarray(s_w, dtype=np.float64)[None, :]
+
+
+def outlier_compensate_percol(max_idx: np.ndarray, min_idx: np.ndarray, r: np.ndarray,
+                              w_idx: np.ndarray, cb_w_cols: np.ndarray, s_w: np.ndarray,
+                              tokens=None) -> np.ndarray:
+    """Y'[i, j] = sum over listed outliers p of r_ip * s_j * C_W[j][w_pj] (fp64)."""
+    n, k = max_idx.shape
+    rows = range(n) if tokens is None else tokens
+    cw = np.asarray(cb_w_cols, dtype=np.float16).astype(np.float64)
+    s = np.asarray(s_w, dtype=np.float64)
+    cols = np.arange(w_idx.shape[1])
+    out = np.zeros((len(rows), w_idx.shape[1]), dtype=np.float64)
+    for rr, i in enumerate(rows):
+        chans = list(max_idx[i]) + list(min_idx[i])
+        for e, p in enumerate(chans):
+            if r[i, e] != 0:
+                out[rr] += float(r[i, e]) * cw[cols, w_idx[int(p)].astype(np.intp)] * s
+    return out
+
+
+def forward_percol(x, w_idx, cb_w_cols, s_w, cb_a, b_a: int, b_w: int, k: int,
+                   mode: int = SCALE_ABSMAX, tokens=None) -> Dict[str, np.ndarray]:
+    """The whole path with per-column weight codebooks (R14)."""
+    q = quantize_act(x, cb_a, b_a, k, mode)
+    lut = build_lut_percol(cb_a, cb_w_cols, b_a, b_w)
+    ys = lut_gemm_percol(q["a"], w_idx, lut, q["t"], s_w, b_w, tokens=tokens)
+    yc = outlier_compensate_percol(q["max_idx"], q["min_idx"], q["residual"], w_idx,
+                                   cb_w_cols, s_w, tokens=tokens)
+    q.update({"lut": lut, "y_star": ys, "y_comp": yc, "y": ys + yc})
+    return q
 
 
 # --------------------------------------------------------------------------

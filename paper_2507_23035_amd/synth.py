@@ -197,6 +197,19 @@ def make_layer(spec: LayerSpec) -> Layer:
     return Layer(spec, x, w_idx, cb_w, s_w, cb_a, heavy, clipped)
 
 
+def percol_codebooks(layer: Layer) -> np.ndarray:
+    """Per-output-channel weight codebooks (fp16 [d_out][2^b_w]) for the
+    per-column variant: column j's codebook is the shared one scaled by u_j in
+    [0.75, 1.25] and shifted by v_j ~ N(0, 0.02^2), rounded to fp16, from a
+    stream of its own (the layer's other streams are untouched)."""
+    spec = layer.spec
+    rng = np.random.default_rng(np.random.SeedSequence([spec.seed, 0x9E37]))
+    u = rng.uniform(0.75, 1.25, spec.d_out)
+    v = 0.02 * rng.standard_normal(spec.d_out)
+    cb = layer.cb_w.astype(np.float64)[None, :] * u[:, None] + v[:, None]
+    return cb.astype(np.float16)
+
+
 def static_thresholds(layer: Layer, k: int):
     """Offline outlier thresholds for OASIS-S (Sec. V-A): the mean over the
     layer's calibration tokens of the k-th largest and the k-th smallest

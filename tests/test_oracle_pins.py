@@ -236,6 +236,49 @@ def test_duplicate_channels_compensated_once():
     assert np.all(q["residual"][0, :4] != 0)
 
 
+# ---------------------------------------------------------------- per-column codebooks (R14)
+def test_percol_by_hand():
+    """One token, two channels, two columns with their own codebooks; t = 1
+    (mode NONE), C_A = (-1, 1), codes a = (1, 0)."""
+    x = np.array([[1.0, -1.0]], dtype=np.float16)
+    cb_a = np.array([-1.0, 1.0], dtype=np.float16)
+    w_idx = np.array([[0, 1], [1, 0]], dtype=np.uint8)            # [p][j]
+    cols = np.array([[0.5, 2.0], [-1.0, 4.0]], dtype=np.float16)  # C_W[j][w]
+    s_w = np.array([1.0, 0.5], dtype=np.float32)
+    r = O.forward_percol(x, w_idx, cols, s_w, cb_a, 1, 1, 0, mode=O.SCALE_NONE)
+    # y_0 = 1 * (1 * 0.5 + (-1) * 2.0) = -1.5;  y_1 = 0.5 * (1 * 4.0 + (-1) * -1.0) = 2.5
+    assert list(r["y"][0]) == [-1.5, 2.5]
+
+
+def test_percol_equal_rows_is_the_shared_codebook():
+    L = small_layer(n=4, d_in=40, d_out=12, k=3, seed=9)
+    cols = np.tile(L.cb_w, (L.spec.d_out, 1))
+    a = O.forward(L.x, L.w_idx, L.cb_w, L.s_w, L.cb_a, 4, 4, 3)
+    b = O.forward_percol(L.x, L.w_idx, cols, L.s_w, L.cb_a, 4, 4, 3)
+    assert np.array_equal(a["y"], b["y"])
+
+
+def test_percol_lut_gemm_equals_dequant_matmul():
+    L = small_layer(n=5, d_in=48, d_out=11, k=2, seed=10)
+    cols = synth.percol_codebooks(L)
+    q = O.quantize_act(L.x, L.cb_a, 4, 2)
+    lut = O.build_lut_percol(L.cb_a, cols, 4, 4)
+    ys = O.lut_gemm_percol(q["a"], L.w_idx, lut, q["t"], L.s_w, 4)
+    xh = q["t"].astype(np.float64)[:, None] * L.cb_a.astype(np.float64)[q["a"]]
+    ref = xh @ O.dequant_weights_percol(L.w_idx, cols, L.s_w)
+    np.testing.assert_allclose(ys, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_percol_all_channels_listed_recover_exact_gemm():
+    L = small_layer(n=3, d_in=16, d_out=9, k=16, seed=11)
+    cols = synth.percol_codebooks(L)
+    r = O.forward_percol(L.x, L.w_idx, cols, L.s_w, L.cb_a, 4, 4, 16)
+    what = O.dequant_weights_percol(L.w_idx, cols, L.s_w)
+    ref = L.x.astype(np.float64) @ what
+    scale = np.abs(L.x.astype(np.float64)) @ np.abs(what)
+    assert np.all(np.abs(r["y"] - ref) <= 2.0 ** -22 * scale + 1e-12)
+
+
 # ---------------------------------------------------------------- inlier scale (R13)
 def test_inlier_scale_by_hand():
     """k = 1: the max list takes 10, the min list -2; the inliers' absmax is 3.
