@@ -303,6 +303,27 @@ int oasis_lut_gemm_compensated_rows(const uint8_t* idx_act, const float* act_sca
                                     float* y, int accumulate, hipStream_t stream);
 
 /*
+ * oasis_lut_gemm_compensated_percol - oasis_lut_gemm_compensated with an
+ * independent weight codebook per output channel: column j's LUT slice is
+ * C_A x C_W[j] (the Cartesian product of Sec. III-B, built per 16-column
+ * tile in LDS) and the compensation dequantizes with C_W[j] (Sec. III-C2);
+ * s_j still scales column j.  A shared codebook is the case of equal rows
+ * (bit for bit the same y as oasis_lut_gemm_compensated).
+ *   cb_wgt_cols : DEVICE fp16 [d_out][16], 2-byte aligned; entries past
+ *                 2^b_w are read but never selected (any finite value).
+ *   lut         : a LUT block built with the same b_a (its C_A is used).
+ *   n <= 32 (one launch of the GEMV kernel); larger n is TOO_LARGE.
+ * Other arguments, results and errors as oasis_lut_gemm_compensated.
+ */
+int oasis_lut_gemm_compensated_percol(const uint8_t* idx_act, const float* act_scale, int n,
+                                      int d_in, const uint32_t* idx_w, const float* w_scale,
+                                      int d_out, const oasis_lut_block* lut,
+                                      const uint16_t* cb_wgt_cols, int b_a, int b_w,
+                                      const int32_t* max_idx, const int32_t* min_idx,
+                                      const float* residual, int k, float* y, int accumulate,
+                                      hipStream_t stream);
+
+/*
  * oasis_pack_weight_indices - HOST helper: pack w_idx uint8 [d_in][d_out]
  * (codes 0..15, row-major, host memory) into the idx_w layout above
  * (host memory, d_in/8 * d_out words).  Errors: NULL, SHAPE.

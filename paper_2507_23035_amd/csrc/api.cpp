@@ -352,6 +352,35 @@ int oasis_lut_gemm_compensated_rows(const uint8_t* idx_act, const float* act_sca
                           b_w, max_idx, min_idx, residual, k, y, accumulate, stream);
 }
 
+int oasis_lut_gemm_compensated_percol(const uint8_t* idx_act, const float* act_scale, int n,
+                                      int d_in, const uint32_t* idx_w, const float* w_scale,
+                                      int d_out, const oasis_lut_block* lut,
+                                      const uint16_t* cb_wgt_cols, int b_a, int b_w,
+                                      const int32_t* max_idx, const int32_t* min_idx,
+                                      const float* residual, int k, float* y, int accumulate,
+                                      hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (n > oasis::kFusedMaxTokens) return OASIS_ERR_TOO_LARGE;  // the GEMV kernel only
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!act_scale || !w_scale || !lut || !y || !cb_wgt_cols || (d_in > 0 && (!idx_act || !idx_w)))
+    return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
+  if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
+      !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
+      !aligned(min_idx, 4) || !aligned(residual, 4) || !aligned(cb_wgt_cols, 2))
+    return OASIS_ERR_ALIGN;
+  if (!offsets_fit(n, d_in, d_out)) return OASIS_ERR_TOO_LARGE;
+  if (d_in == 0) {  // no channels: Y* = Y' = 0
+    if (accumulate) return OASIS_OK;
+    return launched(oasis::launch_fill_zero(y, (size_t)n * d_out, stream));
+  }
+  oasis::GemmArgs a{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y,
+                    accumulate ? 1 : 0, max_idx, min_idx, residual, k, nullptr, cb_wgt_cols};
+  return launched(oasis::launch_gemm_percol(a, stream));
+}
+
 int oasis_pack_weight_indices(const uint8_t* w_idx, int d_in, int d_out, uint32_t* out) {
   if (!w_idx || !out) return OASIS_ERR_NULL;
   if (d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;

@@ -137,6 +137,9 @@ struct GemmArgs {
   // optional: the codes in the row layout ([d_in][ceil(d_out/8)] words); when
   // set, the compensation reads its rows from here (0.5 B per outlier and column)
   const uint32_t* idx_wr;
+  // optional: per-output-channel weight codebooks, fp16 [d_out][16]; when set
+  // they replace the LUT block's C_W (GEMV kernel only)
+  const uint16_t* cb_cols;
 };
 
 struct CompArgs {
@@ -167,6 +170,8 @@ hipError_t launch_outliers(const QuantArgs& a, hipStream_t s);  // lists + resid
 hipError_t launch_inlier_codes(const QuantArgs& a, hipStream_t s);
 hipError_t launch_gemm_lut(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s);
+// per-output-channel weight codebooks (a.cb_cols), n <= 32
+hipError_t launch_gemm_percol(const GemmArgs& a, hipStream_t s);
 // Y (+)= Y* + Y' in one launch when a.n <= kFusedMaxTokens.
 constexpr int kFusedMaxTokens = 32;
 hipError_t launch_compensate(const CompArgs& a, hipStream_t s);

@@ -67,8 +67,11 @@ struct DualTableLoader {
       ha[q] = __builtin_amdgcn_readfirstlane(a32[2 * wave + q]);
     }
   }
+  // ACT_ONLY: the weight half is written elsewhere (per-column codebooks)
+  template <bool ACT_ONLY = false>
   __device__ __forceinline__ void store(uint32_t* tab, uint32_t wave, int lane) const {
     const bool act = (lane >> 3) & 1;
+    if (ACT_ONLY && !act) return;
     const int lq = lane >> 4;
     auto half = [](uint32_t pair, int h) -> uint32_t { return (pair >> (16 * h)) & 0xFFFFu; };
     // low code of step j: lane / 16 + 4 (j mod 4); high code: 4w + j / 4
@@ -319,13 +322,21 @@ __device__ __forceinline__ void comp_rows(const GemmArgs& A, const GemvAddr& ad,
   }
 }
 
-template <int COLS, int B, bool PRE>
+// PERCOL: the weight half of row `code` holds two copies of each tile
+// column's own pair(C_W[j], code) (position 2 * column + copy), so column jl
+// reads position 2 jl + (slice & 1) there.
+template <int COLS, int B, bool PRE, bool PERCOL = false>
 __device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvAddr& ad, uint32_t col4,
                                                   const char* tab, int nslices, int i, int slice,
                                                   const CompEntries<B>& first,
-                                                  const uint4_t (&first_rows)[B], float (&acc)[4]) {
+                                                  const uint4_t (&first_rows)[B], float (&acc)[4],
+                                                  uint32_t jl0 = 0) {
   const int E = 2 * A.k;
-  const uint32_t l4 = (uint32_t)(threadIdx.x & 31) * 4u;
+  uint32_t l4c[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    l4c[c] = PERCOL ? ((jl0 + (uint32_t)c) * 2u + ((uint32_t)slice & 1u)) * 4u
+                    : (uint32_t)(threadIdx.x & 31) * 4u;
   for (int e0 = slice; e0 < E; e0 += B * nslices) {
     CompEntries<B> ce;
     uint4_t w[B];
@@ -342,7 +353,7 @@ __device__ __forceinline__ void tile_compensation(const GemmArgs& A, const GemvA
       const uint32_t sh = ce.p[b] >= 0 ? 4u * ((uint32_t)ce.p[b] & 7u) : 0u;
       const float r = ce.p[b] >= 0 ? ce.r[b] : 0.0f;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) acc[c] += r * weight_centroid(tab, (w[b][c] >> sh) & 15u, l4);
+      for (int c = 0; c < 4; ++c) acc[c] += r * weight_centroid(tab, (w[b][c] >> sh) & 15u, l4c[c]);
     }
   }
 }
@@ -410,8 +421,9 @@ __device__ __forceinline__ void tile_compensation_wr(const GemmArgs& A,
 // the codebooks, and the entries are checked after the table barrier, behind
 // the weight loads in flight.
 // ----------------------------------------------------------------------------
-template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS>
+template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS, bool PERCOL = false>
 __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
+  static_assert(!PERCOL || (CW == 1 && !ROWS), "per-column codebooks: 16-column tiles, GEMM layout");
   constexpr int NT = NW * 64;
   constexpr int SLOTS = 16 * TF, COLS = 16 * CW;
   constexpr int CG = ROWS ? 8 : 4;  // columns per compensation thread
@@ -451,6 +463,18 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   DualTableLoader dt;
   if (wave < 4) dt.load(lutp, (uint32_t)wave);
   if constexpr (!fused) __builtin_amdgcn_sched_barrier(0);
+  // per-column codebooks: thread t writes position t % 32 (tile column
+  // (t % 32) / 2, copy t % 2) of rows t / 32 + 32 i (i < 8) of the weight half,
+  // i.e. low code (t / 32) % 16 and high codes t / 512 + 2 i of that column
+  static_assert(!PERCOL || NT == 1024, "the per-column table takes 8 entries per thread");
+  uint32_t pc_lo = 0, pc_hi[8];
+  if constexpr (PERCOL) {
+    const int col = min(j0 + (tid & 31) / 2, A.d_out - 1);
+    const uint16_t* cb = A.cb_cols + (size_t)col * 16;
+    pc_lo = cb[(tid >> 5) & 15];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pc_hi[i] = cb[(tid >> 9) + 2 * i];
+  }
   float ts[EPT];   // t_i of this thread's epilogue outputs
   float swj[EPT];  // s_j of the same
 #pragma unroll
@@ -470,9 +494,15 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   BlockCodes<CW, TF> buf[PF];
 #pragma unroll
   for (int d = 0; d < PF; ++d)
-    if (!fused || wave + d * NW < nblk) load_block_buf<CW, TF>(ad, wave + d * NW, buf[d]);
+    if (!fused || PERCOL || wave + d * NW < nblk) load_block_buf<CW, TF>(ad, wave + d * NW, buf[d]);
   if constexpr (!fused) __builtin_amdgcn_sched_barrier(0);
-  if (wave < 4) dt.store(tab, (uint32_t)wave, lane);
+  if (wave < 4) dt.store<PERCOL>(tab, (uint32_t)wave, lane);
+  if constexpr (PERCOL) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      tab[(((uint32_t)tid >> 5) + 32u * (uint32_t)i) * 64u + ((uint32_t)tid & 31u)] =
+          pc_lo | (pc_hi[i] << 16);
+  }
   __syncthreads();  // decode table
 
   float4_t acc[CW][TF];
@@ -484,7 +514,11 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
 #pragma unroll
   for (int f = 0; f < TF; ++f) tok_ok[f] = 16 * f + (lane & 15) < A.n;
   const char* tb = reinterpret_cast<const char*>(tab);
-  const uint32_t l4w = (uint32_t)(lane & 31) * 4u, l4a = l4w + 128u;
+  // weight entries: copy lane mod 32 of the shared codebook, or (per column)
+  // position 2 m + (g mod 2) of lane (g, m)'s column m
+  const uint32_t l4a = (uint32_t)(lane & 31) * 4u + 128u;
+  const uint32_t l4w = PERCOL ? ((uint32_t)(lane & 15) * 2u + ((uint32_t)(lane >> 4) & 1u)) * 4u
+                              : (uint32_t)(lane & 31) * 4u;
   // the preloaded entries' row words, in flight during the main loop
   const uint32_t ccol4 = (uint32_t)(j0 + CG * cquad) * 4u;
   // row layout: word (j0 + 8 cquad) / 8 of each row
@@ -513,7 +547,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
       tile_compensation_wr<BE, PRE>(A, rwr, wr_row, wr_off, tb, NSLICES, ci, cslice, ce0, crw0,
                                    cacc);
     else
-      tile_compensation<COLS, BE, PRE>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0, cacc);
+      tile_compensation<COLS, BE, PRE, PERCOL>(A, ad, ccol4, tb, NSLICES, ci, cslice, ce0, crow0,
+                                               cacc, (uint32_t)(CG * cquad));
   }
   __syncthreads();  // every wave is done with the table: reuse it for the reduction
   float4_t (*red)[CW * TF][64] = reinterpret_cast<float4_t (*)[CW * TF][64]>(tab);
@@ -723,16 +758,37 @@ static void launch_prefill(const GemmArgs& a, hipStream_t s) {
                        dim3(WX * WY * 64), 0, s, a, ncx, nty);
 }
 
-template <int CW, int TF, int NW, int B, bool ROWS>
+template <int CW, int TF, int NW, int B, bool ROWS, bool PERCOL = false>
 static void launch_gemv_b(const GemmArgs& a, hipStream_t s) {
   const int ntiles = (a.d_out + 16 * CW - 1) / (16 * CW);
   constexpr int PF = 2;  // blocks in flight per wave
   if ((a.d_in / 8) % 16 == 0)
-    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true, B, ROWS>), dim3(ntiles),
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true, B, ROWS, PERCOL>), dim3(ntiles),
                        dim3(NW * 64), 0, s, a, ntiles);
   else
-    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false, B, ROWS>), dim3(ntiles),
+    hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, false, B, ROWS, PERCOL>), dim3(ntiles),
                        dim3(NW * 64), 0, s, a, ntiles);
+}
+
+// Per-output-channel codebooks: 16-column tiles, 16 waves, GEMM-layout rows
+// for the fused compensation.
+template <int TF>
+static void launch_gemv_percol(const GemmArgs& a, hipStream_t s) {
+  constexpr int NSLICES = (1024 / (16 * TF)) / 4;
+  if (a.k == 0)
+    launch_gemv_b<1, TF, 16, 0, false, true>(a, s);
+  else if (2 * a.k <= 4 * NSLICES)
+    launch_gemv_b<1, TF, 16, 4, false, true>(a, s);
+  else
+    launch_gemv_b<1, TF, 16, 8, false, true>(a, s);
+}
+
+hipError_t launch_gemm_percol(const GemmArgs& a, hipStream_t s) {
+  if (a.n <= 16)
+    launch_gemv_percol<1>(a, s);
+  else
+    launch_gemv_percol<2>(a, s);
+  return hipGetLastError();
 }
 
 // Outlier entries in flight per compensation thread: about a token's share of

@@ -27,7 +27,7 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_lut_gemm", "oasis_outlier_compensate", "oasis_outlier_compensate_rows",
            "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows",
            "oasis_build_lut_quantize_act", "oasis_quantize_act_static",
-           "oasis_build_lut_quantize_act_static",
+           "oasis_build_lut_quantize_act_static", "oasis_lut_gemm_compensated_percol",
            "oasis_lut_gemm_compensated_rows")
 
 
@@ -78,6 +78,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_lut_gemm_compensated_rows.restype = I
     lib.oasis_lut_gemm_compensated_rows.argtypes = [P, P, I, I, P, P, P, I, P, I, I, P, P, P, I,
                                                     P, I, P]
+    lib.oasis_lut_gemm_compensated_percol.restype = I
+    lib.oasis_lut_gemm_compensated_percol.argtypes = [P, P, I, I, P, P, I, P, P, I, I, P, P, P, I,
+                                                      P, I, P]
     lib.oasis_outlier_compensate_rows.restype = I
     lib.oasis_outlier_compensate_rows.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
     lib.oasis_pack_weight_indices.restype = I
@@ -351,6 +354,25 @@ def lut_gemm_compensated_rows(idx_act, act_scale, idx_w, idx_wr, w_scale, lut, b
         _ptr(w_scale), d_out, _ptr(lut), b_a, b_w, _ptr(max_idx) if k else None,
         _ptr(min_idx) if k else None, _ptr(residual) if k else None, k, _ptr(y),
         1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def lut_gemm_compensated_percol(idx_act, act_scale, idx_w, w_scale, lut, cb_cols, b_a: int,
+                                b_w: int, max_idx, min_idx, residual, y=None,
+                                accumulate: bool = False, stream=None):
+    """lut_gemm_compensated with a weight codebook per output channel
+    (cb_cols: fp16 device tensor [d_out][16]); at most 32 tokens."""
+    import torch
+    n = idx_act.shape[0]
+    d_in = idx_act.shape[1] * 2
+    d_out = idx_w.shape[1]
+    k = max_idx.shape[1]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
+    _check("oasis_lut_gemm_compensated_percol", load().oasis_lut_gemm_compensated_percol(
+        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
+        _ptr(cb_cols), b_a, b_w, _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
+        _ptr(residual) if k else None, k, _ptr(y), 1 if accumulate else 0, _stream(stream)))
     return y
 
 

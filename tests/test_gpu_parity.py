@@ -192,6 +192,58 @@ def test_scale_mode_none():
     run_full(synth.make_layer(spec), scale_mode=oasis.SCALE_NONE)
 
 
+PERCOL = [
+    # name or (n, d_in, d_out, k, seed)
+    "decode_8x4096x4096",
+    "tiny_4x256x256",
+    (17, 520, 100, 8, 61),       # two token tiles, partial last K block, ragged columns
+    (3, 264, 40, 0, 62),         # no outliers
+    (32, 1024, 300, 64, 63),
+]
+
+
+def cols_fp16(L, cols):
+    """[d_out][16] fp16 device tensor (entries past 2^b_w: 0)."""
+    full = np.zeros((L.spec.d_out, 16), dtype=np.float16)
+    full[:, : cols.shape[1]] = cols
+    return torch.from_numpy(full.view(np.int16).copy()).to(dev())
+
+
+@pytest.mark.parametrize("case", PERCOL, ids=str)
+def test_percol_codebooks(case):
+    """Per-output-channel codebooks against the oracle; equal rows give the
+    shared-codebook kernel's y bit for bit."""
+    if isinstance(case, str):
+        L = synth.make_layer(synth.config(case))
+    else:
+        n, d_in, d_out, k, seed = case
+        L = synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed))
+    s = L.spec
+    cols = synth.percol_codebooks(L)
+    x, idx_w, s_w, lut = upload(L)
+    ref = O.forward_percol(L.x, L.w_idx, cols, L.s_w, L.cb_a, s.b_a, s.b_w, s.k)
+    q = oasis.quantize_act(x, lut, s.b_a, s.k)
+    cc = cols_fp16(L, cols)
+    y = oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, cc,
+                                          s.b_a, s.b_w, q["max_idx"], q["min_idx"], q["residual"])
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy(), ref["y"], "Y (per-column codebooks)")
+    y.fill_(0.5)
+    oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, cc, s.b_a,
+                                      s.b_w, q["max_idx"], q["min_idx"], q["residual"], y=y,
+                                      accumulate=True)
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy() - 0.5, ref["y"], "Y (per-column codebooks, accumulate)")
+    same = cols_fp16(L, np.tile(L.cb_w, (s.d_out, 1)))
+    y1 = oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, same,
+                                           s.b_a, s.b_w, q["max_idx"], q["min_idx"],
+                                           q["residual"])
+    y2 = oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w, s_w, lut, s.b_a, s.b_w,
+                                    q["max_idx"], q["min_idx"], q["residual"])
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2), "equal rows differ from the shared codebook"
+
+
 INLIER = [
     # name or (n, d_in, d_out, k, seed)
     "decode_8x4096x4096",
