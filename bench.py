@@ -77,6 +77,8 @@ def call_bytes(n, d_in, d_out, k, path):
         # the row-layout copy of a listed channel, where the launch reads it,
         # duplicates codes the operation needs once: not counted
         "lut_gemm_compensated_rows": gemm_bytes(n, d_in, d_out, k, merge=False),
+        # + the columns' own codebooks (16 fp16 each)
+        "lut_gemm_compensated_percol": gemm_bytes(n, d_in, d_out, k, merge=False) + 32 * d_out,
     }
 
 
@@ -89,6 +91,7 @@ KERNEL_SOURCES = {
     "outlier_compensate": ["compensate.hip"],
     "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
     "lut_gemm_compensated_rows": ["lut_gemm.hip", "compensate.hip"],
+    "lut_gemm_compensated_percol": ["lut_gemm.hip"],
 }
 
 
@@ -122,6 +125,7 @@ CALL_SYMBOLS = {   # kernel symbol fragment of each call's dominant kernel
     "detect_outliers": "k_quantize<", "outlier_compensate": "k_compensate",
     "lut_gemm": "k_gemm_mfma", "lut_gemm_compensated": "k_gemm_mfma",
     "lut_gemm_compensated_rows": "k_gemm_mfma",
+    "lut_gemm_compensated_percol": "k_gemm_mfma",
 }
 
 
@@ -193,14 +197,18 @@ def calibrate_copy(mib):
                       "bytes_written_per_copy": nbytes, "copies": 10}), flush=True)
 
 
-def cpu_baseline(layer, budget_s=12.0, mode=0):
+def cpu_baseline(layer, budget_s=12.0, mode=0, cols=None):
     """Time the oracle's whole-layer forward on the host (single-threaded numpy)."""
     from oracle import oasis_oracle as O
     s = layer.spec
     reps, t0 = 0, time.perf_counter()
     while True:
-        O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w, s.k,
-                  mode=mode)
+        if cols is None:
+            O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w, s.k,
+                      mode=mode)
+        else:
+            O.forward_percol(layer.x, layer.w_idx, cols, layer.s_w, layer.cb_a, s.b_a, s.b_w,
+                             s.k, mode=mode)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 50:
@@ -227,6 +235,9 @@ def main():
     ap.add_argument("--scale", default="absmax", choices=["absmax", "inlier"],
                     help="per-token scale: absmax of all channels, or of the channels in "
                          "neither outlier list (a second quantize launch; no look-ahead)")
+    ap.add_argument("--percol", action="store_true",
+                    help="an independent weight codebook per output channel (fused path, "
+                         "<= 32 tokens)")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
     ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate", "lookahead"],
@@ -269,6 +280,11 @@ def main():
                   file=sys.stderr)
             sys.exit(2)
         spec = dataclasses.replace(spec, name=f"{spec.name}_inlier")
+    if args.percol:
+        if args.path not in ("auto", "fused") or spec.n > 32:
+            print("bench.py: --percol runs the fused GEMV (<= 32 tokens)", file=sys.stderr)
+            sys.exit(2)
+        spec = dataclasses.replace(spec, name=f"{spec.name}_percol")
     if args.oasis_s:
         if args.path == "lookahead":
             print("bench.py: --oasis-s has no look-ahead schedule (no top-k to overlap)",
@@ -308,6 +324,13 @@ def main():
     # = d_out/2 contiguous bytes); the main branch streams idx_w
     rows = oasis.pack_weight_rows(layer.w_idx).view(np.int32)
     idx_wr = [torch.from_numpy(rows).to(dev) for _ in range(copies)]
+    # per-column codebooks (--percol): fp16 [d_out][16], entries past 2^b_w zero
+    cols_np, cols_dev = None, None
+    if args.percol:
+        cols_np = synth.percol_codebooks(layer)
+        full = np.zeros((d_out, 16), dtype=np.float16)
+        full[:, : cols_np.shape[1]] = cols_np
+        cols_dev = torch.from_numpy(full.view(np.int16).copy()).to(dev)
 
     # Every call of the path, with the arguments the step uses (c = weight copy).
     calls = {
@@ -332,11 +355,24 @@ def main():
         "lut_gemm_compensated_rows": lambda c: oasis.lut_gemm_compensated_rows(
             q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c], s_w, lut, b_a, b_w, q["max_idx"],
             q["min_idx"], q["residual"], y=y),
+        "lut_gemm_compensated_percol": lambda c: oasis.lut_gemm_compensated_percol(
+            q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, cols_dev, b_a, b_w, q["max_idx"],
+            q["min_idx"], q["residual"], y=y),
     }
+
+    def fused_gemm(c, L, qq, yy=None):
+        """The fused path's GEMM + compensation call."""
+        if args.percol:
+            return oasis.lut_gemm_compensated_percol(qq["idx_act"], qq["act_scale"], idx_w[c], s_w,
+                                                     L, cols_dev, b_a, b_w, qq["max_idx"],
+                                                     qq["min_idx"], qq["residual"], y=yy)
+        return oasis.lut_gemm_compensated_rows(qq["idx_act"], qq["act_scale"], idx_w[c],
+                                               idx_wr[c], s_w, L, b_a, b_w, qq["max_idx"],
+                                               qq["min_idx"], qq["residual"], y=yy)
     if path == "fused":
+        gemm_name = "lut_gemm_compensated_percol" if args.percol else "lut_gemm_compensated_rows"
         names = (["build_lut_quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
-            ["lut_gemm_compensated_rows"]
-        gemm_name = "lut_gemm_compensated_rows"
+            [gemm_name]
     elif path == "lookahead":
         names = ["build_lut", "cluster_act", "detect_outliers", "lut_gemm", "outlier_compensate"]
         gemm_name = "lut_gemm"
@@ -362,9 +398,7 @@ def main():
             # the LUT block is rebuilt with every step (Sec. IV-A builds it once
             # per layer), inside the quantize launch
             quantize(L)
-            oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c],
-                                            s_w, L, b_a, b_w, q["max_idx"], q["min_idx"],
-                                            q["residual"], y=y)
+            fused_gemm(c, L, q, y)
         elif path == "lookahead":
             oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
             # main branch and outlier detection run concurrently (Sec. III-C)
@@ -438,9 +472,7 @@ def main():
     q1 = oasis.quantize_act(x, lut, b_a, k, scale) if not thr else \
         oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1], scale)
     if path == "fused":
-        y_ref = oasis.lut_gemm_compensated_rows(q1["idx_act"], q1["act_scale"], idx_w[c_last],
-                                                idx_wr[c_last], s_w, lut, b_a, b_w,
-                                                q1["max_idx"], q1["min_idx"], q1["residual"])
+        y_ref = fused_gemm(c_last, lut, q1)
     else:
         if path == "lookahead":
             y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a,
@@ -520,7 +552,7 @@ def main():
         "config": {"workload": s.name, "n": n, "d_in": d_in, "d_out": d_out, "k_per_side": k,
                    "b_a": b_a, "b_w": b_w, "algo": args.algo, "launch": mode,
                    "path": path, "outliers": "static" if thr else "top-k",
-                   "scale": args.scale,
+                   "scale": args.scale, "weight_codebooks": "per-column" if args.percol else "shared",
                    "weight_copies": copies},
         "schedule_check": schedule_ok,
         "step_hbm_gbs": round(step_bytes(n, d_in, d_out, k, fused) / (ms_per_step * 1e-3) / 1e9, 1),
@@ -529,7 +561,7 @@ def main():
         "roofline_main_branch": main_branch,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layer, mode=scale)
+        out["cpu_baseline"] = cpu_baseline(layer, mode=scale, cols=cols_np)
     print(json.dumps(out), flush=True)
 
 
