@@ -236,8 +236,8 @@ def main():
                     help="per-token scale: absmax of all channels, or of the channels in "
                          "neither outlier list (a second quantize launch; no look-ahead)")
     ap.add_argument("--percol", action="store_true",
-                    help="an independent weight codebook per output channel (fused path, "
-                         "<= 32 tokens)")
+                    help="an independent weight codebook per output channel (fused GEMV, "
+                         "one launch per 32 tokens)")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
     ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate", "lookahead"],
@@ -281,8 +281,9 @@ def main():
             sys.exit(2)
         spec = dataclasses.replace(spec, name=f"{spec.name}_inlier")
     if args.percol:
-        if args.path not in ("auto", "fused") or spec.n > 32:
-            print("bench.py: --percol runs the fused GEMV (<= 32 tokens)", file=sys.stderr)
+        if args.path not in ("auto", "fused") or args.algo != "mfma":
+            print("bench.py: --percol runs the fused MFMA GEMV (32 tokens per launch)",
+                  file=sys.stderr)
             sys.exit(2)
         spec = dataclasses.replace(spec, name=f"{spec.name}_percol")
     if args.oasis_s:
@@ -318,7 +319,7 @@ def main():
     y = torch.empty((n, d_out), dtype=torch.float32, device=dev)
     path = args.path
     if path == "auto":
-        path = "fused" if (n <= 32 and algo == oasis.ALGO_MFMA) else "separate"
+        path = "fused" if ((n <= 32 or args.percol) and algo == oasis.ALGO_MFMA) else "separate"
     side = torch.cuda.Stream()
     # the outlier branch reads the codes in the row layout (one input channel
     # = d_out/2 contiguous bytes); the main branch streams idx_w
@@ -519,7 +520,8 @@ def main():
 
     def roof(nm):
         us = kern_us[nm]
-        if nm in ("lut_gemm", "lut_gemm_compensated", "lut_gemm_compensated_rows") and n > 32:
+        if nm in ("lut_gemm", "lut_gemm_compensated", "lut_gemm_compensated_rows",
+                  "lut_gemm_compensated_percol") and n > 32:
             tflops = ops / (us * 1e-6) / 1e12
             r = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
                  "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),

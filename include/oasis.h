@@ -312,7 +312,9 @@ int oasis_lut_gemm_compensated_rows(const uint8_t* idx_act, const float* act_sca
  *   cb_wgt_cols : DEVICE fp16 [d_out][16], 2-byte aligned; entries past
  *                 2^b_w are read but never selected (any finite value).
  *   lut         : a LUT block built with the same b_a (its C_A is used).
- *   n <= 32 (one launch of the GEMV kernel); larger n is TOO_LARGE.
+ *   Any n: one launch of the GEMV kernel per 32 tokens (each launch
+ *   re-reads idx_w, so large n is slower per token than the shared-codebook
+ *   prefill kernel).
  * Other arguments, results and errors as oasis_lut_gemm_compensated.
  */
 int oasis_lut_gemm_compensated_percol(const uint8_t* idx_act, const float* act_scale, int n,

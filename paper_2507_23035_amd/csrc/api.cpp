@@ -362,7 +362,6 @@ int oasis_lut_gemm_compensated_percol(const uint8_t* idx_act, const float* act_s
   if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
   if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
   if (k < 0 || k > d_in) return OASIS_ERR_K;
-  if (n > oasis::kFusedMaxTokens) return OASIS_ERR_TOO_LARGE;  // the GEMV kernel only
   if (n == 0 || d_out == 0) return OASIS_OK;
   if (!act_scale || !w_scale || !lut || !y || !cb_wgt_cols || (d_in > 0 && (!idx_act || !idx_w)))
     return OASIS_ERR_NULL;

@@ -783,12 +783,30 @@ static void launch_gemv_percol(const GemmArgs& a, hipStream_t s) {
     launch_gemv_b<1, TF, 16, 8, false, true>(a, s);
 }
 
+// More than 32 tokens: one GEMV launch per 32-token chunk (token-major
+// arguments offset to the chunk); every chunk re-reads the weight codes, from
+// the last-level cache when they fit there.
 hipError_t launch_gemm_percol(const GemmArgs& a, hipStream_t s) {
-  if (a.n <= 16)
-    launch_gemv_percol<1>(a, s);
-  else
-    launch_gemv_percol<2>(a, s);
-  return hipGetLastError();
+  constexpr int CHUNK = 32;
+  for (int t0 = 0; t0 < a.n; t0 += CHUNK) {
+    GemmArgs c = a;
+    c.n = min(CHUNK, a.n - t0);
+    c.idx_act = a.idx_act + (size_t)t0 * (size_t)(a.d_in / 2);
+    c.act_scale = a.act_scale + t0;
+    c.y = a.y + (size_t)t0 * (size_t)a.d_out;
+    if (a.k > 0) {
+      c.max_idx = a.max_idx + (size_t)t0 * a.k;
+      c.min_idx = a.min_idx + (size_t)t0 * a.k;
+      c.residual = a.residual + (size_t)t0 * 2 * a.k;
+    }
+    if (c.n <= 16)
+      launch_gemv_percol<1>(c, s);
+    else
+      launch_gemv_percol<2>(c, s);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Outlier entries in flight per compensation thread: about a token's share of

@@ -361,7 +361,7 @@ def lut_gemm_compensated_percol(idx_act, act_scale, idx_w, w_scale, lut, cb_cols
                                 b_w: int, max_idx, min_idx, residual, y=None,
                                 accumulate: bool = False, stream=None):
     """lut_gemm_compensated with a weight codebook per output channel
-    (cb_cols: fp16 device tensor [d_out][16]); at most 32 tokens."""
+    (cb_cols: fp16 device tensor [d_out][16]); one GEMV launch per 32 tokens."""
     import torch
     n = idx_act.shape[0]
     d_in = idx_act.shape[1] * 2

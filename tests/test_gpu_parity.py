@@ -199,6 +199,10 @@ PERCOL = [
     (17, 520, 100, 8, 61),       # two token tiles, partial last K block, ragged columns
     (3, 264, 40, 0, 62),         # no outliers
     (32, 1024, 300, 64, 63),
+    (70, 520, 100, 8, 64),       # three 32-token launches, the last one of 6 tokens
+    (49, 264, 48, 2, 65),        # a 17-token second launch (two token tiles)
+    "large_decode_16x8192x28672",
+    "prefill_up_2048x4096x11008",  # 64 launches; sampled rows
 ]
 
 
@@ -219,29 +223,45 @@ def test_percol_codebooks(case):
         n, d_in, d_out, k, seed = case
         L = synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed))
     s = L.spec
+    print(f"case percol {s.name} n={s.n} d_in={s.d_in} d_out={s.d_out} k={s.k}", flush=True)
     cols = synth.percol_codebooks(L)
     x, idx_w, s_w, lut = upload(L)
-    ref = O.forward_percol(L.x, L.w_idx, cols, L.s_w, L.cb_a, s.b_a, s.b_w, s.k)
+    small = s.n * s.d_in * s.d_out <= 1 << 28
+    tokens = None if small else sorted({t for t in (0, 5, 31, 32, 1000, s.n - 1) if t < s.n})
+    rows = slice(None) if tokens is None else tokens
+    ref = O.forward_percol(L.x, L.w_idx, cols, L.s_w, L.cb_a, s.b_a, s.b_w, s.k, tokens=tokens)
     q = oasis.quantize_act(x, lut, s.b_a, s.k)
     cc = cols_fp16(L, cols)
     y = oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, cc,
                                           s.b_a, s.b_w, q["max_idx"], q["min_idx"], q["residual"])
     torch.cuda.synchronize()
-    assert_close(y.cpu().numpy(), ref["y"], "Y (per-column codebooks)")
+    assert_close(y.cpu().numpy()[rows], ref["y"], "Y (per-column codebooks)")
     y.fill_(0.5)
     oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, cc, s.b_a,
                                       s.b_w, q["max_idx"], q["min_idx"], q["residual"], y=y,
                                       accumulate=True)
     torch.cuda.synchronize()
-    assert_close(y.cpu().numpy() - 0.5, ref["y"], "Y (per-column codebooks, accumulate)")
+    assert_close(y.cpu().numpy()[rows] - 0.5, ref["y"], "Y (per-column codebooks, accumulate)")
+    # equal rows: the shared-codebook GEMV on the same 32-token launches; bit for
+    # bit while it also runs 16-column tiles (fewer than 256 tiles of 32
+    # columns), else its wider tiles split the compensation into other partial
+    # sums and only the tolerance holds
+    exact = (s.d_out + 31) // 32 < 256
     same = cols_fp16(L, np.tile(L.cb_w, (s.d_out, 1)))
     y1 = oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, same,
                                            s.b_a, s.b_w, q["max_idx"], q["min_idx"],
                                            q["residual"])
-    y2 = oasis.lut_gemm_compensated(q["idx_act"], q["act_scale"], idx_w, s_w, lut, s.b_a, s.b_w,
-                                    q["max_idx"], q["min_idx"], q["residual"])
-    torch.cuda.synchronize()
-    assert torch.equal(y1, y2), "equal rows differ from the shared codebook"
+    for t0 in range(0, min(s.n, 96), 32):
+        t = slice(t0, min(t0 + 32, s.n))
+        y2 = oasis.lut_gemm_compensated(q["idx_act"][t], q["act_scale"][t], idx_w, s_w, lut,
+                                        s.b_a, s.b_w, q["max_idx"][t], q["min_idx"][t],
+                                        q["residual"][t])
+        torch.cuda.synchronize()
+        if exact:
+            assert torch.equal(y1[t], y2), f"equal rows differ from the shared codebook, tokens {t}"
+        else:
+            assert_close(y1[t].cpu().numpy(), y2.cpu().numpy().astype(np.float64),
+                         f"equal rows vs the shared codebook, tokens {t}")
 
 
 INLIER = [
