@@ -198,21 +198,24 @@ def calibrate_copy(mib):
 
 
 def cpu_baseline(layer, budget_s=12.0, mode=0, cols=None):
-    """Time the oracle's whole-layer forward on the host (single-threaded numpy)."""
+    """Time the oracle's whole-layer forward on the host, on one thread (any
+    BLAS or OpenMP pool numpy reaches is limited to one thread meanwhile)."""
+    from threadpoolctl import threadpool_limits
     from oracle import oasis_oracle as O
     s = layer.spec
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        if cols is None:
-            O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w, s.k,
-                      mode=mode)
-        else:
-            O.forward_percol(layer.x, layer.w_idx, cols, layer.s_w, layer.cb_a, s.b_a, s.b_w,
-                             s.k, mode=mode)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 50:
-            break
+    with threadpool_limits(limits=1):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            if cols is None:
+                O.forward(layer.x, layer.w_idx, layer.cb_w, layer.s_w, layer.cb_a, s.b_a, s.b_w,
+                          s.k, mode=mode)
+            else:
+                O.forward_percol(layer.x, layer.w_idx, cols, layer.s_w, layer.cb_a, s.b_a,
+                                 s.b_w, s.k, mode=mode)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 50:
+                break
     per = el / reps
     return {"value": 2.0 * s.n * s.d_in * s.d_out / per / 1e12,
             "unit": "effective TOPS", "cores": 1, "kind": "oracle",
