@@ -309,7 +309,7 @@ int oasis_lut_gemm_compensated_rows(const uint8_t* idx_act, const float* act_sca
  * tile in LDS) and the compensation dequantizes with C_W[j] (Sec. III-C2);
  * s_j still scales column j.  A shared codebook is the case of equal rows
  * (bit for bit the same y as oasis_lut_gemm_compensated).
- *   cb_wgt_cols : DEVICE fp16 [d_out][16], 2-byte aligned; entries past
+ *   cb_wgt_cols : DEVICE fp16 [d_out][16], 16-byte aligned; entries past
  *                 2^b_w are read but never selected (any finite value).
  *   lut         : a LUT block built with the same b_a (its C_A is used).
  *   Any n: one launch of the GEMV kernel per 32 tokens (each launch

@@ -368,7 +368,7 @@ int oasis_lut_gemm_compensated_percol(const uint8_t* idx_act, const float* act_s
   if (k > 0 && (!max_idx || !min_idx || !residual)) return OASIS_ERR_NULL;
   if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
       !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
-      !aligned(min_idx, 4) || !aligned(residual, 4) || !aligned(cb_wgt_cols, 2))
+      !aligned(min_idx, 4) || !aligned(residual, 4) || !aligned(cb_wgt_cols, 16))
     return OASIS_ERR_ALIGN;
   if (!offsets_fit(n, d_in, d_out)) return OASIS_ERR_TOO_LARGE;
   if (d_in == 0) {  // no channels: Y* = Y' = 0

@@ -467,13 +467,21 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   // (t % 32) / 2, copy t % 2) of rows t / 32 + 32 i (i < 8) of the weight half,
   // i.e. low code (t / 32) % 16 and high codes t / 512 + 2 i of that column
   static_assert(!PERCOL || NT == 1024, "the per-column table takes 8 entries per thread");
+  // (the column's 32-byte codebook in two 16-byte loads; t / 512 is
+  // wave-uniform, so the high codes are one half of every word)
   uint32_t pc_lo = 0, pc_hi[8];
   if constexpr (PERCOL) {
     const int col = min(j0 + (tid & 31) / 2, A.d_out - 1);
-    const uint16_t* cb = A.cb_cols + (size_t)col * 16;
-    pc_lo = cb[(tid >> 5) & 15];
+    const uint4_t* cb = reinterpret_cast<const uint4_t*>(A.cb_cols + (size_t)col * 16);
+    const uint4_t c0 = cb[0], c1 = cb[1];
+    const uint32_t cw[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+    const uint32_t e = ((uint32_t)tid >> 5) & 15u, hs = 16u * ((uint32_t)tid >> 9);
+    uint32_t d = 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) pc_hi[i] = cb[(tid >> 9) + 2 * i];
+    for (int q = 0; q < 8; ++q) d = (e >> 1) == (uint32_t)q ? cw[q] : d;
+    pc_lo = (d >> (16u * (e & 1u))) & 0xFFFFu;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pc_hi[i] = (cw[i] >> hs) & 0xFFFFu;
   }
   float ts[EPT];   // t_i of this thread's epilogue outputs
   float swj[EPT];  // s_j of the same

@@ -228,6 +228,7 @@ def test_percol_errors(lib):
     assert g(P, P, 4, 12, P, P, 8, P, P, 4, 4, P, P, P, 2, P, 0, None) == -2
     assert g(P, P, 4, 16, P, P, 8, P, None, 4, 4, P, P, P, 2, P, 0, None) == -1
     assert g(P, P, 4, 16, P, P, 8, P, P + 1, 4, 4, P, P, P, 2, P, 0, None) == -6
+    assert g(P, P, 4, 16, P, P, 8, P, P + 2, 4, 4, P, P, P, 2, P, 0, None) == -6  # 16 B
     assert g(P, P, 33, 16, P, P, 8, P, P, 4, 4, P, P, P, 17, P, 0, None) == -4  # any n
     assert g(P, P, 4, 16, P, P, 8, P, P, 4, 4, P, P, P, 17, P, 0, None) == -4
 
