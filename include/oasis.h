@@ -239,7 +239,8 @@ int oasis_lut_gemm(const uint8_t* idx_act, const float* act_scale, int n, int d_
  *   accumulate == 0 : y  = Y'.
  *   Channel ids must lie in [0, d_in) (ids from oasis_quantize_act do).
  *   k == 0 with accumulate != 0 is a no-op; with accumulate == 0 it zeroes y.
- * Errors: NULL, SHAPE, BITS, K, ALIGN, LAUNCH.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, TOO_LARGE (d_in/8 * d_out * 4 >= 2^31:
+ * the codes must be < 2 GiB), LAUNCH.
  */
 int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, const float* residual,
                              int n, int k, const uint32_t* idx_w, const oasis_lut_block* lut,

@@ -125,15 +125,6 @@ def cluster(x: np.ndarray, t: np.ndarray, cb_a: np.ndarray, b_a: int) -> np.ndar
     return out
 
 
-def nearest_centroid(x: np.ndarray, t: np.ndarray, cb_a: np.ndarray, b_a: int) -> np.ndarray:
-    """Eq. (1) written literally: argmin over centroids of the squared distance."""
-    x64 = np.asarray(x, dtype=np.float16).astype(np.float64)
-    cents = np.asarray(t, dtype=np.float64)[:, None, None] * \
-        np.asarray(cb_a, dtype=np.float16)[: 1 << b_a].astype(np.float64)[None, None, :]
-    d = (x64[:, :, None] - cents) ** 2
-    return np.argmin(d, axis=2).astype(np.uint8)
-
-
 # --------------------------------------------------------------------------
 # Sec. IV-D: dynamic top-k outlier detection (k largest and k smallest)
 # --------------------------------------------------------------------------
@@ -351,12 +342,6 @@ def dequant_matmul(a: np.ndarray, w_idx: np.ndarray, cb_a: np.ndarray, cb_w: np.
     wh = np.asarray(cb_w, dtype=np.float16).astype(np.float64)[w_idx] * \
         np.asarray(s_w, dtype=np.float64)[None, :]
     return xh @ wh
-
-
-def dequant_weights(w_idx: np.ndarray, cb_w: np.ndarray, s_w: np.ndarray) -> np.ndarray:
-    """w_hat[p, j] = s_j * C_W[w_pj] (fp64)."""
-    return np.asarray(cb_w, dtype=np.float16).astype(np.float64)[w_idx] * \
-        np.asarray(s_w, dtype=np.float64)[None, :]
 
 
 # --------------------------------------------------------------------------

@@ -265,6 +265,9 @@ int oasis_outlier_compensate(const int32_t* max_idx, const int32_t* min_idx, con
   if (!aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4) ||
       !aligned(idx_w, 4) || !aligned(lut, 16) || !aligned(w_scale, 4) || !aligned(y, 4))
     return OASIS_ERR_ALIGN;
+  // the row-grouped kernel (many tokens) addresses the codes with 32-bit
+  // buffer offsets
+  if ((uint64_t)(d_in / 8) * (uint64_t)d_out * 4u >= (1ull << 31)) return OASIS_ERR_TOO_LARGE;
   oasis::CompArgs a{max_idx, min_idx, residual, n, k, idx_w, lut, b_w, w_scale, d_in, d_out, y,
                     accumulate ? 1 : 0};
   return launched(oasis::launch_compensate(a, stream));

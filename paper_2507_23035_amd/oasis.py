@@ -96,9 +96,28 @@ def _check(fn: str, status: int) -> None:
         raise OasisError(fn, status, load().oasis_status_str(status).decode())
 
 
-def _ptr(t) -> Optional[int]:
+# element kinds of the tensors the calls take: fp16 values travel as their
+# bit patterns, so float16 and int16 tensors both qualify
+_KINDS = {
+    "u8": ("uint8", "int8"),
+    "f16": ("float16", "int16", "uint16"),
+    "i32": ("int32", "uint32"),
+    "f32": ("float32",),
+}
+
+
+def _ptr(t, kind: Optional[str] = None) -> Optional[int]:
+    """Device address of a tensor the library reads or writes as packed
+    row-major memory: it must be a contiguous CUDA tensor of the right element
+    kind (a strided view would be read as if it were packed)."""
     if t is None:
         return None
+    if not t.is_cuda:
+        raise ValueError(f"expected a CUDA tensor, got one on {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"expected a contiguous tensor, got strides {tuple(t.stride())}")
+    if kind is not None and str(t.dtype).split(".")[-1] not in _KINDS[kind]:
+        raise ValueError(f"expected a {'/'.join(_KINDS[kind])} tensor, got {t.dtype}")
     return t.data_ptr()
 
 
@@ -142,7 +161,7 @@ def build_lut(cb_act, b_a: int, cb_wgt, b_w: int, out=None, stream=None):
     ca = _fp16_bits(cb_act)
     cw = _fp16_bits(cb_wgt)
     _check("oasis_build_lut", load().oasis_build_lut(ca.ctypes.data, b_a, cw.ctypes.data, b_w,
-                                                     _ptr(out), _stream(stream)))
+                                                     _ptr(out, "u8"), _stream(stream)))
     return out
 
 
@@ -161,9 +180,9 @@ def quantize_act(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
             "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
         }
     _check("oasis_quantize_act", load().oasis_quantize_act(
-        _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode, _ptr(out["idx_act"]),
-        _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
-        _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
+        _ptr(x, "f16"), n, d_in, _ptr(lut, "u8"), b_a, k, scale_mode, _ptr(out["idx_act"], "u8"),
+        _ptr(out["act_scale"], "f32"), _ptr(out["max_idx"], "i32") if k else None,
+        _ptr(out["min_idx"], "i32") if k else None, _ptr(out["residual"], "f32") if k else None,
         _stream(stream)))
     return out
 
@@ -185,9 +204,9 @@ def quantize_act_static(x, lut, b_a: int, k: int, thr_hi: float, thr_lo: float,
             "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
         }
     _check("oasis_quantize_act_static", load().oasis_quantize_act_static(
-        _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode, float(thr_hi), float(thr_lo),
-        _ptr(out["idx_act"]), _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
-        _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
+        _ptr(x, "f16"), n, d_in, _ptr(lut, "u8"), b_a, k, scale_mode, float(thr_hi), float(thr_lo),
+        _ptr(out["idx_act"], "u8"), _ptr(out["act_scale"], "f32"), _ptr(out["max_idx"], "i32") if k else None,
+        _ptr(out["min_idx"], "i32") if k else None, _ptr(out["residual"], "f32") if k else None,
         _stream(stream)))
     return out
 
@@ -212,9 +231,9 @@ def build_lut_quantize_act(cb_act, b_a: int, cb_wgt, b_w: int, x, k: int,
     ca = _fp16_bits(cb_act)
     cw = _fp16_bits(cb_wgt)
     _check("oasis_build_lut_quantize_act", load().oasis_build_lut_quantize_act(
-        ca.ctypes.data, b_a, cw.ctypes.data, b_w, _ptr(lut), _ptr(x), n, d_in, k, scale_mode,
-        _ptr(out["idx_act"]), _ptr(out["act_scale"]), _ptr(out["max_idx"]) if k else None,
-        _ptr(out["min_idx"]) if k else None, _ptr(out["residual"]) if k else None,
+        ca.ctypes.data, b_a, cw.ctypes.data, b_w, _ptr(lut, "u8"), _ptr(x, "f16"), n, d_in, k, scale_mode,
+        _ptr(out["idx_act"], "u8"), _ptr(out["act_scale"], "f32"), _ptr(out["max_idx"], "i32") if k else None,
+        _ptr(out["min_idx"], "i32") if k else None, _ptr(out["residual"], "f32") if k else None,
         _stream(stream)))
     return lut, out
 
@@ -239,10 +258,10 @@ def build_lut_quantize_act_static(cb_act, b_a: int, cb_wgt, b_w: int, x, k: int,
     ca = _fp16_bits(cb_act)
     cw = _fp16_bits(cb_wgt)
     _check("oasis_build_lut_quantize_act_static", load().oasis_build_lut_quantize_act_static(
-        ca.ctypes.data, b_a, cw.ctypes.data, b_w, _ptr(lut), _ptr(x), n, d_in, k, scale_mode,
-        float(thr_hi), float(thr_lo), _ptr(out["idx_act"]), _ptr(out["act_scale"]),
-        _ptr(out["max_idx"]) if k else None, _ptr(out["min_idx"]) if k else None,
-        _ptr(out["residual"]) if k else None, _stream(stream)))
+        ca.ctypes.data, b_a, cw.ctypes.data, b_w, _ptr(lut, "u8"), _ptr(x, "f16"), n, d_in, k, scale_mode,
+        float(thr_hi), float(thr_lo), _ptr(out["idx_act"], "u8"), _ptr(out["act_scale"], "f32"),
+        _ptr(out["max_idx"], "i32") if k else None, _ptr(out["min_idx"], "i32") if k else None,
+        _ptr(out["residual"], "f32") if k else None, _stream(stream)))
     return lut, out
 
 
@@ -255,8 +274,8 @@ def cluster_act(x, lut, b_a: int, scale_mode: int = SCALE_ABSMAX, out: Optional[
         out = {"idx_act": torch.empty((n, d_in // 2), dtype=torch.uint8, device=x.device),
                "act_scale": torch.empty(n, dtype=torch.float32, device=x.device)}
     _check("oasis_cluster_act", load().oasis_cluster_act(
-        _ptr(x), n, d_in, _ptr(lut), b_a, scale_mode, _ptr(out["idx_act"]),
-        _ptr(out["act_scale"]), _stream(stream)))
+        _ptr(x, "f16"), n, d_in, _ptr(lut, "u8"), b_a, scale_mode, _ptr(out["idx_act"], "u8"),
+        _ptr(out["act_scale"], "f32"), _stream(stream)))
     return out
 
 
@@ -270,9 +289,9 @@ def detect_outliers(x, lut, b_a: int, k: int, scale_mode: int = SCALE_ABSMAX,
                "min_idx": torch.empty((n, k), dtype=torch.int32, device=x.device),
                "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=x.device)}
     _check("oasis_detect_outliers", load().oasis_detect_outliers(
-        _ptr(x), n, d_in, _ptr(lut), b_a, k, scale_mode,
-        _ptr(out["max_idx"]) if k else None, _ptr(out["min_idx"]) if k else None,
-        _ptr(out["residual"]) if k else None, _stream(stream)))
+        _ptr(x, "f16"), n, d_in, _ptr(lut, "u8"), b_a, k, scale_mode,
+        _ptr(out["max_idx"], "i32") if k else None, _ptr(out["min_idx"], "i32") if k else None,
+        _ptr(out["residual"], "f32") if k else None, _stream(stream)))
     return out
 
 
@@ -286,8 +305,8 @@ def lut_gemm(idx_act, act_scale, idx_w, w_scale, lut, b_a: int, b_w: int, algo: 
     if y is None:
         y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
     _check("oasis_lut_gemm", load().oasis_lut_gemm(
-        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
-        b_a, b_w, algo, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+        _ptr(idx_act, "u8"), _ptr(act_scale, "f32"), n, d_in, _ptr(idx_w, "i32"), _ptr(w_scale, "f32"), d_out, _ptr(lut, "u8"),
+        b_a, b_w, algo, _ptr(y, "f32"), 1 if accumulate else 0, _stream(stream)))
     return y
 
 
@@ -300,9 +319,9 @@ def outlier_compensate(max_idx, min_idx, residual, idx_w, lut, b_w: int, w_scale
     if y is None:
         y = torch.empty((n, d_out), dtype=torch.float32, device=max_idx.device)
     _check("oasis_outlier_compensate", load().oasis_outlier_compensate(
-        _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
-        _ptr(residual) if k else None, n, k, _ptr(idx_w), _ptr(lut), b_w, _ptr(w_scale), d_in,
-        d_out, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+        _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
+        _ptr(residual, "f32") if k else None, n, k, _ptr(idx_w, "i32"), _ptr(lut, "u8"), b_w, _ptr(w_scale, "f32"), d_in,
+        d_out, _ptr(y, "f32"), 1 if accumulate else 0, _stream(stream)))
     return y
 
 
@@ -315,9 +334,9 @@ def outlier_compensate_rows(max_idx, min_idx, residual, idx_wr, lut, b_w: int, w
     if y is None:
         y = torch.empty((n, d_out), dtype=torch.float32, device=max_idx.device)
     _check("oasis_outlier_compensate_rows", load().oasis_outlier_compensate_rows(
-        _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
-        _ptr(residual) if k else None, n, k, _ptr(idx_wr), _ptr(lut), b_w, _ptr(w_scale), d_in,
-        d_out, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+        _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
+        _ptr(residual, "f32") if k else None, n, k, _ptr(idx_wr, "i32"), _ptr(lut, "u8"), b_w, _ptr(w_scale, "f32"), d_in,
+        d_out, _ptr(y, "f32"), 1 if accumulate else 0, _stream(stream)))
     return y
 
 
@@ -332,9 +351,9 @@ def lut_gemm_compensated(idx_act, act_scale, idx_w, w_scale, lut, b_a: int, b_w:
     if y is None:
         y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
     _check("oasis_lut_gemm_compensated", load().oasis_lut_gemm_compensated(
-        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
-        b_a, b_w, _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
-        _ptr(residual) if k else None, k, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+        _ptr(idx_act, "u8"), _ptr(act_scale, "f32"), n, d_in, _ptr(idx_w, "i32"), _ptr(w_scale, "f32"), d_out, _ptr(lut, "u8"),
+        b_a, b_w, _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
+        _ptr(residual, "f32") if k else None, k, _ptr(y, "f32"), 1 if accumulate else 0, _stream(stream)))
     return y
 
 
@@ -350,9 +369,9 @@ def lut_gemm_compensated_rows(idx_act, act_scale, idx_w, idx_wr, w_scale, lut, b
     if y is None:
         y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
     _check("oasis_lut_gemm_compensated_rows", load().oasis_lut_gemm_compensated_rows(
-        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(idx_wr) if k else None,
-        _ptr(w_scale), d_out, _ptr(lut), b_a, b_w, _ptr(max_idx) if k else None,
-        _ptr(min_idx) if k else None, _ptr(residual) if k else None, k, _ptr(y),
+        _ptr(idx_act, "u8"), _ptr(act_scale, "f32"), n, d_in, _ptr(idx_w, "i32"), _ptr(idx_wr, "i32") if k else None,
+        _ptr(w_scale, "f32"), d_out, _ptr(lut, "u8"), b_a, b_w, _ptr(max_idx, "i32") if k else None,
+        _ptr(min_idx, "i32") if k else None, _ptr(residual, "f32") if k else None, k, _ptr(y, "f32"),
         1 if accumulate else 0, _stream(stream)))
     return y
 
@@ -370,9 +389,9 @@ def lut_gemm_compensated_percol(idx_act, act_scale, idx_w, w_scale, lut, cb_cols
     if y is None:
         y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
     _check("oasis_lut_gemm_compensated_percol", load().oasis_lut_gemm_compensated_percol(
-        _ptr(idx_act), _ptr(act_scale), n, d_in, _ptr(idx_w), _ptr(w_scale), d_out, _ptr(lut),
-        _ptr(cb_cols), b_a, b_w, _ptr(max_idx) if k else None, _ptr(min_idx) if k else None,
-        _ptr(residual) if k else None, k, _ptr(y), 1 if accumulate else 0, _stream(stream)))
+        _ptr(idx_act, "u8"), _ptr(act_scale, "f32"), n, d_in, _ptr(idx_w, "i32"), _ptr(w_scale, "f32"), d_out, _ptr(lut, "u8"),
+        _ptr(cb_cols, "f16"), b_a, b_w, _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
+        _ptr(residual, "f32") if k else None, k, _ptr(y, "f32"), 1 if accumulate else 0, _stream(stream)))
     return y
 
 

@@ -188,6 +188,8 @@ def test_compensate_errors(lib):
     assert c(None, P, P, 4, 3, P, P, 4, P, 16, 8, P, 1, None) == -1
     assert c(P, P, P, 4, 3, P, P, 4, P, 16, 8, MIS, 1, None) == -6
     assert c(P, P, P, 0, 3, P, P, 4, P, 16, 8, P, 1, None) == 0
+    # codes of 2^31 bytes (d_in / 8 * d_out words): 32-bit buffer offsets
+    assert c(P, P, P, 100, 3, P, P, 4, P, 65536, 65536, P, 1, None) == -9
 
 
 def test_compensate_rows_errors(lib):
@@ -240,3 +242,14 @@ def test_pack_weight_indices_matches_oracle_packing():
     assert np.array_equal(oasis.pack_weight_indices(w), O.pack_weight_indices(w))
     with pytest.raises(oasis.OasisError):
         oasis.pack_weight_indices(np.zeros((12, 4), dtype=np.uint8))
+
+
+def test_binding_refuses_host_tensors():
+    """The wrappers pass raw addresses: a tensor that is not on the GPU (or,
+    on a GPU, not contiguous or of the wrong element type) is refused before
+    any call."""
+    torch = pytest.importorskip("torch")
+    t = torch.zeros(16, dtype=torch.float32)
+    with pytest.raises(ValueError, match="CUDA"):
+        oasis._ptr(t, "f32")
+    assert oasis._ptr(None, "f32") is None

@@ -2,8 +2,13 @@
 
 Integer outputs (activation codes, per-token scale, outlier lists, LUT block)
 and the residuals (one fp32 rounding on both sides) must match bit for bit.
-fp32 outputs must satisfy |y - y_ref| <= max(1e-3 * |y_ref|, 1e-2) for every
-entry, y_ref being the oracle's fp64 result.
+fp32 outputs are held to 1e-3 relative error, with an absolute floor only for
+entries near zero: |y - y_ref| <= max(1e-3 * |y_ref|, min(1e-2, 1e-4 * rms)),
+rms being the root mean square of the reference row and y_ref the oracle's
+fp64 result.  An entry is "near zero" when |y_ref| < min(10, 0.1 * rms); every
+other entry must meet the relative bound alone.  The floor is never looser
+than the stated 1e-2, and it scales with the row: fp32 summation over K
+channels errs by about 1e-7 * sqrt(K) * rms (6e-6 * rms at K = 11008).
 """
 import dataclasses
 
@@ -17,6 +22,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 RTOL, ATOL = 1e-3, 1e-2
+ATOL_RMS = 1e-4   # absolute floor near zero, relative to the reference row's rms
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -40,10 +46,19 @@ def upload(L):
     return x, idx_w, s_w, lut
 
 
+def tolerance(ref):
+    """Per-entry bound: 1e-3 relative, an absolute floor only near zero."""
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.ndim == 0 or ref.size == 0:
+        return np.maximum(RTOL * np.abs(ref), ATOL)
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    return np.maximum(RTOL * np.abs(ref), np.minimum(ATOL, ATOL_RMS * rms))
+
+
 def assert_close(y, ref, what):
     y = np.asarray(y, dtype=np.float64)
     err = np.abs(y - ref)
-    bound = np.maximum(RTOL * np.abs(ref), ATOL)
+    bound = tolerance(ref)
     bad = err > bound
     assert not bad.any(), (f"{what}: {bad.sum()} of {bad.size} entries out of tolerance, "
                            f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}")
@@ -455,13 +470,24 @@ FULL = ["prefill_up_2048x4096x11008", "prefill_down_2048x11008x4096",
         "large_decode_16x8192x28672", "large_prefill_4096x8192x28672"]
 
 
+def sampled_tokens(n, seed):
+    """Rows checked at full size: the first and last token and one random token
+    in every 128-token tile (the prefill kernels' token tiles are 128 tokens
+    or a multiple of it), so every tile's output is checked somewhere."""
+    rng = np.random.default_rng(seed)
+    picks = {0, n - 1}
+    for t0 in range(0, n, 128):
+        picks.add(int(t0 + rng.integers(0, min(128, n - t0))))
+    return sorted(picks)
+
+
 @pytest.mark.parametrize("name", ["decode_8x4096x4096", "prefill_up_2048x4096x11008"])
 def test_w4a3_layers(name):
     """The paper's second precision point: 3-bit activations (8 centroids, a
     128-entry LUT), codes still one per nibble."""
     L = synth.make_layer(dataclasses.replace(synth.config(name), b_a=3, name=f"{name}_a3"))
     n = L.spec.n
-    tokens = None if n <= 8 else sorted({0, n - 1, 777, 1500})
+    tokens = None if n <= 8 else sampled_tokens(n, 4)
     run_full(L, tokens=tokens)
 
 
@@ -469,7 +495,6 @@ def test_w4a3_layers(name):
 def test_full_size_layers(name):
     L = synth.make_layer(synth.config(name))
     n = L.spec.n
-    rng = np.random.default_rng(3)
-    tokens = sorted({0, n - 1, *rng.choice(n, 2, replace=False).tolist()})
+    tokens = sampled_tokens(n, 3)
     algos = (oasis.ALGO_MFMA, oasis.ALGO_LUT) if n <= 2048 else (oasis.ALGO_MFMA,)
     run_full(L, algos=algos, tokens=tokens)

@@ -396,3 +396,60 @@ def test_pack_roundtrip():
     for p in range(16):
         for j in range(5):
             assert (int(pw[p // 8, j]) >> (4 * (p % 8))) & 0xF == w[p, j]
+
+
+# Hand-written packings of the three index layouts the library exchanges
+# (activation codes: channel 2q in the low nibble of byte q; weight codes,
+# GEMM layout: channel 8b+e of column j at bits 4e..4e+3 of word (b, j);
+# row layout: column 8m+c of channel p at bits 4c..4c+3 of word (p, m)).
+def check_act_packing(pack, unpack):
+    assert np.array_equal(pack(np.array([[1, 2, 3, 4]], dtype=np.uint8)),
+                          np.array([[0x21, 0x43]], dtype=np.uint8))
+    assert np.array_equal(pack(np.array([[15, 0, 0, 10], [7, 8, 9, 6]], dtype=np.uint8)),
+                          np.array([[0x0F, 0xA0], [0x87, 0x69]], dtype=np.uint8))
+    assert np.array_equal(unpack(np.array([[0x21, 0x43]], dtype=np.uint8), 4),
+                          np.array([[1, 2, 3, 4]], dtype=np.uint8))
+
+
+def test_act_packing_by_hand():
+    check_act_packing(O.pack_act_indices, O.unpack_act_indices)
+
+
+def test_act_packing_pin_catches_a_nibble_swap():
+    """The hand pin fails for a packer (and unpacker) with the nibbles swapped,
+    a mistake the round trip alone cannot see."""
+    def pack_swapped(a):
+        a = np.asarray(a, dtype=np.uint8)
+        return (a[:, 1::2] | (a[:, 0::2] << 4)).astype(np.uint8)
+
+    def unpack_swapped(p, K):
+        p = np.asarray(p, dtype=np.uint8)
+        out = np.zeros((p.shape[0], K), dtype=np.uint8)
+        out[:, 1::2] = p & 0xF
+        out[:, 0::2] = p >> 4
+        return out
+
+    a = np.arange(8, dtype=np.uint8).reshape(1, 8)
+    assert np.array_equal(unpack_swapped(pack_swapped(a), 8), a)   # round trip holds
+    with pytest.raises(AssertionError):
+        check_act_packing(pack_swapped, unpack_swapped)
+
+
+def test_weight_packing_by_hand():
+    w = np.zeros((8, 2), dtype=np.uint8)
+    w[:, 0] = np.arange(1, 9)            # channel e of column 0 holds e + 1
+    w[:, 1] = 15 - np.arange(8)          # channel e of column 1 holds 15 - e
+    assert np.array_equal(O.pack_weight_indices(w),
+                          np.array([[0x87654321, 0x89ABCDEF]], dtype=np.uint32))
+    w16 = np.zeros((16, 1), dtype=np.uint8)
+    w16[9, 0] = 5                         # channel 9 = word 1, nibble 1
+    assert np.array_equal(O.pack_weight_indices(w16), np.array([[0], [0x50]], dtype=np.uint32))
+
+
+def test_weight_row_packing_by_hand():
+    w = np.arange(1, 11, dtype=np.uint8).reshape(1, 10)   # columns 0..9 of channel 0
+    assert np.array_equal(O.pack_weight_rows(w),
+                          np.array([[0x87654321, 0x000000A9]], dtype=np.uint32))
+    w2 = np.zeros((2, 3), dtype=np.uint8)
+    w2[1, 2] = 12                         # channel 1, column 2: word (1, 0), nibble 2
+    assert np.array_equal(O.pack_weight_rows(w2), np.array([[0], [0xC00]], dtype=np.uint32))
