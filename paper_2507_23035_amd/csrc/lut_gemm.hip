@@ -754,6 +754,227 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
   }
 }
 
+// ----------------------------------------------------------------------------
+// MFMA kernel, many tokens: v_mfma_f32_32x32x16_f16 (A = weights, 32 output
+// columns; B = activations, 32 tokens; 16 channels), every wave expanding its
+// own operands from the codes through the dual table.
+//
+// A wave owns 32*CW columns x 32*FT tokens (CW * FT accumulator tiles of 16
+// registers); WX x WY waves form the workgroup tile.  An expanded operand
+// (32 rows x 16 channels, 1 KiB, four ds_read_b32 per lane) feeds CW or FT
+// MFMAs, so the LDS traffic per MFMA is 1 KiB * (1/CW + 1/FT): with 4 x 2
+// that is 3/4 of what the LDS delivers (128 B/clk per CU for these reads)
+// while the matrix cores run at their peak (one 32x32x16 MFMA per 8 clk per
+// CU), with 4 x 4 one half.
+//
+// Channel order inside the MFMA: lane (r, h) (r = lane mod 32, h = lane / 32)
+// of step s (0..3) takes word 4h + s of a block of 8 words (64 channels) on
+// both operands; a token's four words of one lane are one 16-byte load, a
+// weight word one 4-byte load (32 lanes: 128 contiguous bytes of a row).
+//
+// Output: lane (r, h), register v of tile (c, f) holds column
+// j0 + 32 c + 8 (v / 4) + 4 h + (v mod 4) of token t0 + 32 f + r.
+// ----------------------------------------------------------------------------
+typedef float float16_t __attribute__((ext_vector_type(16)));
+
+template <int CW, int FT>
+struct TileCodes {
+  uint32_t w[4][CW];  // weight word 4h + s of column group c
+  uint4_t a[FT];      // activation words 4h .. 4h + 3 of token group f
+};
+
+template <int CW, int FT, int WX, int WY>
+__global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
+  __shared__ uint32_t tab[256 * 64];  // 64 KiB dual decode table
+  const char* tb = reinterpret_cast<const char*>(tab);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r32 = lane & 31, h = lane >> 5;
+
+  const int tile = xcd_tile(blockIdx.x, ncx * nty);
+  const int cx = tile / nty, ty = tile % nty;
+  const int j0 = (cx * WX + wave % WX) * 32 * CW;
+  const int t0 = (ty * WY + wave / WX) * 32 * FT;
+  const uint32_t KB = (uint32_t)(A.d_in >> 3);  // words per token row = weight rows
+  const int nblk = (int)(KB >> 3);              // blocks of 8 words (64 channels)
+  const uint32_t d_out = (uint32_t)A.d_out;
+
+  // Reads past either tensor return 0 (the descriptor's size check covers the
+  // whole per-lane offset); the two blocks past the last one are requested
+  // too, so every refill is unconditional.  Columns and tokens past the end
+  // are clamped to the last one (their outputs are never stored).
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(A.idx_w), 0, (int)(KB * d_out * 4u), 0x00020000);
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(A.idx_act), 0, (int)((uint32_t)A.n * KB * 4u), 0x00020000);
+  uint32_t woff[CW], aoff[FT];
+#pragma unroll
+  for (int c = 0; c < CW; ++c)
+    woff[c] = ((uint32_t)(4 * h) * d_out + (uint32_t)min(j0 + 32 * c + r32, A.d_out - 1)) * 4u;
+#pragma unroll
+  for (int f = 0; f < FT; ++f)
+    aoff[f] = ((uint32_t)min(t0 + 32 * f + r32, A.n - 1) * KB + 4u * (uint32_t)h) * 4u;
+  const uint32_t wrow = d_out * 4u, wblk = 8u * d_out * 4u;
+
+  auto load = [&](int blk, TileCodes<CW, FT>& tc) {
+#pragma unroll
+    for (int f = 0; f < FT; ++f)
+      tc.a[f] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                ra, (int)(aoff[f] + (uint32_t)blk * 32u), 0, 0));
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int c = 0; c < CW; ++c)
+        tc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
+            rw, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
+  };
+
+  float16_t acc[CW][FT];
+#pragma unroll
+  for (int c = 0; c < CW; ++c)
+#pragma unroll
+    for (int f = 0; f < FT; ++f)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[c][f][v] = 0.0f;
+
+  const uint32_t l4w = (uint32_t)r32 * 4u, l4a = l4w + 128u;
+  // operands of step st (every block is full: d_in is a multiple of 64)
+  auto operands = [&](const TileCodes<CW, FT>& tc, int st, half8_t (&a)[CW], half8_t (&b)[FT]) {
+#pragma unroll
+    for (int c = 0; c < CW; ++c) a[c] = expand_dual(tc.w[st][c], tb, l4w);
+#pragma unroll
+    for (int f = 0; f < FT; ++f) b[f] = expand_dual(tc.a[f][st], tb, l4a);
+  };
+  auto mma = [&](const half8_t (&a)[CW], const half8_t (&b)[FT]) {
+#pragma unroll
+    for (int c = 0; c < CW; ++c)
+#pragma unroll
+      for (int f = 0; f < FT; ++f)
+        acc[c][f] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[c], b[f], acc[c][f], 0, 0, 0);
+  };
+  // Instruction order of one step: each MFMA keeps the matrix unit busy for
+  // 32 cycles, and the wave issues in order, so the table lookups of the next
+  // step (VALU v_perm + ds_read) and the code loads are spread between the
+  // MFMAs instead of being issued as a burst after them.
+  constexpr int NM = CW * FT;                     // MFMAs per step
+  constexpr int NX = 4 * (CW + FT);               // perms (= table reads) per step
+  constexpr int PX = (NX + NM - 1) / NM;          // per MFMA
+  constexpr int NL = FT + 4 * CW;                 // code loads per block
+  auto interleave = [&](bool with_loads) {
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, PX, 0);  // VALU
+      __builtin_amdgcn_sched_group_barrier(0x100, PX, 0);  // DS read
+      if (with_loads) __builtin_amdgcn_sched_group_barrier(0x020, (NL + NM - 1) / NM, 0);
+    }
+  };
+  // One block on the codes in `cur`; a0/b0 hold its step 0 operands on entry
+  // and the step 0 operands of the block in `nxt` on exit.  The registers of
+  // `cur` are refilled with block `refill` during the last step, once its
+  // step 3 operands are expanded.
+  half8_t a0[CW], b0[FT], a1[CW], b1[FT];
+  auto block = [&](const TileCodes<CW, FT>& cur, const TileCodes<CW, FT>& nxt,
+                   TileCodes<CW, FT>& refill_into, int refill) {
+    operands(cur, 1, a1, b1);
+    mma(a0, b0);
+    interleave(false);
+    __builtin_amdgcn_sched_barrier(0);
+    operands(cur, 2, a0, b0);
+    mma(a1, b1);
+    interleave(false);
+    __builtin_amdgcn_sched_barrier(0);
+    operands(cur, 3, a1, b1);
+    mma(a0, b0);
+    interleave(false);
+    __builtin_amdgcn_sched_barrier(0);
+    operands(nxt, 0, a0, b0);
+    load(refill, refill_into);
+    mma(a1, b1);
+    interleave(true);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // ---- prologue: first two blocks' codes requested, then the table
+  TileCodes<CW, FT> c0, c1;
+  load(0, c0);
+  load(1, c1);
+  if (wave < 4) {
+    DualTableLoader dt;
+    dt.load(A.lut, (uint32_t)wave);
+    dt.store(tab, (uint32_t)wave, lane);
+  }
+  __syncthreads();
+
+  // block b's codes are in c0 (b even) or c1; during its last step the
+  // registers are refilled with the codes two blocks ahead (requested one
+  // block before the step that expands them).  The loop body is straight-line
+  // (an odd last block is peeled): with a conditional half in it the
+  // compiler's wait analysis would assume the worst at the loop head and wait
+  // for every load in flight.  Blocks past the end read zeros (never used).
+  operands(c0, 0, a0, b0);
+  int blk = 0;
+  for (; blk + 1 < nblk; blk += 2) {
+    block(c0, c1, c0, blk + 2);
+    block(c1, c0, c1, blk + 3);
+  }
+  if (blk < nblk) block(c0, c1, c0, blk + 2);
+
+  // ---- epilogue: y (+)= t_i * s_j * acc, four consecutive columns per store
+  const bool vec = (A.d_out & 3) == 0 && (reinterpret_cast<uintptr_t>(A.y) & 15u) == 0 &&
+                   (reinterpret_cast<uintptr_t>(A.w_scale) & 15u) == 0;
+#pragma unroll
+  for (int f = 0; f < FT; ++f) {
+    const int tok = t0 + 32 * f + r32;
+    if (tok >= A.n) continue;
+    const float ts = A.act_scale[tok];
+    float* yrow = A.y + (size_t)tok * A.d_out;
+#pragma unroll
+    for (int c = 0; c < CW; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int j = j0 + 32 * c + 8 * g + 4 * h;
+        if (vec) {
+          if (j >= A.d_out) continue;  // d_out % 4 == 0: the four columns are all in or out
+          const float4_t sw = *reinterpret_cast<const float4_t*>(A.w_scale + j);
+          float4_t v = {acc[c][f][4 * g], acc[c][f][4 * g + 1], acc[c][f][4 * g + 2],
+                        acc[c][f][4 * g + 3]};
+          v = ts * sw * v;
+          float4_t* dst = reinterpret_cast<float4_t*>(yrow + j);
+          *dst = A.accumulate ? *dst + v : v;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (j + q >= A.d_out) continue;
+            const float v = ts * A.w_scale[j + q] * acc[c][f][4 * g + q];
+            yrow[j + q] = A.accumulate ? yrow[j + q] + v : v;
+          }
+        }
+      }
+  }
+}
+
+template <int CW, int FT, int WX, int WY>
+static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
+  constexpr int TC = 32 * CW * WX, TT = 32 * FT * WY;
+  const int ncx = (a.d_out + TC - 1) / TC;
+  const int nty = (a.n + TT - 1) / TT;
+  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY>), dim3(ncx * nty), dim3(WX * WY * 64), 0,
+                     s, a, ncx, nty);
+  return hipGetLastError();
+}
+
+// Workgroup tile 256 x 256 (2 x 2 waves of 128 x 128, 256 accumulator
+// registers per lane: one wave per SIMD) when the grid fills at least three
+// rounds of the 256 CUs, else 256 x 128 (waves of 128 x 64, two workgroups
+// and two waves per SIMD on a CU).  Needs d_in % 64 == 0 (whole blocks of 64
+// channels).
+static hipError_t launch_gemm_tiles(const GemmArgs& a, hipStream_t s) {
+  const long t44 = (long)((a.d_out + 255) / 256) * ((a.n + 255) / 256);
+  if (t44 >= 3 * 256) return launch_tile<4, 4, 2, 2>(a, s);
+  return launch_tile<4, 2, 2, 2>(a, s);
+}
+
 template <int CW, int TF, int WX, int WY>
 static void launch_prefill(const GemmArgs& a, hipStream_t s) {
   const int ncx = (a.d_out + WX * 16 * CW - 1) / (WX * 16 * CW);
@@ -863,6 +1084,8 @@ hipError_t launch_gemm_mfma(const GemmArgs& a, hipStream_t s) {
     launch_gemv_tf<1>(a, s);
   } else if (a.n <= 32) {
     launch_gemv_tf<2>(a, s);
+  } else if (a.d_in % 64 == 0) {
+    return launch_gemm_tiles(a, s);
   } else {
     launch_prefill<4, 4, 2, 2>(a, s);
   }
