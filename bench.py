@@ -92,7 +92,7 @@ KERNEL_SOURCES = {
     "build_lut_quantize_act": ["quantize.hip"], "quantize_act_static": ["quantize.hip"],
     "build_lut_quantize_act_static": ["quantize.hip"],
     "detect_outliers": ["quantize.hip"],
-    "outlier_compensate": ["compensate.hip"],
+    "outlier_compensate": ["compensate.hip", "split.hip", "lut_gemm.hip"],
     "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
     "lut_gemm_compensated_rows": ["lut_gemm.hip", "compensate.hip"],
     "lut_gemm_compensated_percol": ["lut_gemm.hip"],
@@ -313,6 +313,9 @@ def run_workload(args, layer, weights, dev, side):
         "residual": torch.empty((n, 2 * k), dtype=torch.float32, device=dev),
     }
     y = torch.empty((n, d_out), dtype=torch.float32, device=dev)
+    # scratch of the split compensation (many tokens), allocated once
+    ws = torch.empty(max(1, oasis.split_workspace_bytes(n, d_in, d_out, k)), dtype=torch.uint8,
+                     device=dev)
     path = args.path
     if path == "auto":
         path = "fused" if ((n <= 32 or args.percol) and algo == oasis.ALGO_MFMA) else "separate"
@@ -336,9 +339,9 @@ def run_workload(args, layer, weights, dev, side):
             cb_a, b_a, cb_w, b_w, x, k, thr[0], thr[1], scale, lut=lut, out=q),
         "cluster_act": lambda c: oasis.cluster_act(x, lut, b_a, out=q),
         "detect_outliers": lambda c: oasis.detect_outliers(x, lut, b_a, k, out=q),
-        "outlier_compensate": lambda c: oasis.outlier_compensate_rows(
-            q["max_idx"], q["min_idx"], q["residual"], idx_wr[c], lut, b_w, s_w, d_in, y=y,
-            accumulate=False),
+        "outlier_compensate": lambda c: oasis.outlier_compensate_split(
+            q["max_idx"], q["min_idx"], q["residual"], idx_w[c], idx_wr[c], lut, b_w, s_w, d_in,
+            y=y, accumulate=False, workspace=ws),
         "lut_gemm": lambda c: oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut,
                                              b_a, b_w, algo, y=y, accumulate=True),
         "lut_gemm_compensated": lambda c: oasis.lut_gemm_compensated(
@@ -401,12 +404,14 @@ def run_workload(args, layer, weights, dev, side):
             oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo,
                            y=y, accumulate=False)
             main.wait_stream(side)
-            oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr[c],
-                                          L, b_w, s_w, d_in, y=y, accumulate=True)
+            oasis.outlier_compensate_split(q["max_idx"], q["min_idx"], q["residual"], idx_w[c],
+                                           idx_wr[c], L, b_w, s_w, d_in, y=y, accumulate=True,
+                                           workspace=ws)
         else:
             quantize(L)
-            oasis.outlier_compensate_rows(q["max_idx"], q["min_idx"], q["residual"], idx_wr[c],
-                                          L, b_w, s_w, d_in, y=y, accumulate=False)
+            oasis.outlier_compensate_split(q["max_idx"], q["min_idx"], q["residual"], idx_w[c],
+                                           idx_wr[c], L, b_w, s_w, d_in, y=y, accumulate=False,
+                                           workspace=ws)
             oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, L, b_a, b_w, algo, y=y,
                            accumulate=True)
 
@@ -469,13 +474,13 @@ def run_workload(args, layer, weights, dev, side):
         if path == "lookahead":
             y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a,
                                    b_w, algo)
-            oasis.outlier_compensate_rows(q1["max_idx"], q1["min_idx"], q1["residual"],
-                                          idx_wr[c_last], lut, b_w, s_w, d_in, y=y_ref,
-                                          accumulate=True)
+            oasis.outlier_compensate_split(q1["max_idx"], q1["min_idx"], q1["residual"],
+                                           idx_w[c_last], idx_wr[c_last], lut, b_w, s_w, d_in,
+                                           y=y_ref, accumulate=True, workspace=ws)
         else:
-            y_ref = oasis.outlier_compensate_rows(q1["max_idx"], q1["min_idx"], q1["residual"],
-                                                  idx_wr[c_last], lut, b_w, s_w, d_in,
-                                                  accumulate=False)
+            y_ref = oasis.outlier_compensate_split(q1["max_idx"], q1["min_idx"], q1["residual"],
+                                                   idx_w[c_last], idx_wr[c_last], lut, b_w, s_w,
+                                                   d_in, accumulate=False, workspace=ws)
             oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a, b_w,
                            algo, y=y_ref, accumulate=True)
     torch.cuda.synchronize()
@@ -545,7 +550,7 @@ def run_workload(args, layer, weights, dev, side):
         "roofline": roof(dom),
         "roofline_main_branch": roof(gemm_name),
     }
-    del q, y, x
+    del q, y, x, ws
     return out
 
 

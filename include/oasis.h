@@ -56,7 +56,8 @@ enum oasis_status {
   OASIS_ERR_ALIGN = -6,       /* a pointer is not aligned as documented            */
   OASIS_ERR_MODE = -7,        /* unknown scale mode or algorithm                   */
   OASIS_ERR_LAUNCH = -8,      /* the HIP runtime refused a launch                  */
-  OASIS_ERR_TOO_LARGE = -9    /* a size exceeds what a kernel supports             */
+  OASIS_ERR_TOO_LARGE = -9,   /* a size exceeds what a kernel supports             */
+  OASIS_ERR_WORKSPACE = -10   /* workspace missing, too small or misaligned        */
 };
 
 enum oasis_scale_mode {
@@ -265,6 +266,38 @@ int oasis_outlier_compensate_rows(const int32_t* max_idx, const int32_t* min_idx
                                   const oasis_lut_block* lut, int b_w, const float* w_scale,
                                   int d_in, int d_out, float* y, int accumulate,
                                   hipStream_t stream);
+
+/*
+ * oasis_outlier_compensate_split - the error compensation of Sec. III-C2 for
+ * many tokens, split by channel.  Outliers of LLM activations gather in a few
+ * channels that most tokens list: channels listed by at least max(2, n / 8)
+ * tokens (at most 256 of them, lowest channels first) are compensated
+ * together as a dense contraction on the matrix cores (the residuals of a
+ * token, scaled by a power of two, as an fp16 hi/lo pair per channel), every
+ * other entry by the row-layout kernel of oasis_outlier_compensate_rows over
+ * compacted per-token lists.  The result is Y' of oasis_outlier_compensate;
+ * which channels count as heavy changes only the fp32 summation order.  (A
+ * list naming a channel twice with nonzero residuals has both entries summed,
+ * in an order that may vary between runs.)
+ *   idx_w     : DEVICE weight codes in the GEMM layout (the dense part reads
+ *               the heavy channels' rows from here).
+ *   idx_wr    : DEVICE weight codes in the row layout (the other entries).
+ *   workspace : DEVICE scratch of at least
+ *               oasis_outlier_compensate_split_workspace(n, d_in, d_out, k)
+ *               bytes, 256-byte aligned, owned by the caller; overwritten.
+ *               Calls that share a workspace must not overlap.
+ *   Every other argument, the result and accumulate as in
+ *   oasis_outlier_compensate.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, TOO_LARGE (either code layout of
+ * 2^31 bytes or more), WORKSPACE, LAUNCH.
+ */
+size_t oasis_outlier_compensate_split_workspace(int n, int d_in, int d_out, int k);
+int oasis_outlier_compensate_split(const int32_t* max_idx, const int32_t* min_idx,
+                                   const float* residual, int n, int k, const uint32_t* idx_w,
+                                   const uint32_t* idx_wr, const oasis_lut_block* lut, int b_w,
+                                   const float* w_scale, int d_in, int d_out, float* y,
+                                   int accumulate, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
 
 /*
  * oasis_lut_gemm_compensated - main branch and outlier branch in one call

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liboasis.so")
-SOURCES = ["lut.hip", "quantize.hip", "lut_gemm.hip", "compensate.hip", "api.cpp"]
+SOURCES = ["lut.hip", "quantize.hip", "lut_gemm.hip", "compensate.hip", "split.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

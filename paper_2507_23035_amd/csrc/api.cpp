@@ -59,6 +59,7 @@ const char* oasis_status_str(int status) {
     case OASIS_ERR_MODE: return "unknown scale mode or algorithm";
     case OASIS_ERR_LAUNCH: return "HIP launch failed";
     case OASIS_ERR_TOO_LARGE: return "size exceeds kernel limits";
+    case OASIS_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     default: return "unknown status";
   }
 }
@@ -292,6 +293,42 @@ int oasis_outlier_compensate_rows(const int32_t* max_idx, const int32_t* min_idx
   oasis::CompArgs a{max_idx, min_idx, residual, n, k, idx_wr, lut, b_w, w_scale, d_in, d_out, y,
                     accumulate ? 1 : 0};
   return launched(oasis::launch_compensate_wr(a, stream));
+}
+
+size_t oasis_outlier_compensate_split_workspace(int n, int d_in, int d_out, int k) {
+  if (n < 0 || d_in < 0 || d_out < 0 || k < 0) return 0;
+  return oasis::split_layout(n, d_in, d_out, k).total;
+}
+
+int oasis_outlier_compensate_split(const int32_t* max_idx, const int32_t* min_idx,
+                                   const float* residual, int n, int k, const uint32_t* idx_w,
+                                   const uint32_t* idx_wr, const oasis_lut_block* lut, int b_w,
+                                   const float* w_scale, int d_in, int d_out, float* y,
+                                   int accumulate, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!lut || !w_scale || !y) return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual || !idx_w || !idx_wr)) return OASIS_ERR_NULL;
+  if (!aligned(max_idx, 4) || !aligned(min_idx, 4) || !aligned(residual, 4) ||
+      !aligned(idx_w, 16) || !aligned(idx_wr, 4) || !aligned(lut, 16) || !aligned(w_scale, 4) ||
+      !aligned(y, 4))
+    return OASIS_ERR_ALIGN;
+  // 32-bit byte offsets into the row-layout codes, the heavy rows and the
+  // dense operand
+  if ((uint64_t)d_in * (uint64_t)((d_out + 7) / 8) * 4u >= (1ull << 31)) return OASIS_ERR_TOO_LARGE;
+  if (!offsets_fit(n, oasis::kSplitPos, d_out) ||
+      (uint64_t)(n + 1) * 2u * oasis::kSplitPos >= (1ull << 31))
+    return OASIS_ERR_TOO_LARGE;
+  if (k > 0) {
+    if (!workspace || !aligned(workspace, 256)) return OASIS_ERR_WORKSPACE;
+    if (workspace_bytes < oasis::split_layout(n, d_in, d_out, k).total) return OASIS_ERR_WORKSPACE;
+  }
+  oasis::CompArgs a{max_idx, min_idx, residual, n, k, idx_wr, lut, b_w, w_scale, d_in, d_out, y,
+                    accumulate ? 1 : 0, nullptr};
+  return launched(oasis::launch_compensate_split(a, idx_w, workspace, stream));
 }
 
 static int gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,

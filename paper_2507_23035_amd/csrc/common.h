@@ -140,6 +140,12 @@ struct GemmArgs {
   // optional: per-output-channel weight codebooks, fp16 [d_out][16]; when set
   // they replace the LUT block's C_W (GEMV kernel only)
   const uint16_t* cb_cols;
+  // optional (many-token kernel only): the B operand is an fp16 matrix
+  // [n][a_row / 2] of values (idx_act holds its bytes) instead of activation
+  // codes, and the reduction runs over ceil(2 * *kdyn / 64) blocks of 64
+  // positions (a length known on the device only)
+  const int* kdyn;
+  int a_row;  // bytes per row of that matrix
 };
 
 struct CompArgs {
@@ -154,7 +160,28 @@ struct CompArgs {
   int d_in, d_out;
   float* y;
   int accumulate;
+  // optional: compacted lists (row-layout kernel only): token i's live entries
+  // are max_idx[i][0..cnt[i]) (channels) and residual[i][0..cnt[i]), in list
+  // order, each row 2k long; min_idx is not read
+  const int32_t* cnt;
 };
+
+// Heavy / sparse split of the compensation for many tokens: channels listed
+// by at least one token in eight (at most kSplitHeavy of them, lowest
+// channels first) are compensated as a dense contraction on the matrix cores,
+// the other entries by the row-layout kernel.  The workspace holds the
+// per-channel counts, the heavy channel list, the dense residual operand, the
+// heavy channels' weight codes and the compacted lists of the other entries.
+constexpr int kSplitHeavy = 256;
+constexpr int kSplitPos = 2 * kSplitHeavy;  // dense positions: hi and lo half of each channel
+struct SplitLayout {
+  size_t count, slot, hlist, pow2, rh, idxh, spp, spr, spc, total;
+};
+SplitLayout split_layout(int n, int d_in, int d_out, int k);
+hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm, void* ws,
+                                   hipStream_t s);
+// the dense part: the many-token MFMA kernel with an fp16 value operand
+hipError_t launch_gemm_values(const GemmArgs& a, hipStream_t s);
 
 // Bytes of dynamic LDS the quantize kernel needs for a token of d_in values
 // and k outliers per side.

@@ -385,7 +385,8 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
 // row `byte` holds 32 copies of pair(C_W, byte), lane l reads copy l mod 32,
 // so the reads are conflict free - and each centroid meets the residual in
 // one fp32 FMA (v_fma_mix_f32 takes the fp16 half directly).  48 KiB of LDS
-// per workgroup keeps three workgroups on a CU to hide the row loads.
+// per workgroup keeps three workgroups on a CU to hide the row loads (a
+// 64-copy table, whose offsets need no shift, left two and measured slower).
 // ----------------------------------------------------------------------------
 constexpr int WR_U = 16;    // entries per unit of word loads
 constexpr int WR_C = 512;   // list entries per wave held in LDS at a time
@@ -409,8 +410,30 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   const int tw = tok0 + wave;  // first token of this wave; then every fourth
   const int tend = min(A.n, tok0 + tt);
   const int ntw = tw < tend ? (tend - tw + 3) / 4 : 0;
-  const int nch = (E + WR_U - 1) / WR_U;  // units per token
-  const int U = ntw * nch;
+  // units per token: the whole list, or with compacted lists the token's own
+  // entries (at least one unit: a token's last unit writes y).  Lane j < ntw
+  // holds the first unit past token tw + 4j (inclusive prefix sum); units are
+  // numbered over the wave's tokens in order.
+  const int nch = (E + WR_U - 1) / WR_U;
+  int nu = 0;
+  if (lane < ntw) {
+    nu = nch;
+    if (A.cnt) nu = max(1, (min(max(A.cnt[tw + 4 * lane], 0), E) + WR_U - 1) / WR_U);
+  }
+  const int uend = (int)wave_incl_scan((uint32_t)nu);
+  const int U = __builtin_amdgcn_readlane(uend, 63);
+  // token slot j of unit u (the first j whose end exceeds u) and its first unit
+  auto unit_token = [&](int u, int& j, int& ubeg) {
+    j = 0;
+    ubeg = 0;
+    for (int q = 0; q + 1 < ntw; ++q) {
+      const int endq = __builtin_amdgcn_readlane(uend, q);
+      if (u >= endq) {
+        j = q + 1;
+        ubeg = endq;
+      }
+    }
+  };
   // copy the lists of units [c0, c1) into this wave's LDS area, validated:
   // dead entries (past the lists, duplicates with residual 0, channels out of
   // range) get channel -1 and residual 0.  LDS operations of one wave run in
@@ -423,13 +446,23 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
     for (int j = 0; j < PER; ++j) {  // every load first, then the checks
       const int f = lane + 64 * j;
       const int u = c0 + f / WR_U;
-      const int i = tw + 4 * (u / nch), e = WR_U * (u % nch) + f % WR_U;
+      int slot_j, ubeg;
+      unit_token(u, slot_j, ubeg);
+      const int i = tw + 4 * slot_j, e = WR_U * (u - ubeg) + f % WR_U;
       pv[j] = -1;
       rv[j] = 0.0f;
       if (f < (c1 - c0) * WR_U && e < E) {
-        const int32_t* src = e < k ? A.max_idx + (size_t)i * k + e : A.min_idx + (size_t)i * k + (e - k);
-        pv[j] = *src;
-        rv[j] = A.residual[(size_t)i * E + e];
+        if (A.cnt) {  // compacted: max_idx rows hold the channels, 2k long
+          if (e < A.cnt[i]) {
+            pv[j] = A.max_idx[(size_t)i * E + e];
+            rv[j] = A.residual[(size_t)i * E + e];
+          }
+        } else {
+          const int32_t* src =
+              e < k ? A.max_idx + (size_t)i * k + e : A.min_idx + (size_t)i * k + (e - k);
+          pv[j] = *src;
+          rv[j] = A.residual[(size_t)i * E + e];
+        }
       }
     }
 #pragma unroll
@@ -512,9 +545,11 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
         }
       }
     }
-    if (u % nch != nch - 1) return;
+    int slot_j, ubeg;
+    unit_token(u, slot_j, ubeg);
+    if (u != __builtin_amdgcn_readlane(uend, slot_j) - 1) return;
     // the token's last unit: y (+)= s_j * acc
-    const int i = tw + 4 * (u / nch);
+    const int i = tw + 4 * slot_j;
     float* dst = A.y + (size_t)i * d_out + 8u * m;
     if (vec) {
       float4* d4 = reinterpret_cast<float4*>(dst);

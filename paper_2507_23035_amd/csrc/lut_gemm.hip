@@ -777,14 +777,18 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
 // ----------------------------------------------------------------------------
 typedef float float16_t __attribute__((ext_vector_type(16)));
 
-template <int CW, int FT>
+// BV: the B operand is an fp16 value matrix (GemmArgs::kdyn), one 16-byte load
+// per lane, step and token group, instead of activation codes.
+template <int CW, int FT, bool BV>
 struct TileCodes {
-  uint32_t w[4][CW];  // weight word 4h + s of column group c
-  uint4_t a[FT];      // activation words 4h .. 4h + 3 of token group f
+  uint32_t w[4][CW];        // weight word 4h + s of column group c
+  uint4_t a[BV ? 4 : 1][FT];  // codes: words 4h .. 4h + 3 of token group f;
+                              // values: positions 8 (4h + s) .. + 7 of step s
 };
 
-template <int CW, int FT, int WX, int WY>
-__global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
+template <int CW, int FT, int WX, int WY, bool BV>
+__global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
+    k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
   __shared__ uint32_t tab[256 * 64];  // 64 KiB dual decode table
   const char* tb = reinterpret_cast<const char*>(tab);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -796,7 +800,10 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
   const int j0 = (cx * WX + wave % WX) * 32 * CW;
   const int t0 = (ty * WY + wave / WX) * 32 * FT;
   const uint32_t KB = (uint32_t)(A.d_in >> 3);  // words per token row = weight rows
-  const int nblk = (int)(KB >> 3);              // blocks of 8 words (64 channels)
+  // blocks of 8 words (64 channels); with a value operand, of 64 positions up
+  // to the device-side length
+  const int nblk = BV ? (2 * __builtin_amdgcn_readfirstlane(*A.kdyn) + 63) / 64 : (int)(KB >> 3);
+  const uint32_t arow = BV ? (uint32_t)A.a_row : KB * 4u;  // bytes per token row
   const uint32_t d_out = (uint32_t)A.d_out;
 
   // Reads past either tensor return 0 (the descriptor's size check covers the
@@ -806,21 +813,30 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(A.idx_w), 0, (int)(KB * d_out * 4u), 0x00020000);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(A.idx_act), 0, (int)((uint32_t)A.n * KB * 4u), 0x00020000);
+      const_cast<uint8_t*>(A.idx_act), 0, (int)((uint32_t)A.n * arow), 0x00020000);
   uint32_t woff[CW], aoff[FT];
 #pragma unroll
   for (int c = 0; c < CW; ++c)
     woff[c] = ((uint32_t)(4 * h) * d_out + (uint32_t)min(j0 + 32 * c + r32, A.d_out - 1)) * 4u;
 #pragma unroll
   for (int f = 0; f < FT; ++f)
-    aoff[f] = ((uint32_t)min(t0 + 32 * f + r32, A.n - 1) * KB + 4u * (uint32_t)h) * 4u;
+    aoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * arow + (BV ? 64u : 16u) * (uint32_t)h;
   const uint32_t wrow = d_out * 4u, wblk = 8u * d_out * 4u;
 
-  auto load = [&](int blk, TileCodes<CW, FT>& tc) {
+  auto load = [&](int blk, TileCodes<CW, FT, BV>& tc) {
 #pragma unroll
-    for (int f = 0; f < FT; ++f)
-      tc.a[f] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                ra, (int)(aoff[f] + (uint32_t)blk * 32u), 0, 0));
+    for (int f = 0; f < FT; ++f) {
+      if constexpr (BV) {
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+          tc.a[st][f] = __builtin_bit_cast(
+              uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                           ra, (int)(aoff[f] + (uint32_t)blk * 128u + 16u * (uint32_t)st), 0, 0));
+      } else {
+        tc.a[0][f] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                     ra, (int)(aoff[f] + (uint32_t)blk * 32u), 0, 0));
+      }
+    }
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
@@ -839,11 +855,13 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
 
   const uint32_t l4w = (uint32_t)r32 * 4u, l4a = l4w + 128u;
   // operands of step st (every block is full: d_in is a multiple of 64)
-  auto operands = [&](const TileCodes<CW, FT>& tc, int st, half8_t (&a)[CW], half8_t (&b)[FT]) {
+  auto operands = [&](const TileCodes<CW, FT, BV>& tc, int st, half8_t (&a)[CW],
+                      half8_t (&b)[FT]) {
 #pragma unroll
     for (int c = 0; c < CW; ++c) a[c] = expand_dual(tc.w[st][c], tb, l4w);
 #pragma unroll
-    for (int f = 0; f < FT; ++f) b[f] = expand_dual(tc.a[f][st], tb, l4a);
+    for (int f = 0; f < FT; ++f)
+      b[f] = BV ? __builtin_bit_cast(half8_t, tc.a[st][f]) : expand_dual(tc.a[0][f][st], tb, l4a);
   };
   auto mma = [&](const half8_t (&a)[CW], const half8_t (&b)[FT]) {
 #pragma unroll
@@ -857,9 +875,9 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
   // step (VALU v_perm + ds_read) and the code loads are spread between the
   // MFMAs instead of being issued as a burst after them.
   constexpr int NM = CW * FT;                     // MFMAs per step
-  constexpr int NX = 4 * (CW + FT);               // perms (= table reads) per step
+  constexpr int NX = 4 * (CW + (BV ? 0 : FT));    // perms (= table reads) per step
   constexpr int PX = (NX + NM - 1) / NM;          // per MFMA
-  constexpr int NL = FT + 4 * CW;                 // code loads per block
+  constexpr int NL = (BV ? 4 : 1) * FT + 4 * CW;  // loads per block
   auto interleave = [&](bool with_loads) {
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
@@ -874,8 +892,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
   // `cur` are refilled with block `refill` during the last step, once its
   // step 3 operands are expanded.
   half8_t a0[CW], b0[FT], a1[CW], b1[FT];
-  auto block = [&](const TileCodes<CW, FT>& cur, const TileCodes<CW, FT>& nxt,
-                   TileCodes<CW, FT>& refill_into, int refill) {
+  auto block = [&](const TileCodes<CW, FT, BV>& cur, const TileCodes<CW, FT, BV>& nxt,
+                   TileCodes<CW, FT, BV>& refill_into, int refill) {
     operands(cur, 1, a1, b1);
     mma(a0, b0);
     interleave(false);
@@ -896,7 +914,7 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
   };
 
   // ---- prologue: first two blocks' codes requested, then the table
-  TileCodes<CW, FT> c0, c1;
+  TileCodes<CW, FT, BV> c0, c1;
   load(0, c0);
   load(1, c1);
   if (wave < 4) {
@@ -954,14 +972,21 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 ? 1 : 2)) k_gemm_mf
   }
 }
 
-template <int CW, int FT, int WX, int WY>
+template <int CW, int FT, int WX, int WY, bool BV = false>
 static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   constexpr int TC = 32 * CW * WX, TT = 32 * FT * WY;
   const int ncx = (a.d_out + TC - 1) / TC;
   const int nty = (a.n + TT - 1) / TT;
-  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY>), dim3(ncx * nty), dim3(WX * WY * 64), 0,
-                     s, a, ncx, nty);
+  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV>), dim3(ncx * nty), dim3(WX * WY * 64),
+                     0, s, a, ncx, nty);
   return hipGetLastError();
+}
+
+// The dense part of the split compensation: B = fp16 values (a.idx_act, rows
+// of a.a_row bytes), reduction length 2 * *a.kdyn positions, weight codes
+// a.idx_w in the GEMM layout over those positions.
+hipError_t launch_gemm_values(const GemmArgs& a, hipStream_t s) {
+  return launch_tile<4, 2, 2, 2, true>(a, s);
 }
 
 // Workgroup tile 256 x 256 (2 x 2 waves of 128 x 128, 256 accumulator

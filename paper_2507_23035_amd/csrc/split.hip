@@ -1,0 +1,263 @@
+// Error compensation of many tokens (Sec. III-C2) split by channel:
+//   Y'[i][j] = s_j * sum_e r_ie * C_W[w(p_ie, j)]
+//            = s_j * sum_{h in H} R[i][h] * C_W[w(h, j)]        (heavy channels)
+//            + s_j * sum_{e : p_ie not in H} r_ie * C_W[w(p_ie, j)] (the rest)
+// with R[i][h] the residual of token i at heavy channel h (0 when the token
+// does not list it).  Activation outliers of LLMs gather in a few channels
+// that most tokens list, so the first sum is a dense contraction over a short
+// reduction: it runs on the matrix cores (the many-token MFMA kernel with an
+// fp16 value operand), the second on the row-layout kernel over compacted
+// lists.
+//
+// Dense operand: R is scaled per token by a power of two 2^-E_i (exact) so
+// that |R 2^-E_i| < 2, then split into fp16 hi = fp16(v) and lo = fp16(v - hi);
+// hi + lo equals v to about 2^-22 relative, and C_W values are exact fp16, so
+// the products carry no more error than the fp32 sums.  Positions 2h and 2h+1
+// of the reduction are the hi and lo halves of heavy channel h, both paired
+// with channel h's weight code; the kernel's per-token scale is 2^E_i.
+//
+// Heavy channels: listed by at least max(2, n / 8) tokens (a live entry:
+// nonzero residual, channel in range), the first kSplitHeavy of them in
+// channel order.  Which channels are heavy changes only the summation order.
+#include <algorithm>
+
+#include "common.h"
+
+namespace oasis {
+
+static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+SplitLayout split_layout(int n, int d_in, int d_out, int k) {
+  SplitLayout L;
+  size_t o = 0;
+  const size_t E = 2 * (size_t)k;
+  L.count = o; o += align256(4 * (size_t)d_in);
+  L.slot = o; o += align256(4 * (size_t)d_in);
+  L.hlist = o; o += align256(4 * (size_t)(kSplitHeavy + 1));  // + the count nh
+  L.pow2 = o; o += align256(4 * (size_t)n);
+  L.rh = o; o += align256(2 * (size_t)kSplitPos * n);
+  L.idxh = o; o += align256(4 * (size_t)(kSplitPos / 8) * d_out);
+  L.spp = o; o += align256(4 * E * n);
+  L.spr = o; o += align256(4 * E * n);
+  L.spc = o; o += align256(4 * (size_t)n);
+  L.total = o;
+  return L;
+}
+
+// entry f of the lists: token f / 2k, place f mod 2k; live when its
+// residual is nonzero and its channel in range
+__device__ __forceinline__ bool split_entry(const CompArgs& A, size_t f, int& p, float& r) {
+  const int E = 2 * A.k;
+  const size_t i = f / (size_t)E;
+  const int e = (int)(f - i * (size_t)E);
+  p = e < A.k ? A.max_idx[i * A.k + e] : A.min_idx[i * A.k + (e - A.k)];
+  r = A.residual[i * (size_t)E + e];
+  return r != 0.0f && p >= 0 && p < A.d_in;
+}
+
+// how many tokens list each channel.  LDS: a histogram of the workgroup's
+// share of the entries (d_in <= kSplitLdsBins), flushed with one global add
+// per touched channel - the heavy channels are listed by most tokens, and
+// global atomics on them from every entry would serialize.
+constexpr int kSplitLdsBins = 16384;
+template <bool LDS>
+__global__ void __launch_bounds__(256) k_split_count(CompArgs A, int* __restrict__ count) {
+  __shared__ int hist[LDS ? kSplitLdsBins : 1];
+  const size_t tot = (size_t)A.n * 2 * A.k;
+  if constexpr (LDS) {
+    for (int p = threadIdx.x; p < A.d_in; p += 256) hist[p] = 0;
+    __syncthreads();
+  }
+  for (size_t f = (size_t)blockIdx.x * 256 + threadIdx.x; f < tot; f += (size_t)gridDim.x * 256) {
+    int p;
+    float r;
+    if (split_entry(A, f, p, r)) {
+      if constexpr (LDS) atomicAdd(&hist[p], 1);
+      else atomicAdd(&count[p], 1);
+    }
+  }
+  if constexpr (LDS) {
+    __syncthreads();
+    for (int p = threadIdx.x; p < A.d_in; p += 256)
+      if (hist[p]) atomicAdd(&count[p], hist[p]);
+  }
+}
+
+// heavy channels in channel order: slot[p] = index in the list or -1;
+// hlist[0..nh) = the channels, hlist[kSplitHeavy] = nh; one workgroup
+__global__ void __launch_bounds__(1024) k_split_select(int d_in, int thr,
+                                                        const int* __restrict__ count,
+                                                        int* __restrict__ slot,
+                                                        int* __restrict__ hlist) {
+  __shared__ uint64_t tmp[16];
+  __shared__ int total;
+  const int t = threadIdx.x;
+  const int per = (d_in + 1023) / 1024;
+  const int p0 = min(d_in, t * per), p1 = min(d_in, p0 + per);
+  uint64_t mine = 0;
+  for (int p = p0; p < p1; ++p) mine += count[p] >= thr;
+  const uint64_t incl = block_scan64<1024>(mine, tmp);
+  int idx = (int)(incl - mine);
+  for (int p = p0; p < p1; ++p) {
+    int sl = -1;
+    if (count[p] >= thr) {
+      if (idx < kSplitHeavy) {
+        sl = idx;
+        hlist[idx] = p;
+      }
+      ++idx;
+    }
+    slot[p] = sl;
+  }
+  if (t == 1023) total = (int)min((uint64_t)kSplitHeavy, incl);  // the last prefix is the total
+  __syncthreads();
+  const int nh = total;
+  if (t == 0) hlist[kSplitHeavy] = nh;
+  for (int h = nh + t; h < kSplitHeavy; h += 1024) hlist[h] = -1;
+}
+
+// One wave per token: the token's heavy residuals summed per heavy channel
+// (in LDS, fp32), scaled and split into the fp16 hi/lo row of the dense
+// operand; the other live entries compacted in list order.
+__global__ void __launch_bounds__(64) k_split_rows(CompArgs A, const int* __restrict__ slot,
+                                                   float* __restrict__ pow2,
+                                                   uint16_t* __restrict__ rh,
+                                                   int32_t* __restrict__ spp,
+                                                   float* __restrict__ spr,
+                                                   int32_t* __restrict__ spc) {
+  __shared__ float acc[kSplitHeavy];
+  const int i = blockIdx.x, lane = threadIdx.x;
+  const int E = 2 * A.k;
+  for (int h = lane; h < kSplitHeavy; h += 64) acc[h] = 0.0f;
+  __builtin_amdgcn_wave_barrier();
+  uint32_t base = 0;  // sparse entries written so far
+  for (int e0 = 0; e0 < E; e0 += 64) {
+    const int e = e0 + lane;
+    int p = -1;
+    float r = 0.0f;
+    bool live = false;
+    if (e < E) live = split_entry(A, (size_t)i * E + e, p, r);
+    const int sl = live ? slot[p] : -1;
+    if (sl >= 0) atomicAdd(&acc[sl], r);
+    const bool sparse = live && sl < 0;
+    const uint64_t m = __ballot(sparse);
+    const uint32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    if (sparse) {
+      spp[(size_t)i * E + base + before] = p;
+      spr[(size_t)i * E + base + before] = r;
+    }
+    base += (uint32_t)__popcll(m);
+  }
+  __builtin_amdgcn_wave_barrier();
+  // per-token power of two: |acc| * 2^-E < 2
+  float m = 0.0f;
+  for (int h = lane; h < kSplitHeavy; h += 64) m = fmaxf(m, fabsf(acc[h]));
+  const float mx = __builtin_bit_cast(float, wave_max(__builtin_bit_cast(uint32_t, m)));
+  const int ex = mx > 0.0f ? ilogbf(mx) : 0;
+  const float down = ldexpf(1.0f, -ex);
+  // lane l writes positions 8l .. 8l + 7 (heavy channels 4l .. 4l + 3)
+  uint32_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float v = acc[4 * lane + q] * down;
+    const _Float16 hi = (_Float16)v;
+    const _Float16 lo = (_Float16)(v - (float)hi);
+    w[q] = (uint32_t)__builtin_bit_cast(uint16_t, hi) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
+  }
+  reinterpret_cast<uint4_t*>(rh + (size_t)i * kSplitPos)[lane] = uint4_t{w[0], w[1], w[2], w[3]};
+  if (lane == 0) {
+    spc[i] = (int)base;
+    pow2[i] = ldexpf(1.0f, ex);
+  }
+}
+
+// Weight codes of the dense positions in the GEMM layout: word (q, j) holds
+// positions 8q .. 8q + 7 of column j, i.e. heavy channels 4q .. 4q + 3 each
+// twice (hi and lo); positions past the list get code 0 (their operand is 0).
+__global__ void __launch_bounds__(256) k_split_wgather(const uint32_t* __restrict__ idx_w,
+                                                       int d_out, const int* __restrict__ hlist,
+                                                       uint32_t* __restrict__ idxh) {
+  const int q = blockIdx.y;
+  const int nh = hlist[kSplitHeavy];
+  if (8 * q >= ((2 * nh + 63) / 64) * 64) return;  // beyond the blocks the kernel reads
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= d_out) return;
+  uint32_t word = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int c = hlist[4 * q + u];
+    uint32_t code = 0;
+    if (c >= 0) code = (idx_w[(size_t)(c >> 3) * d_out + j] >> (4 * (c & 7))) & 15u;
+    word |= (code | (code << 4)) << (8 * u);
+  }
+  idxh[(size_t)q * d_out + j] = word;
+}
+
+hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm, void* ws,
+                                   hipStream_t s) {
+  if (a.n == 0 || a.d_out == 0) return hipSuccess;
+  if (a.k == 0) {
+    if (a.accumulate) return hipSuccess;
+    return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
+  }
+  const SplitLayout L = split_layout(a.n, a.d_in, a.d_out, a.k);
+  char* base = static_cast<char*>(ws);
+  int* count = reinterpret_cast<int*>(base + L.count);
+  int* slot = reinterpret_cast<int*>(base + L.slot);
+  int* hlist = reinterpret_cast<int*>(base + L.hlist);
+  float* pow2 = reinterpret_cast<float*>(base + L.pow2);
+  uint16_t* rh = reinterpret_cast<uint16_t*>(base + L.rh);
+  uint32_t* idxh = reinterpret_cast<uint32_t*>(base + L.idxh);
+  int32_t* spp = reinterpret_cast<int32_t*>(base + L.spp);
+  float* spr = reinterpret_cast<float*>(base + L.spr);
+  int32_t* spc = reinterpret_cast<int32_t*>(base + L.spc);
+
+  hipError_t e = launch_fill_zero(reinterpret_cast<float*>(count), (size_t)a.d_in, s);
+  if (e != hipSuccess) return e;
+  const size_t tot = (size_t)a.n * 2 * a.k;
+  if (a.d_in <= kSplitLdsBins) {
+    // about 64 workgroups: each flushes at most d_in counts
+    const unsigned cblocks = (unsigned)std::min<size_t>((tot + 255) / 256, 64);
+    hipLaunchKernelGGL(k_split_count<true>, dim3(cblocks), dim3(256), 0, s, a, count);
+  } else {
+    const unsigned cblocks = (unsigned)std::min<size_t>((tot + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_split_count<false>, dim3(cblocks), dim3(256), 0, s, a, count);
+  }
+  const int thr = std::max(2, a.n / 8);
+  hipLaunchKernelGGL(k_split_select, dim3(1), dim3(1024), 0, s, a.d_in, thr, count, slot, hlist);
+  hipLaunchKernelGGL(k_split_rows, dim3(a.n), dim3(64), 0, s, a, slot, pow2, rh, spp, spr, spc);
+  hipLaunchKernelGGL(k_split_wgather, dim3((a.d_out + 255) / 256, kSplitPos / 8), dim3(256), 0, s,
+                     idx_w_gemm, a.d_out, hlist, idxh);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+
+  // dense part: y (+)= 2^E_i * s_j * sum_q R~[i][q] C_W[w(q, j)]
+  GemmArgs g{};
+  g.idx_act = reinterpret_cast<const uint8_t*>(rh);
+  g.act_scale = pow2;
+  g.n = a.n;
+  g.d_in = kSplitPos;
+  g.idx_w = idxh;
+  g.w_scale = a.w_scale;
+  g.d_out = a.d_out;
+  g.lut = a.lut;
+  g.b_a = 4;
+  g.b_w = a.b_w;
+  g.y = a.y;
+  g.accumulate = a.accumulate;
+  g.kdyn = hlist + kSplitHeavy;
+  g.a_row = 2 * kSplitPos;
+  if ((e = launch_gemm_values(g, s)) != hipSuccess) return e;
+
+  // the rest: y += Y' of the compacted lists
+  CompArgs c = a;
+  c.max_idx = spp;
+  c.min_idx = nullptr;
+  c.residual = spr;
+  c.cnt = spc;
+  c.accumulate = 1;
+  return launch_compensate_wr(c, s);
+}
+
+}  // namespace oasis

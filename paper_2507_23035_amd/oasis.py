@@ -28,7 +28,8 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_lut_gemm_compensated", "oasis_pack_weight_indices", "oasis_pack_weight_rows",
            "oasis_build_lut_quantize_act", "oasis_quantize_act_static",
            "oasis_build_lut_quantize_act_static", "oasis_lut_gemm_compensated_percol",
-           "oasis_lut_gemm_compensated_rows")
+           "oasis_lut_gemm_compensated_rows", "oasis_outlier_compensate_split",
+           "oasis_outlier_compensate_split_workspace")
 
 
 class OasisError(RuntimeError):
@@ -83,6 +84,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                       P, I, P]
     lib.oasis_outlier_compensate_rows.restype = I
     lib.oasis_outlier_compensate_rows.argtypes = [P, P, P, I, I, P, P, I, P, I, I, P, I, P]
+    S = ctypes.c_size_t
+    lib.oasis_outlier_compensate_split_workspace.restype = S
+    lib.oasis_outlier_compensate_split_workspace.argtypes = [I, I, I, I]
+    lib.oasis_outlier_compensate_split.restype = I
+    lib.oasis_outlier_compensate_split.argtypes = [P, P, P, I, I, P, P, P, I, P, I, I, P, I, P, S,
+                                                   P]
     lib.oasis_pack_weight_indices.restype = I
     lib.oasis_pack_weight_indices.argtypes = [P, I, I, P]
     lib.oasis_pack_weight_rows.restype = I
@@ -337,6 +344,34 @@ def outlier_compensate_rows(max_idx, min_idx, residual, idx_wr, lut, b_w: int, w
         _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
         _ptr(residual, "f32") if k else None, n, k, _ptr(idx_wr, "i32"), _ptr(lut, "u8"), b_w, _ptr(w_scale, "f32"), d_in,
         d_out, _ptr(y, "f32"), 1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def split_workspace_bytes(n: int, d_in: int, d_out: int, k: int) -> int:
+    """Bytes of device workspace outlier_compensate_split needs."""
+    return int(load().oasis_outlier_compensate_split_workspace(n, d_in, d_out, k))
+
+
+def outlier_compensate_split(max_idx, min_idx, residual, idx_w, idx_wr, lut, b_w: int, w_scale,
+                             d_in: int, y=None, accumulate: bool = True, workspace=None,
+                             stream=None):
+    """Outlier branch Y' split by channel: the heavy channels as a dense MFMA
+    contraction, the other entries from the row-layout codes (y += Y' with
+    accumulate, else y = Y').  workspace: a uint8 CUDA tensor of at least
+    split_workspace_bytes(...) bytes (allocated here when None)."""
+    import torch
+    n, k = max_idx.shape
+    d_out = w_scale.shape[0]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=max_idx.device)
+    need = split_workspace_bytes(n, d_in, d_out, k)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=max_idx.device)
+    _check("oasis_outlier_compensate_split", load().oasis_outlier_compensate_split(
+        _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
+        _ptr(residual, "f32") if k else None, n, k, _ptr(idx_w, "i32"), _ptr(idx_wr, "i32"),
+        _ptr(lut, "u8"), b_w, _ptr(w_scale, "f32"), d_in, d_out, _ptr(y, "f32"),
+        1 if accumulate else 0, _ptr(workspace, "u8"), workspace.numel(), _stream(stream)))
     return y
 
 

@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_status_strings(lib):
     assert lib.oasis_status_str(0) == b"ok"
-    for s in range(-9, 0):
+    for s in range(-10, 0):
         assert lib.oasis_status_str(s) != b"unknown status"
     assert lib.oasis_version().startswith(b"oasis")
 
@@ -253,3 +253,26 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError, match="CUDA"):
         oasis._ptr(t, "f32")
     assert oasis._ptr(None, "f32") is None
+
+
+def test_compensate_split_errors(lib):
+    c = lib.oasis_outlier_compensate_split
+    c.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int] * 2 + [ctypes.c_void_p] * 3 + \
+        [ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+         ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    wsz = lib.oasis_outlier_compensate_split_workspace
+    wsz.restype = ctypes.c_size_t
+    wsz.argtypes = [ctypes.c_int] * 4
+    need = wsz(4, 16, 8, 3)
+    assert need > 0 and wsz(4, 16, 8, 3) == need and wsz(-1, 16, 8, 3) == 0
+    ok = (P, P, P, 4, 3, P, P, P, 4, P, 16, 8, P, 1)
+    assert c(P, P, P, 4, 3, P, P, P, 4, P, 20, 8, P, 1, P, need, None) == -2
+    assert c(P, P, P, 4, 17, P, P, P, 4, P, 16, 8, P, 1, P, need, None) == -4
+    assert c(P, P, P, 4, 3, P, P, P, 5, P, 16, 8, P, 1, P, need, None) == -3
+    assert c(P, P, P, 4, 3, P, None, P, 4, P, 16, 8, P, 1, P, need, None) == -1   # idx_wr
+    assert c(P, P, P, 4, 3, MIS, P, P, 4, P, 16, 8, P, 1, P, need, None) == -6
+    assert c(*ok, None, need, None) == -10                       # no workspace
+    assert c(*ok, P + 16, need, None) == -10                     # not 256-byte aligned
+    assert c(*ok, P, need - 1, None) == -10                      # too small
+    assert c(P, P, P, 4, 3, P, P, P, 4, P, 65536, 65536, P, 1, P, 1 << 40, None) == -9
+    assert c(P, P, P, 0, 3, P, P, P, 4, P, 16, 8, P, 1, None, 0, None) == 0   # no tokens

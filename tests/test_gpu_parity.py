@@ -101,6 +101,21 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
                                        b_w, s_w, L.spec.d_in, accumulate=False)
     torch.cuda.synchronize()
     assert_close(yr.cpu().numpy()[rows], ref["y_comp"], "Y' (row layout)")
+    # split by channel (heavy channels on the matrix cores); the workspace is
+    # reused by a second call, poisoned in between
+    n, k_ = q["max_idx"].shape
+    ws = torch.empty(max(1, oasis.split_workspace_bytes(n, L.spec.d_in, L.spec.d_out, k_)),
+                     dtype=torch.uint8, device=dev())
+    ys = oasis.outlier_compensate_split(q["max_idx"], q["min_idx"], q["residual"], idx_w, idx_wr,
+                                        lut, b_w, s_w, L.spec.d_in, accumulate=False, workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(ys.cpu().numpy()[rows], ref["y_comp"], "Y' (split by channel)")
+    ws.fill_(0xA5)
+    ys2 = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
+    oasis.outlier_compensate_split(q["max_idx"], q["min_idx"], q["residual"], idx_w, idx_wr, lut,
+                                   b_w, s_w, L.spec.d_in, y=ys2, accumulate=True, workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(ys2.cpu().numpy()[rows], ref["y"], "Y (gemm then split compensation)")
     yf = oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut,
                                          b_a, b_w, q["max_idx"], q["min_idx"], q["residual"])
     torch.cuda.synchronize()
@@ -193,6 +208,8 @@ RAGGED = [
     (72, 1032, 260, 300, 4, 4, 14),  # row-grouped compensation: 6 tokens per tile
     (70, 4096, 96, 2048, 4, 4, 15),  # one token per tile
     (66, 4104, 40, 2050, 4, 4, 16),  # lists too long for a tile: per-token kernel
+    (64, 1024, 136, 256, 4, 4, 18),  # ~512 channels listed by every token: more heavy
+                                     # channels than the dense part takes (256)
 ]
 
 
