@@ -81,6 +81,9 @@ def call_bytes(n, d_in, d_out, k, path):
         # the row-layout copy of a listed channel, where the launch reads it,
         # duplicates codes the operation needs once: not counted
         "lut_gemm_compensated_rows": gemm_bytes(n, d_in, d_out, k, merge=False),
+        # the compacted lists' rows are part of comp; y written by the lists'
+        # kernel and merged by the GEMM
+        "lut_gemm_compensated_split": gemm_bytes(n, d_in, d_out) + comp - 4 * d_out,
         # + the columns' own codebooks (16 fp16 each)
         "lut_gemm_compensated_percol": gemm_bytes(n, d_in, d_out, k, merge=False) + 32 * d_out,
     }
@@ -95,6 +98,7 @@ KERNEL_SOURCES = {
     "outlier_compensate": ["compensate.hip", "split.hip", "lut_gemm.hip"],
     "lut_gemm": ["lut_gemm.hip"], "lut_gemm_compensated": ["lut_gemm.hip", "compensate.hip"],
     "lut_gemm_compensated_rows": ["lut_gemm.hip", "compensate.hip"],
+    "lut_gemm_compensated_split": ["lut_gemm.hip", "compensate.hip", "split.hip"],
     "lut_gemm_compensated_percol": ["lut_gemm.hip"],
 }
 
@@ -129,6 +133,7 @@ CALL_SYMBOLS = {   # kernel symbol fragment of each call's dominant kernel
     "detect_outliers": "k_quantize<", "outlier_compensate": "k_compensate",
     "lut_gemm": "k_gemm_mfma", "lut_gemm_compensated": "k_gemm_mfma",
     "lut_gemm_compensated_rows": "k_gemm_mfma",
+    "lut_gemm_compensated_split": "k_gemm_mfma",
     "lut_gemm_compensated_percol": "k_gemm_mfma",
 }
 
@@ -155,6 +160,7 @@ def summarize_pmc(root, workload, path):
     lines = [f"| call | kernel | dispatches | FETCH_SIZE | WRITE_SIZE | HBM bytes/launch |",
              "|---|---|---|---|---|---|"]
     names = {"fused": ["build_lut_quantize_act", "lut_gemm_compensated_rows"],
+             "split": ["build_lut_quantize_act", "lut_gemm"],
              "separate": ["build_lut_quantize_act", "outlier_compensate", "lut_gemm"],
              "lookahead": ["cluster_act", "detect_outliers", "lut_gemm",
                            "outlier_compensate"]}[path]
@@ -163,6 +169,8 @@ def summarize_pmc(root, workload, path):
         vals = {}
         for c, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
             rs = [r for r in _pmc_rows(os.path.join(root, sub), c) if sym in r["Kernel_Name"]]
+            if call == "lut_gemm":  # the main-branch kernel alone, not its variants with
+                rs = [r for r in rs if "true>" not in r["Kernel_Name"]]   # value blocks
             if call in ("cluster_act", "detect_outliers", "quantize_act",
                         "build_lut_quantize_act"):
                 want = {"cluster_act": "true, false", "detect_outliers": "false, true",
@@ -318,7 +326,10 @@ def run_workload(args, layer, weights, dev, side):
                      device=dev)
     path = args.path
     if path == "auto":
-        path = "fused" if ((n <= 32 or args.percol) and algo == oasis.ALGO_MFMA) else "separate"
+        if (n <= 32 or args.percol) and algo == oasis.ALGO_MFMA:
+            path = "fused"
+        else:
+            path = "split" if algo == oasis.ALGO_MFMA else "separate"
     # per-column codebooks (--percol): fp16 [d_out][16], entries past 2^b_w zero
     cols_dev = None
     if args.percol:
@@ -350,6 +361,9 @@ def run_workload(args, layer, weights, dev, side):
         "lut_gemm_compensated_rows": lambda c: oasis.lut_gemm_compensated_rows(
             q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c], s_w, lut, b_a, b_w, q["max_idx"],
             q["min_idx"], q["residual"], y=y),
+        "lut_gemm_compensated_split": lambda c: oasis.lut_gemm_compensated_split(
+            q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c], s_w, lut, b_a, b_w, q["max_idx"],
+            q["min_idx"], q["residual"], y=y, workspace=ws),
         "lut_gemm_compensated_percol": lambda c: oasis.lut_gemm_compensated_percol(
             q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, cols_dev, b_a, b_w, q["max_idx"],
             q["min_idx"], q["residual"], y=y),
@@ -370,6 +384,12 @@ def run_workload(args, layer, weights, dev, side):
             [gemm_name]
     elif path == "lookahead":
         names = ["build_lut", "cluster_act", "detect_outliers", "lut_gemm", "outlier_compensate"]
+        gemm_name = "lut_gemm"
+    elif path == "split":
+        # the step's two calls, then the main-branch GEMM and the split
+        # compensation each on their own (what the GEMM call's kernels cost)
+        names = (["build_lut_quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
+            ["lut_gemm_compensated_split", "lut_gemm", "outlier_compensate"]
         gemm_name = "lut_gemm"
     else:
         names = (["build_lut_quantize_act_static"] if thr else ["build_lut_quantize_act"]) + \
@@ -394,6 +414,11 @@ def run_workload(args, layer, weights, dev, side):
             # per layer), inside the quantize launch
             quantize(L)
             fused_gemm(c, L, q, y)
+        elif path == "split":
+            quantize(L)
+            oasis.lut_gemm_compensated_split(q["idx_act"], q["act_scale"], idx_w[c], idx_wr[c],
+                                             s_w, L, b_a, b_w, q["max_idx"], q["min_idx"],
+                                             q["residual"], y=y, workspace=ws)
         elif path == "lookahead":
             oasis.build_lut(cb_a, b_a, cb_w, b_w, out=L)
             # main branch and outlier detection run concurrently (Sec. III-C)
@@ -470,6 +495,11 @@ def run_workload(args, layer, weights, dev, side):
         oasis.quantize_act_static(x, lut, b_a, k, thr[0], thr[1], scale)
     if path == "fused":
         y_ref = fused_gemm(c_last, lut, q1)
+    elif path == "split":
+        y_ref = oasis.lut_gemm_compensated_split(q1["idx_act"], q1["act_scale"], idx_w[c_last],
+                                                 idx_wr[c_last], s_w, lut, b_a, b_w,
+                                                 q1["max_idx"], q1["min_idx"], q1["residual"],
+                                                 workspace=ws)
     else:
         if path == "lookahead":
             y_ref = oasis.lut_gemm(q1["idx_act"], q1["act_scale"], idx_w[c_last], s_w, lut, b_a,
@@ -578,9 +608,13 @@ def main():
                          "one launch per 32 tokens)")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: auto, >512 MiB)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graphs")
-    ap.add_argument("--path", default="auto", choices=["auto", "fused", "separate", "lookahead"],
-                    help="fused: one call for Y* + Y' (default for <= 32 tokens); lookahead: "
-                         "outlier detection on a second stream beside the main-branch GEMM")
+    ap.add_argument("--path", default="auto",
+                    choices=["auto", "fused", "split", "separate", "lookahead"],
+                    help="fused: one call for Y* + Y' (default for <= 32 tokens); split: the "
+                         "compensation split by channel, heavy channels inside the GEMM "
+                         "(default for more tokens); separate: split compensation, then the "
+                         "GEMM; lookahead: outlier detection on a second stream beside the "
+                         "main-branch GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",

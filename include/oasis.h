@@ -300,6 +300,32 @@ int oasis_outlier_compensate_split(const int32_t* max_idx, const int32_t* min_id
                                    hipStream_t stream);
 
 /*
+ * oasis_lut_gemm_compensated_split - main branch and compensation for many
+ * tokens with the heavy channels of oasis_outlier_compensate_split inside the
+ * GEMM: the compacted lists of the other entries are compensated first
+ * (y = or += their Y'), then the GEMM reduces over the activation codes and
+ * over the heavy channels' residuals divided by t_i (fp16 hi/lo pairs) in one
+ * pass, y += Y* + Y'.  A heavy channel whose residual over t_i is not below
+ * 2^15 (or whose token has t_i = 0) is compensated with the lists instead, so
+ * every scale mode gives Y = Y* + Y' of oasis_lut_gemm_compensated up to fp32
+ * summation order.
+ *   Arguments and results as oasis_lut_gemm_compensated_rows, plus the
+ *   workspace of oasis_outlier_compensate_split (the same size query,
+ *   oasis_outlier_compensate_split_workspace(n, d_in, d_out, k)).
+ *   n <= 32 tokens or k == 0: the call of oasis_lut_gemm_compensated_rows
+ *   (no workspace needed).  d_in not a multiple of 64: the split compensation
+ *   then the GEMM, two passes over y.
+ * Errors: NULL, SHAPE, BITS, K, ALIGN, TOO_LARGE, WORKSPACE, LAUNCH.
+ */
+int oasis_lut_gemm_compensated_split(const uint8_t* idx_act, const float* act_scale, int n,
+                                     int d_in, const uint32_t* idx_w, const uint32_t* idx_wr,
+                                     const float* w_scale, int d_out, const oasis_lut_block* lut,
+                                     int b_a, int b_w, const int32_t* max_idx,
+                                     const int32_t* min_idx, const float* residual, int k,
+                                     float* y, int accumulate, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
+/*
  * oasis_lut_gemm_compensated - main branch and outlier branch in one call
  * (look-ahead computation with error compensation, Sec. III-C):
  *   y (+)= Y* + Y', with Y* as in oasis_lut_gemm and Y' as in

@@ -371,6 +371,49 @@ static int gemm_compensated(const uint8_t* idx_act, const float* act_scale, int 
                          : oasis::launch_compensate(c, stream));
 }
 
+int oasis_lut_gemm_compensated_split(const uint8_t* idx_act, const float* act_scale, int n,
+                                     int d_in, const uint32_t* idx_w, const uint32_t* idx_wr,
+                                     const float* w_scale, int d_out, const oasis_lut_block* lut,
+                                     int b_a, int b_w, const int32_t* max_idx,
+                                     const int32_t* min_idx, const float* residual, int k,
+                                     float* y, int accumulate, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || (d_in % 8) != 0) return OASIS_ERR_SHAPE;
+  if (!bits_ok(b_a) || !bits_ok(b_w)) return OASIS_ERR_BITS;
+  if (k < 0 || k > d_in) return OASIS_ERR_K;
+  if (n == 0 || d_out == 0) return OASIS_OK;
+  if (!act_scale || !w_scale || !lut || !y || (d_in > 0 && (!idx_act || !idx_w)))
+    return OASIS_ERR_NULL;
+  if (k > 0 && (!max_idx || !min_idx || !residual || !idx_wr)) return OASIS_ERR_NULL;
+  if (!aligned(idx_act, 16) || !aligned(idx_w, 16) || !aligned(lut, 16) || !aligned(y, 4) ||
+      !aligned(act_scale, 4) || !aligned(w_scale, 4) || !aligned(max_idx, 4) ||
+      !aligned(min_idx, 4) || !aligned(residual, 4) || !aligned(idx_wr, 4))
+    return OASIS_ERR_ALIGN;
+  if (!offsets_fit(n, d_in, d_out)) return OASIS_ERR_TOO_LARGE;
+  if (idx_wr && (uint64_t)d_in * (uint64_t)((d_out + 7) / 8) * 4u >= (1ull << 31))
+    return OASIS_ERR_TOO_LARGE;
+  if (!offsets_fit(n, oasis::kSplitPos, d_out) ||
+      (uint64_t)(n + 1) * 2u * oasis::kSplitPos >= (1ull << 31))
+    return OASIS_ERR_TOO_LARGE;
+  // few tokens or no lists: the fused GEMV (or the GEMM alone), no workspace
+  if (n <= oasis::kFusedMaxTokens || k == 0 || d_in == 0)
+    return gemm_compensated(idx_act, act_scale, n, d_in, idx_w, idx_wr, w_scale, d_out, lut, b_a,
+                            b_w, max_idx, min_idx, residual, k, y, accumulate, stream);
+  if (!workspace || !aligned(workspace, 256) ||
+      workspace_bytes < oasis::split_layout(n, d_in, d_out, k).total)
+    return OASIS_ERR_WORKSPACE;
+  oasis::GemmArgs g{idx_act, act_scale, n, d_in, idx_w, w_scale, d_out, lut, b_a, b_w, y, 1,
+                    nullptr, nullptr, nullptr, 0, nullptr};
+  oasis::CompArgs c{max_idx, min_idx, residual, n, k, idx_wr, lut, b_w, w_scale, d_in, d_out, y,
+                    accumulate ? 1 : 0, nullptr};
+  if (d_in % 64 == 0)
+    return launched(oasis::launch_gemm_compensated_split(g, c, idx_w, workspace, stream));
+  // other reductions (the 16x16x32 kernel): split compensation, then the GEMM
+  hipError_t e = oasis::launch_compensate_split(c, idx_w, workspace, stream);
+  if (e != hipSuccess) return launched(e);
+  return launched(oasis::launch_gemm_mfma(g, stream));
+}
+
 int oasis_lut_gemm_compensated(const uint8_t* idx_act, const float* act_scale, int n, int d_in,
                                const uint32_t* idx_w, const float* w_scale, int d_out,
                                const oasis_lut_block* lut, int b_a, int b_w,

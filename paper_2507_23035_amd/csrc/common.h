@@ -146,6 +146,11 @@ struct GemmArgs {
   // positions (a length known on the device only)
   const int* kdyn;
   int a_row;  // bytes per row of that matrix
+  // optional (many-token kernel, codes): after the reduction over the codes,
+  // ceil(2 * *kdyn / 64) more blocks with the fp16 value operand hv ([n] rows
+  // of a_row bytes) and the weight codes hw (GEMM layout, kSplitPos / 8 rows)
+  const uint8_t* hv;
+  const uint32_t* hw;
 };
 
 struct CompArgs {
@@ -182,6 +187,12 @@ hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm
                                    hipStream_t s);
 // the dense part: the many-token MFMA kernel with an fp16 value operand
 hipError_t launch_gemm_values(const GemmArgs& a, hipStream_t s);
+// the many-token MFMA kernel over the codes, then the dense positions a.hv/a.hw
+hipError_t launch_gemm_heavy(const GemmArgs& a, hipStream_t s);
+// y (+)= Y* + Y' with the heavy channels inside the GEMM (g: n > 32, d_in % 64
+// == 0; a: the compensation's arguments, its idx_w in the row layout)
+hipError_t launch_gemm_compensated_split(const GemmArgs& g, const CompArgs& a,
+                                         const uint32_t* idx_w_gemm, void* ws, hipStream_t s);
 
 // Bytes of dynamic LDS the quantize kernel needs for a token of d_in values
 // and k outliers per side.

@@ -786,7 +786,9 @@ struct TileCodes {
                               // values: positions 8 (4h + s) .. + 7 of step s
 };
 
-template <int CW, int FT, int WX, int WY, bool BV>
+// HV: after the codes, the blocks of the value operand A.hv with the codes
+// A.hw (the heavy channels of the split compensation).
+template <int CW, int FT, int WX, int WY, bool BV, bool HV = false>
 __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
   __shared__ uint32_t tab[256 * 64];  // 64 KiB dual decode table
@@ -823,18 +825,22 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     aoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * arow + (BV ? 64u : 16u) * (uint32_t)h;
   const uint32_t wrow = d_out * 4u, wblk = 8u * d_out * 4u;
 
-  auto load = [&](int blk, TileCodes<CW, FT, BV>& tc) {
+  // codes (or values) of block blk from the descriptors rwx / rax at the
+  // per-lane offsets aoffx; the type of tc says which operand B is
+  auto load_from = [&](int blk, auto& tc, __amdgpu_buffer_rsrc_t rwx,
+                       __amdgpu_buffer_rsrc_t rax, const uint32_t (&aoffx)[FT]) {
+    constexpr bool VALS = sizeof(tc.a) / sizeof(tc.a[0]) == 4;
 #pragma unroll
     for (int f = 0; f < FT; ++f) {
-      if constexpr (BV) {
+      if constexpr (VALS) {
 #pragma unroll
         for (int st = 0; st < 4; ++st)
           tc.a[st][f] = __builtin_bit_cast(
               uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                           ra, (int)(aoff[f] + (uint32_t)blk * 128u + 16u * (uint32_t)st), 0, 0));
+                           rax, (int)(aoffx[f] + (uint32_t)blk * 128u + 16u * (uint32_t)st), 0, 0));
       } else {
         tc.a[0][f] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                     ra, (int)(aoff[f] + (uint32_t)blk * 32u), 0, 0));
+                                                     rax, (int)(aoffx[f] + (uint32_t)blk * 32u), 0, 0));
       }
     }
 #pragma unroll
@@ -842,8 +848,9 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
 #pragma unroll
       for (int c = 0; c < CW; ++c)
         tc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
-            rw, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
+            rwx, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
   };
+  auto load = [&](int blk, auto& tc) { load_from(blk, tc, rw, ra, aoff); };
 
   float16_t acc[CW][FT];
 #pragma unroll
@@ -855,13 +862,15 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
 
   const uint32_t l4w = (uint32_t)r32 * 4u, l4a = l4w + 128u;
   // operands of step st (every block is full: d_in is a multiple of 64)
-  auto operands = [&](const TileCodes<CW, FT, BV>& tc, int st, half8_t (&a)[CW],
-                      half8_t (&b)[FT]) {
+  auto operands = [&](const auto& tc, int st, half8_t (&a)[CW], half8_t (&b)[FT]) {
+    constexpr bool VALS = sizeof(tc.a) / sizeof(tc.a[0]) == 4;
 #pragma unroll
     for (int c = 0; c < CW; ++c) a[c] = expand_dual(tc.w[st][c], tb, l4w);
 #pragma unroll
-    for (int f = 0; f < FT; ++f)
-      b[f] = BV ? __builtin_bit_cast(half8_t, tc.a[st][f]) : expand_dual(tc.a[0][f][st], tb, l4a);
+    for (int f = 0; f < FT; ++f) {
+      if constexpr (VALS) b[f] = __builtin_bit_cast(half8_t, tc.a[st][f]);
+      else b[f] = expand_dual(tc.a[0][f][st], tb, l4a);
+    }
   };
   auto mma = [&](const half8_t (&a)[CW], const half8_t (&b)[FT]) {
 #pragma unroll
@@ -892,8 +901,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   // `cur` are refilled with block `refill` during the last step, once its
   // step 3 operands are expanded.
   half8_t a0[CW], b0[FT], a1[CW], b1[FT];
-  auto block = [&](const TileCodes<CW, FT, BV>& cur, const TileCodes<CW, FT, BV>& nxt,
-                   TileCodes<CW, FT, BV>& refill_into, int refill) {
+  auto block_with = [&](const auto& cur, const auto& nxt, auto& refill_into, int refill,
+                        auto&& loadfn) {
     operands(cur, 1, a1, b1);
     mma(a0, b0);
     interleave(false);
@@ -907,10 +916,13 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     interleave(false);
     __builtin_amdgcn_sched_barrier(0);
     operands(nxt, 0, a0, b0);
-    load(refill, refill_into);
+    loadfn(refill, refill_into);
     mma(a1, b1);
     interleave(true);
     __builtin_amdgcn_sched_barrier(0);
+  };
+  auto block = [&](const auto& cur, const auto& nxt, auto& refill_into, int refill) {
+    block_with(cur, nxt, refill_into, refill, load);
   };
 
   // ---- prologue: first two blocks' codes requested, then the table
@@ -937,6 +949,34 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     block(c1, c0, c1, blk + 3);
   }
   if (blk < nblk) block(c0, c1, c0, blk + 2);
+
+  if constexpr (HV) {
+    // the heavy channels of the split compensation: value operand A.hv,
+    // weight codes A.hw, ceil(2 nh / 64) blocks of 64 positions
+    const int nhb = (2 * __builtin_amdgcn_readfirstlane(*A.kdyn) + 63) / 64;
+    if (nhb > 0) {
+      const __amdgpu_buffer_rsrc_t rhw = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint32_t*>(A.hw), 0, (int)((uint32_t)(kSplitPos / 8) * d_out * 4u),
+          0x00020000);
+      const __amdgpu_buffer_rsrc_t rhv = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint8_t*>(A.hv), 0, (int)((uint32_t)A.n * (uint32_t)A.a_row), 0x00020000);
+      uint32_t hoff[FT];
+#pragma unroll
+      for (int f = 0; f < FT; ++f)
+        hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * (uint32_t)A.a_row + 64u * (uint32_t)h;
+      auto hload = [&](int b, auto& tc) { load_from(b, tc, rhw, rhv, hoff); };
+      TileCodes<CW, FT, true> h0, h1;
+      hload(0, h0);
+      hload(1, h1);
+      operands(h0, 0, a0, b0);
+      int hb = 0;
+      for (; hb + 1 < nhb; hb += 2) {
+        block_with(h0, h1, h0, hb + 2, hload);
+        block_with(h1, h0, h1, hb + 3, hload);
+      }
+      if (hb < nhb) block_with(h0, h1, h0, hb + 2, hload);
+    }
+  }
 
   // ---- epilogue: y (+)= t_i * s_j * acc, four consecutive columns per store
   const bool vec = (A.d_out & 3) == 0 && (reinterpret_cast<uintptr_t>(A.y) & 15u) == 0 &&
@@ -972,13 +1012,13 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   }
 }
 
-template <int CW, int FT, int WX, int WY, bool BV = false>
+template <int CW, int FT, int WX, int WY, bool BV = false, bool HV = false>
 static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   constexpr int TC = 32 * CW * WX, TT = 32 * FT * WY;
   const int ncx = (a.d_out + TC - 1) / TC;
   const int nty = (a.n + TT - 1) / TT;
-  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV>), dim3(ncx * nty), dim3(WX * WY * 64),
-                     0, s, a, ncx, nty);
+  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV, HV>), dim3(ncx * nty),
+                     dim3(WX * WY * 64), 0, s, a, ncx, nty);
   return hipGetLastError();
 }
 
@@ -994,10 +1034,15 @@ hipError_t launch_gemm_values(const GemmArgs& a, hipStream_t s) {
 // rounds of the 256 CUs, else 256 x 128 (waves of 128 x 64, two workgroups
 // and two waves per SIMD on a CU).  Needs d_in % 64 == 0 (whole blocks of 64
 // channels).
+template <bool HV = false>
 static hipError_t launch_gemm_tiles(const GemmArgs& a, hipStream_t s) {
   const long t44 = (long)((a.d_out + 255) / 256) * ((a.n + 255) / 256);
-  if (t44 >= 3 * 256) return launch_tile<4, 4, 2, 2>(a, s);
-  return launch_tile<4, 2, 2, 2>(a, s);
+  if (t44 >= 3 * 256) return launch_tile<4, 4, 2, 2, false, HV>(a, s);
+  return launch_tile<4, 2, 2, 2, false, HV>(a, s);
+}
+
+hipError_t launch_gemm_heavy(const GemmArgs& a, hipStream_t s) {
+  return launch_gemm_tiles<true>(a, s);
 }
 
 template <int CW, int TF, int WX, int WY>

@@ -119,27 +119,76 @@ __global__ void __launch_bounds__(1024) k_split_select(int d_in, int thr,
 // One wave per token: the token's heavy residuals summed per heavy channel
 // (in LDS, fp32), scaled and split into the fp16 hi/lo row of the dense
 // operand; the other live entries compacted in list order.
+//   tscale == nullptr: the dense part runs on its own and the token's scale
+//     is a power of two 2^E_i with |R 2^-E_i| < 2 (pow2[i] = 2^E_i).
+//   tscale != nullptr: the dense part joins the main-branch GEMM, whose
+//     epilogue multiplies by t_i, so the operand is R / t_i.  A channel whose
+//     R / t_i is not below 2^15 in magnitude (or whose token has t_i = 0 and
+//     R != 0) leaves the dense operand (0 there) and its entries join the
+//     compacted lists, so any scale mode stays exact.
 __global__ void __launch_bounds__(64) k_split_rows(CompArgs A, const int* __restrict__ slot,
+                                                   const float* __restrict__ tscale,
                                                    float* __restrict__ pow2,
                                                    uint16_t* __restrict__ rh,
                                                    int32_t* __restrict__ spp,
                                                    float* __restrict__ spr,
                                                    int32_t* __restrict__ spc) {
   __shared__ float acc[kSplitHeavy];
+  __shared__ int out[kSplitHeavy];  // heavy channel handled by the lists instead
   const int i = blockIdx.x, lane = threadIdx.x;
   const int E = 2 * A.k;
-  for (int h = lane; h < kSplitHeavy; h += 64) acc[h] = 0.0f;
+  for (int h = lane; h < kSplitHeavy; h += 64) {
+    acc[h] = 0.0f;
+    out[h] = 0;
+  }
   __builtin_amdgcn_wave_barrier();
-  uint32_t base = 0;  // sparse entries written so far
   for (int e0 = 0; e0 < E; e0 += 64) {
     const int e = e0 + lane;
     int p = -1;
     float r = 0.0f;
-    bool live = false;
-    if (e < E) live = split_entry(A, (size_t)i * E + e, p, r);
-    const int sl = live ? slot[p] : -1;
-    if (sl >= 0) atomicAdd(&acc[sl], r);
-    const bool sparse = live && sl < 0;
+    if (e < E && split_entry(A, (size_t)i * E + e, p, r)) {
+      const int sl = slot[p];
+      if (sl >= 0) atomicAdd(&acc[sl], r);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  float down;
+  if (tscale) {
+    const float t = tscale[i];
+    for (int h = lane; h < kSplitHeavy; h += 64) {
+      const float v = acc[h];
+      if (v == 0.0f) continue;
+      const float q = t > 0.0f ? v / t : INFINITY;
+      if (!(fabsf(q) < 32768.0f)) {
+        out[h] = 1;
+        acc[h] = 0.0f;
+      } else {
+        acc[h] = q;
+      }
+    }
+    down = 1.0f;
+  } else {
+    // per-token power of two: |acc| * 2^-E < 2
+    float m = 0.0f;
+    for (int h = lane; h < kSplitHeavy; h += 64) m = fmaxf(m, fabsf(acc[h]));
+    const float mx = __builtin_bit_cast(float, wave_max(__builtin_bit_cast(uint32_t, m)));
+    const int ex = mx > 0.0f ? ilogbf(mx) : 0;
+    down = ldexpf(1.0f, -ex);
+    if (lane == 0) pow2[i] = ldexpf(1.0f, ex);
+  }
+  __builtin_amdgcn_wave_barrier();
+  // the compacted lists: live entries of channels that are not heavy (or left
+  // the dense operand), in list order
+  uint32_t base = 0;
+  for (int e0 = 0; e0 < E; e0 += 64) {
+    const int e = e0 + lane;
+    int p = -1;
+    float r = 0.0f;
+    bool sparse = false;
+    if (e < E && split_entry(A, (size_t)i * E + e, p, r)) {
+      const int sl = slot[p];
+      sparse = sl < 0 || out[sl];
+    }
     const uint64_t m = __ballot(sparse);
     const uint32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -149,13 +198,6 @@ __global__ void __launch_bounds__(64) k_split_rows(CompArgs A, const int* __rest
     }
     base += (uint32_t)__popcll(m);
   }
-  __builtin_amdgcn_wave_barrier();
-  // per-token power of two: |acc| * 2^-E < 2
-  float m = 0.0f;
-  for (int h = lane; h < kSplitHeavy; h += 64) m = fmaxf(m, fabsf(acc[h]));
-  const float mx = __builtin_bit_cast(float, wave_max(__builtin_bit_cast(uint32_t, m)));
-  const int ex = mx > 0.0f ? ilogbf(mx) : 0;
-  const float down = ldexpf(1.0f, -ex);
   // lane l writes positions 8l .. 8l + 7 (heavy channels 4l .. 4l + 3)
   uint32_t w[4];
 #pragma unroll
@@ -167,10 +209,7 @@ __global__ void __launch_bounds__(64) k_split_rows(CompArgs A, const int* __rest
            ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
   }
   reinterpret_cast<uint4_t*>(rh + (size_t)i * kSplitPos)[lane] = uint4_t{w[0], w[1], w[2], w[3]};
-  if (lane == 0) {
-    spc[i] = (int)base;
-    pow2[i] = ldexpf(1.0f, ex);
-  }
+  if (lane == 0) spc[i] = (int)base;
 }
 
 // Weight codes of the dense positions in the GEMM layout: word (q, j) holds
@@ -195,13 +234,10 @@ __global__ void __launch_bounds__(256) k_split_wgather(const uint32_t* __restric
   idxh[(size_t)q * d_out + j] = word;
 }
 
-hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm, void* ws,
-                                   hipStream_t s) {
-  if (a.n == 0 || a.d_out == 0) return hipSuccess;
-  if (a.k == 0) {
-    if (a.accumulate) return hipSuccess;
-    return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
-  }
+// Heavy channels, dense operand rows, heavy weight codes and compacted lists
+// (tscale: see k_split_rows).
+static hipError_t split_prepass(const CompArgs& a, const uint32_t* idx_w_gemm, void* ws,
+                                const float* tscale, hipStream_t s) {
   const SplitLayout L = split_layout(a.n, a.d_in, a.d_out, a.k);
   char* base = static_cast<char*>(ws);
   int* count = reinterpret_cast<int*>(base + L.count);
@@ -227,10 +263,41 @@ hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm
   }
   const int thr = std::max(2, a.n / 8);
   hipLaunchKernelGGL(k_split_select, dim3(1), dim3(1024), 0, s, a.d_in, thr, count, slot, hlist);
-  hipLaunchKernelGGL(k_split_rows, dim3(a.n), dim3(64), 0, s, a, slot, pow2, rh, spp, spr, spc);
+  hipLaunchKernelGGL(k_split_rows, dim3(a.n), dim3(64), 0, s, a, slot, tscale, pow2, rh, spp,
+                     spr, spc);
   hipLaunchKernelGGL(k_split_wgather, dim3((a.d_out + 255) / 256, kSplitPos / 8), dim3(256), 0, s,
                      idx_w_gemm, a.d_out, hlist, idxh);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+// The compacted lists of the workspace as the row-layout kernel's lists.
+static CompArgs sparse_args(const CompArgs& a, void* ws, int accumulate) {
+  const SplitLayout L = split_layout(a.n, a.d_in, a.d_out, a.k);
+  char* base = static_cast<char*>(ws);
+  CompArgs c = a;
+  c.max_idx = reinterpret_cast<const int32_t*>(base + L.spp);
+  c.min_idx = nullptr;
+  c.residual = reinterpret_cast<const float*>(base + L.spr);
+  c.cnt = reinterpret_cast<const int32_t*>(base + L.spc);
+  c.accumulate = accumulate;
+  return c;
+}
+
+hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm, void* ws,
+                                   hipStream_t s) {
+  if (a.n == 0 || a.d_out == 0) return hipSuccess;
+  if (a.k == 0) {
+    if (a.accumulate) return hipSuccess;
+    return launch_fill_zero(a.y, (size_t)a.n * a.d_out, s);
+  }
+  hipError_t e = split_prepass(a, idx_w_gemm, ws, nullptr, s);
+  if (e != hipSuccess) return e;
+  const SplitLayout L = split_layout(a.n, a.d_in, a.d_out, a.k);
+  char* base = static_cast<char*>(ws);
+  int* hlist = reinterpret_cast<int*>(base + L.hlist);
+  float* pow2 = reinterpret_cast<float*>(base + L.pow2);
+  uint16_t* rh = reinterpret_cast<uint16_t*>(base + L.rh);
+  uint32_t* idxh = reinterpret_cast<uint32_t*>(base + L.idxh);
 
   // dense part: y (+)= 2^E_i * s_j * sum_q R~[i][q] C_W[w(q, j)]
   GemmArgs g{};
@@ -251,13 +318,27 @@ hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm
   if ((e = launch_gemm_values(g, s)) != hipSuccess) return e;
 
   // the rest: y += Y' of the compacted lists
-  CompArgs c = a;
-  c.max_idx = spp;
-  c.min_idx = nullptr;
-  c.residual = spr;
-  c.cnt = spc;
-  c.accumulate = 1;
-  return launch_compensate_wr(c, s);
+  return launch_compensate_wr(sparse_args(a, ws, 1), s);
+}
+
+// Main branch and compensation with the heavy channels inside the GEMM: the
+// compacted lists first (y (+)= their Y'), then the GEMM over the codes and
+// the dense positions (y += Y* + Y' of the heavy channels).  g: the main
+// GEMM's arguments (n > 32 tokens, d_in % 64 == 0).
+hipError_t launch_gemm_compensated_split(const GemmArgs& g, const CompArgs& a,
+                                         const uint32_t* idx_w_gemm, void* ws, hipStream_t s) {
+  hipError_t e = split_prepass(a, idx_w_gemm, ws, g.act_scale, s);
+  if (e != hipSuccess) return e;
+  if ((e = launch_compensate_wr(sparse_args(a, ws, a.accumulate), s)) != hipSuccess) return e;
+  const SplitLayout L = split_layout(a.n, a.d_in, a.d_out, a.k);
+  char* base = static_cast<char*>(ws);
+  GemmArgs m = g;
+  m.accumulate = 1;
+  m.kdyn = reinterpret_cast<const int*>(base + L.hlist) + kSplitHeavy;
+  m.hv = reinterpret_cast<const uint8_t*>(base + L.rh);
+  m.hw = reinterpret_cast<const uint32_t*>(base + L.idxh);
+  m.a_row = 2 * kSplitPos;
+  return launch_gemm_heavy(m, s);
 }
 
 }  // namespace oasis

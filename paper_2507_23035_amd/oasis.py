@@ -29,7 +29,7 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_build_lut_quantize_act", "oasis_quantize_act_static",
            "oasis_build_lut_quantize_act_static", "oasis_lut_gemm_compensated_percol",
            "oasis_lut_gemm_compensated_rows", "oasis_outlier_compensate_split",
-           "oasis_outlier_compensate_split_workspace")
+           "oasis_outlier_compensate_split_workspace", "oasis_lut_gemm_compensated_split")
 
 
 class OasisError(RuntimeError):
@@ -90,6 +90,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_outlier_compensate_split.restype = I
     lib.oasis_outlier_compensate_split.argtypes = [P, P, P, I, I, P, P, P, I, P, I, I, P, I, P, S,
                                                    P]
+    lib.oasis_lut_gemm_compensated_split.restype = I
+    lib.oasis_lut_gemm_compensated_split.argtypes = [P, P, I, I, P, P, P, I, P, I, I, P, P, P, I,
+                                                     P, I, P, S, P]
     lib.oasis_pack_weight_indices.restype = I
     lib.oasis_pack_weight_indices.argtypes = [P, I, I, P]
     lib.oasis_pack_weight_rows.restype = I
@@ -408,6 +411,32 @@ def lut_gemm_compensated_rows(idx_act, act_scale, idx_w, idx_wr, w_scale, lut, b
         _ptr(w_scale, "f32"), d_out, _ptr(lut, "u8"), b_a, b_w, _ptr(max_idx, "i32") if k else None,
         _ptr(min_idx, "i32") if k else None, _ptr(residual, "f32") if k else None, k, _ptr(y, "f32"),
         1 if accumulate else 0, _stream(stream)))
+    return y
+
+
+def lut_gemm_compensated_split(idx_act, act_scale, idx_w, idx_wr, w_scale, lut, b_a: int,
+                               b_w: int, max_idx, min_idx, residual, y=None,
+                               accumulate: bool = False, workspace=None, stream=None):
+    """Main branch plus compensation for many tokens, the heavy channels of the
+    split compensation inside the GEMM (y (+)= Y* + Y').  workspace: a uint8
+    CUDA tensor of at least split_workspace_bytes(...) bytes (allocated here
+    when None)."""
+    import torch
+    n = idx_act.shape[0]
+    d_in = idx_act.shape[1] * 2
+    d_out = idx_w.shape[1]
+    k = max_idx.shape[1]
+    if y is None:
+        y = torch.empty((n, d_out), dtype=torch.float32, device=idx_act.device)
+    if workspace is None:
+        workspace = torch.empty(max(1, split_workspace_bytes(n, d_in, d_out, k)),
+                                dtype=torch.uint8, device=idx_act.device)
+    _check("oasis_lut_gemm_compensated_split", load().oasis_lut_gemm_compensated_split(
+        _ptr(idx_act, "u8"), _ptr(act_scale, "f32"), n, d_in, _ptr(idx_w, "i32"),
+        _ptr(idx_wr, "i32") if k else None, _ptr(w_scale, "f32"), d_out, _ptr(lut, "u8"), b_a,
+        b_w, _ptr(max_idx, "i32") if k else None, _ptr(min_idx, "i32") if k else None,
+        _ptr(residual, "f32") if k else None, k, _ptr(y, "f32"), 1 if accumulate else 0,
+        _ptr(workspace, "u8"), workspace.numel(), _stream(stream)))
     return y
 
 

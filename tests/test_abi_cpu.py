@@ -276,3 +276,22 @@ def test_compensate_split_errors(lib):
     assert c(*ok, P, need - 1, None) == -10                      # too small
     assert c(P, P, P, 4, 3, P, P, P, 4, P, 65536, 65536, P, 1, P, 1 << 40, None) == -9
     assert c(P, P, P, 0, 3, P, P, P, 4, P, 16, 8, P, 1, None, 0, None) == 0   # no tokens
+
+
+def test_gemm_compensated_split_errors(lib):
+    g = lib.oasis_lut_gemm_compensated_split
+    g.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                  ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                  ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
+                  ctypes.c_void_p]
+    assert g(P, P, 40, 12, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P, 1 << 20, None) == -2
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 5, P, P, P, 2, P, 0, P, 1 << 20, None) == -3
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 65, P, 0, P, 1 << 20, None) == -4
+    assert g(P, P, 40, 64, P, None, P, 8, P, 4, 4, P, P, P, 2, P, 0, P, 1 << 20, None) == -1
+    assert g(P, P, 40, 64, MIS, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P, 1 << 20, None) == -6
+    # many tokens with lists: the workspace is required, 256-byte aligned, large enough
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, None, 1 << 20, None) == -10
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P + 16, 1 << 20, None) == -10
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P, 64, None) == -10
+    assert g(P, P, 0, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, None, 0, None) == 0

@@ -110,6 +110,20 @@ def run_full(L, algos=(oasis.ALGO_MFMA, oasis.ALGO_LUT), scale_mode=oasis.SCALE_
                                         lut, b_w, s_w, L.spec.d_in, accumulate=False, workspace=ws)
     torch.cuda.synchronize()
     assert_close(ys.cpu().numpy()[rows], ref["y_comp"], "Y' (split by channel)")
+    # heavy channels inside the GEMM (one call for y = Y* + Y'), then again
+    # accumulating into a preset y with the same (poisoned) workspace
+    yg = oasis.lut_gemm_compensated_split(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut,
+                                          b_a, b_w, q["max_idx"], q["min_idx"], q["residual"],
+                                          workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(yg.cpu().numpy()[rows], ref["y"], "Y (GEMM with the heavy channels, split)")
+    ws.fill_(0x5A)
+    yg.fill_(0.5)
+    oasis.lut_gemm_compensated_split(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut, b_a,
+                                     b_w, q["max_idx"], q["min_idx"], q["residual"], y=yg,
+                                     accumulate=True, workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(yg.cpu().numpy()[rows] - 0.5, ref["y"], "Y (split in the GEMM, accumulate)")
     ws.fill_(0xA5)
     ys2 = oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w, s_w, lut, b_a, b_w, algos[0])
     oasis.outlier_compensate_split(q["max_idx"], q["min_idx"], q["residual"], idx_w, idx_wr, lut,
@@ -216,6 +230,20 @@ RAGGED = [
 @pytest.mark.parametrize("n,d_in,d_out,k,b_a,b_w,seed", RAGGED)
 def test_ragged_shapes(n, d_in, d_out, k, b_a, b_w, seed):
     run_full(synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed, b_a=b_a, b_w=b_w)))
+
+
+def test_split_heavy_channels_out_of_range():
+    """Scale mode NONE (t = 1) with a channel of +-40000 in every token: its
+    residual over t cannot be an fp16 hi/lo pair below 2^15, so the GEMM with
+    the heavy channels must hand it to the lists; 64 tokens (the many-token
+    path), d_in a multiple of 64 (the heavy phase inside the GEMM)."""
+    L = synth.make_layer(synth.custom(64, 256, 136, 4, seed=19, dist="normal",
+                                      outlier_count=3, outlier_scale=6.0))
+    x = L.x.copy()
+    x[:, 7] = np.float16(40000.0)
+    x[::2, 9] = np.float16(-40000.0)
+    L.x = x
+    run_full(L, scale_mode=oasis.SCALE_NONE)
 
 
 def test_scale_mode_none():
