@@ -326,6 +326,27 @@ int oasis_lut_gemm_compensated_split(const uint8_t* idx_act, const float* act_sc
                                      size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * oasis_lut_gemm_compensated_split_noalloc - oasis_lut_gemm_compensated_split
+ * for callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the workspace is a static
+ * device array of 32 MiB inside the library (one per GPU, held until the
+ * process ends); the call allocates nothing.  Every call on one GPU shares
+ * that array, so calls that overlap on a GPU (other streams, other threads)
+ * race; stream-ordered calls do not.
+ *   Arguments, results and errors as oasis_lut_gemm_compensated_split without
+ *   the workspace; TOO_LARGE when the workspace the call needs
+ *   (oasis_outlier_compensate_split_workspace) exceeds 32 MiB.
+ */
+int oasis_lut_gemm_compensated_split_noalloc(const uint8_t* idx_act, const float* act_scale,
+                                             int n, int d_in, const uint32_t* idx_w,
+                                             const uint32_t* idx_wr, const float* w_scale,
+                                             int d_out, const oasis_lut_block* lut, int b_a,
+                                             int b_w, const int32_t* max_idx,
+                                             const int32_t* min_idx, const float* residual,
+                                             int k, float* y, int accumulate,
+                                             hipStream_t stream);
+
+/*
  * oasis_lut_gemm_compensated - main branch and outlier branch in one call
  * (look-ahead computation with error compensation, Sec. III-C):
  *   y (+)= Y* + Y', with Y* as in oasis_lut_gemm and Y' as in

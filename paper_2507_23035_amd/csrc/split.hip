@@ -20,6 +20,7 @@
 // nonzero residual, channel in range), the first kSplitHeavy of them in
 // channel order.  Which channels are heavy changes only the summation order.
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 
@@ -341,4 +342,51 @@ hipError_t launch_gemm_compensated_split(const GemmArgs& g, const CompArgs& a,
   return launch_gemm_heavy(m, s);
 }
 
+// ----------------------------------------------------------------------------
+// The same call without a caller workspace, for callers that cannot allocate
+// (HIP graph capture, tight serving loops): the scratch is a file-scope device
+// array of kScratchBytes that every GPU the library runs on holds until the
+// process ends.  Its device address (per device, taken with that device
+// current on the first call there) is what the kernels receive; the array's
+// name in host code is only a stand-in for it.  Every call on one GPU shares
+// the array: calls that overlap on a GPU race.  What must start at zero (the
+// channel counts) is cleared by a fill kernel in every call.
+// ----------------------------------------------------------------------------
+constexpr size_t kScratchBytes = 32u << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's copy of `scratch` (nullptr on error).
+void* scratch_address() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
 }  // namespace oasis
+
+extern "C" int oasis_lut_gemm_compensated_split_noalloc(
+    const uint8_t* idx_act, const float* act_scale, int n, int d_in, const uint32_t* idx_w,
+    const uint32_t* idx_wr, const float* w_scale, int d_out, const oasis_lut_block* lut, int b_a,
+    int b_w, const int32_t* max_idx, const int32_t* min_idx, const float* residual, int k,
+    float* y, int accumulate, hipStream_t stream) {
+  if (n < 0 || d_in < 0 || d_out < 0 || k < 0) return OASIS_ERR_SHAPE;
+  if ((size_t)oasis_outlier_compensate_split_workspace(n, d_in, d_out, k) > oasis::kScratchBytes)
+    return OASIS_ERR_TOO_LARGE;
+  void* ws = oasis::scratch_address();
+  if (!ws) return OASIS_ERR_LAUNCH;
+  return oasis_lut_gemm_compensated_split(idx_act, act_scale, n, d_in, idx_w, idx_wr, w_scale,
+                                          d_out, lut, b_a, b_w, max_idx, min_idx, residual, k, y,
+                                          accumulate, ws, oasis::kScratchBytes, stream);
+}

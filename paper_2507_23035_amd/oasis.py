@@ -29,7 +29,8 @@ EXPORTS = ("oasis_status_str", "oasis_version", "oasis_build_lut", "oasis_quanti
            "oasis_build_lut_quantize_act", "oasis_quantize_act_static",
            "oasis_build_lut_quantize_act_static", "oasis_lut_gemm_compensated_percol",
            "oasis_lut_gemm_compensated_rows", "oasis_outlier_compensate_split",
-           "oasis_outlier_compensate_split_workspace", "oasis_lut_gemm_compensated_split")
+           "oasis_outlier_compensate_split_workspace", "oasis_lut_gemm_compensated_split",
+           "oasis_lut_gemm_compensated_split_noalloc")
 
 
 class OasisError(RuntimeError):
@@ -93,6 +94,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.oasis_lut_gemm_compensated_split.restype = I
     lib.oasis_lut_gemm_compensated_split.argtypes = [P, P, I, I, P, P, P, I, P, I, I, P, P, P, I,
                                                      P, I, P, S, P]
+    lib.oasis_lut_gemm_compensated_split_noalloc.restype = I
+    lib.oasis_lut_gemm_compensated_split_noalloc.argtypes = [P, P, I, I, P, P, P, I, P, I, I, P,
+                                                             P, P, I, P, I, P]
     lib.oasis_pack_weight_indices.restype = I
     lib.oasis_pack_weight_indices.argtypes = [P, I, I, P]
     lib.oasis_pack_weight_rows.restype = I
