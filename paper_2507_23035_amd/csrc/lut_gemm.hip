@@ -1060,7 +1060,7 @@ static void launch_prefill(const GemmArgs& a, hipStream_t s) {
 template <int CW, int TF, int NW, int B, bool ROWS, bool PERCOL = false>
 static void launch_gemv_b(const GemmArgs& a, hipStream_t s) {
   const int ntiles = (a.d_out + 16 * CW - 1) / (16 * CW);
-  constexpr int PF = 2;  // blocks in flight per wave
+  constexpr int PF = 2;  // blocks in flight per wave (four measured slower)
   if ((a.d_in / 8) % 16 == 0)
     hipLaunchKernelGGL((k_gemm_mfma_gemv<CW, TF, NW, PF, true, B, ROWS, PERCOL>), dim3(ntiles),
                        dim3(NW * 64), 0, s, a, ntiles);

@@ -15,10 +15,16 @@ def token_variants(x):
     return [x, -x, x[::-1], np.roll(x, 3, axis=1)]
 
 
-@pytest.mark.parametrize("schedule", ["fused", "fused_percol", "separate", "lookahead"])
+@pytest.mark.parametrize("schedule", ["fused", "fused_percol", "separate", "lookahead", "split",
+                                      "split_noalloc"])
 def test_graph_replays_match_eager(schedule):
     name = "decode_8x4096x4096" if schedule.startswith("fused") else None
-    spec = synth.config(name) if name else synth.custom(70, 1032, 300, 20, seed=71)
+    if name:
+        spec = synth.config(name)
+    elif schedule.startswith("split"):   # d_in a multiple of 64: heavy channels in the GEMM
+        spec = synth.custom(70, 1024, 300, 20, seed=72)
+    else:
+        spec = synth.custom(70, 1032, 300, 20, seed=71)
     L = synth.make_layer(spec)
     s = L.spec
     print(f"case graph {schedule} n={s.n} d_in={s.d_in} d_out={s.d_out} k={s.k}", flush=True)
@@ -35,6 +41,9 @@ def test_graph_replays_match_eager(schedule):
     lut, q = oasis.build_lut_quantize_act(L.cb_a, s.b_a, L.cb_w, s.b_w, x, s.k)
     y = torch.empty((s.n, s.d_out), dtype=torch.float32, device=dev)
     side = torch.cuda.Stream()
+    ws = torch.empty(oasis.split_workspace_bytes(s.n, s.d_in, s.d_out, s.k), dtype=torch.uint8,
+                     device=dev)
+    lib = oasis.load()
 
     def step():
         if schedule == "lookahead":
@@ -54,6 +63,18 @@ def test_graph_replays_match_eager(schedule):
             oasis.lut_gemm_compensated_rows(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut,
                                             s.b_a, s.b_w, q["max_idx"], q["min_idx"],
                                             q["residual"], y=y)
+        elif schedule == "split":
+            oasis.lut_gemm_compensated_split(q["idx_act"], q["act_scale"], idx_w, idx_wr, s_w, lut,
+                                             s.b_a, s.b_w, q["max_idx"], q["min_idx"],
+                                             q["residual"], y=y, workspace=ws)
+        elif schedule == "split_noalloc":
+            st = lib.oasis_lut_gemm_compensated_split_noalloc(
+                q["idx_act"].data_ptr(), q["act_scale"].data_ptr(), s.n, s.d_in,
+                idx_w.data_ptr(), idx_wr.data_ptr(), s_w.data_ptr(), s.d_out, lut.data_ptr(),
+                s.b_a, s.b_w, q["max_idx"].data_ptr(), q["min_idx"].data_ptr(),
+                q["residual"].data_ptr(), s.k, y.data_ptr(), 0,
+                torch.cuda.current_stream().cuda_stream)
+            assert st == 0
         elif schedule == "fused_percol":
             oasis.lut_gemm_compensated_percol(q["idx_act"], q["act_scale"], idx_w, s_w, lut, cols,
                                               s.b_a, s.b_w, q["max_idx"], q["min_idx"],
