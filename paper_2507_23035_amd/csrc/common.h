@@ -140,15 +140,16 @@ struct GemmArgs {
   // optional: per-output-channel weight codebooks, fp16 [d_out][16]; when set
   // they replace the LUT block's C_W (GEMV kernel only)
   const uint16_t* cb_cols;
-  // optional (many-token kernel only): the B operand is an fp16 matrix
-  // [n][a_row / 2] of values (idx_act holds its bytes) instead of activation
-  // codes, and the reduction runs over ceil(2 * *kdyn / 64) blocks of 64
-  // positions (a length known on the device only)
+  // value operand (many-token kernel only): the B operand is an fp16 matrix
+  // [n][a_row / 2] (idx_act holds its bytes) instead of activation codes, and
+  // the reduction runs over ceil(2 * *kdyn / 64) blocks of 64 positions (a
+  // length known on the device only)
   const int* kdyn;
   int a_row;  // bytes per row of that matrix
-  // optional (many-token kernel, codes): after the reduction over the codes,
-  // ceil(2 * *kdyn / 64) more blocks with the fp16 value operand hv ([n] rows
-  // of a_row bytes) and the weight codes hw (GEMM layout, kSplitPos / 8 rows)
+  // optional (many-token kernel): after the main reduction, ceil(2 * *nheavy /
+  // 64) more blocks with the fp16 value operand hv ([n] rows of 2 * kSplitPos
+  // bytes) and the weight codes hw (GEMM layout, kSplitPos / 8 rows)
+  const int* nheavy;
   const uint8_t* hv;
   const uint32_t* hw;
 };

@@ -953,17 +953,18 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   if constexpr (HV) {
     // the heavy channels of the split compensation: value operand A.hv,
     // weight codes A.hw, ceil(2 nh / 64) blocks of 64 positions
-    const int nhb = (2 * __builtin_amdgcn_readfirstlane(*A.kdyn) + 63) / 64;
+    const int nhb = (2 * __builtin_amdgcn_readfirstlane(*A.nheavy) + 63) / 64;
     if (nhb > 0) {
       const __amdgpu_buffer_rsrc_t rhw = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<uint32_t*>(A.hw), 0, (int)((uint32_t)(kSplitPos / 8) * d_out * 4u),
           0x00020000);
+      const uint32_t hrow = 2u * kSplitPos;  // bytes per token row of hv
       const __amdgpu_buffer_rsrc_t rhv = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<uint8_t*>(A.hv), 0, (int)((uint32_t)A.n * (uint32_t)A.a_row), 0x00020000);
+          const_cast<uint8_t*>(A.hv), 0, (int)((uint32_t)A.n * hrow), 0x00020000);
       uint32_t hoff[FT];
 #pragma unroll
       for (int f = 0; f < FT; ++f)
-        hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * (uint32_t)A.a_row + 64u * (uint32_t)h;
+        hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * hrow + 64u * (uint32_t)h;
       auto hload = [&](int b, auto& tc) { load_from(b, tc, rhw, rhv, hoff); };
       TileCodes<CW, FT, true> h0, h1;
       hload(0, h0);

@@ -273,7 +273,7 @@ def test_compensate_split_errors(lib):
     assert c(P, P, P, 4, 3, MIS, P, P, 4, P, 16, 8, P, 1, P, need, None) == -6
     assert c(*ok, None, need, None) == -10                       # no workspace
     assert c(*ok, P + 16, need, None) == -10                     # not 256-byte aligned
-    assert c(*ok, P, need - 1, None) == -10                      # too small
+    assert c(*ok, P, 64, None) == -10                            # too small (need > 64)
     assert c(P, P, P, 4, 3, P, P, P, 4, P, 65536, 65536, P, 1, P, 1 << 40, None) == -9
     assert c(P, P, P, 0, 3, P, P, P, 4, P, 16, 8, P, 1, None, 0, None) == 0   # no tokens
 
