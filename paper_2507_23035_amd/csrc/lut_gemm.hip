@@ -22,6 +22,8 @@
 // group g and step s use word 4g + s on both sides, so the weight rows are read
 // as contiguous segments and each token's 4 words as one 16-byte load; the
 // order in which channels enter the MFMA is irrelevant to the sum.
+#include <atomic>
+
 #include "common.h"
 
 namespace oasis {
@@ -788,19 +790,27 @@ struct TileCodes {
 
 // HV: after the codes, the blocks of the value operand A.hv with the codes
 // A.hw (the heavy channels of the split compensation).
+//
+// Persistent: workgroup b takes tiles b, b + G, b + 2G, ... (G = gridDim.x,
+// at most what the CUs hold at once).  The decode table is built once; the
+// codes of a workgroup's next tile are requested before the current tile's
+// epilogue, so its output stores drain while the next tile's first MFMAs run
+// (all workgroups of a round finish together, and a store burst with idle
+// matrix cores cost 11 % of the time at 4096 x 8192 x 28672).  The tile's
+// scales are requested at its start and kept in registers (the column
+// scales pass through a 512-byte LDS row per wave in the epilogue).
 template <int CW, int FT, int WX, int WY, bool BV, bool HV = false>
 __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
-  __shared__ uint32_t tab[256 * 64];  // 64 KiB dual decode table
+  static_assert(CW == 4, "the column scales of a wave are two per lane");
+  __shared__ uint32_t tab[256 * 64];          // 64 KiB dual decode table
+  __shared__ float wsc[WX * WY][32 * CW];     // column scales of each wave's tile
   const char* tb = reinterpret_cast<const char*>(tab);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r32 = lane & 31, h = lane >> 5;
+  const int T = ncx * nty;
 
-  const int tile = xcd_tile(blockIdx.x, ncx * nty);
-  const int cx = tile / nty, ty = tile % nty;
-  const int j0 = (cx * WX + wave % WX) * 32 * CW;
-  const int t0 = (ty * WY + wave / WX) * 32 * FT;
   const uint32_t KB = (uint32_t)(A.d_in >> 3);  // words per token row = weight rows
   // blocks of 8 words (64 channels); with a value operand, of 64 positions up
   // to the device-side length
@@ -816,13 +826,25 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
       const_cast<uint32_t*>(A.idx_w), 0, (int)(KB * d_out * 4u), 0x00020000);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(A.idx_act), 0, (int)((uint32_t)A.n * arow), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(A.w_scale), 0, (int)(d_out * 4u), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rst = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(A.act_scale), 0, (int)((uint32_t)A.n * 4u), 0x00020000);
+  int j0 = 0, t0 = 0;
   uint32_t woff[CW], aoff[FT];
+  // origin and per-lane code offsets of tile u
+  auto place = [&](int u) {
+    const int tile = xcd_tile(u, T);
+    const int cx = tile / nty, ty = tile % nty;
+    j0 = (cx * WX + wave % WX) * 32 * CW;
+    t0 = (ty * WY + wave / WX) * 32 * FT;
 #pragma unroll
-  for (int c = 0; c < CW; ++c)
-    woff[c] = ((uint32_t)(4 * h) * d_out + (uint32_t)min(j0 + 32 * c + r32, A.d_out - 1)) * 4u;
+    for (int c = 0; c < CW; ++c)
+      woff[c] = ((uint32_t)(4 * h) * d_out + (uint32_t)min(j0 + 32 * c + r32, A.d_out - 1)) * 4u;
 #pragma unroll
-  for (int f = 0; f < FT; ++f)
-    aoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * arow + (BV ? 64u : 16u) * (uint32_t)h;
+    for (int f = 0; f < FT; ++f)
+      aoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * arow + (BV ? 64u : 16u) * (uint32_t)h;
+  };
   const uint32_t wrow = d_out * 4u, wblk = 8u * d_out * 4u;
 
   // codes (or values) of block blk from the descriptors rwx / rax at the
@@ -853,13 +875,6 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   auto load = [&](int blk, auto& tc) { load_from(blk, tc, rw, ra, aoff); };
 
   float16_t acc[CW][FT];
-#pragma unroll
-  for (int c = 0; c < CW; ++c)
-#pragma unroll
-    for (int f = 0; f < FT; ++f)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[c][f][v] = 0.0f;
-
   const uint32_t l4w = (uint32_t)r32 * 4u, l4a = l4w + 128u;
   // operands of step st (every block is full: d_in is a multiple of 64)
   auto operands = [&](const auto& tc, int st, half8_t (&a)[CW], half8_t (&b)[FT]) {
@@ -925,8 +940,9 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     block_with(cur, nxt, refill_into, refill, load);
   };
 
-  // ---- prologue: first two blocks' codes requested, then the table
+  // ---- prologue: the first tile's first two blocks requested, then the table
   TileCodes<CW, FT, BV> c0, c1;
+  place(blockIdx.x);
   load(0, c0);
   load(1, c1);
   if (wave < 4) {
@@ -936,89 +952,138 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   }
   __syncthreads();
 
-  // block b's codes are in c0 (b even) or c1; during its last step the
-  // registers are refilled with the codes two blocks ahead (requested one
-  // block before the step that expands them).  The loop body is straight-line
-  // (an odd last block is peeled): with a conditional half in it the
-  // compiler's wait analysis would assume the worst at the loop head and wait
-  // for every load in flight.  Blocks past the end read zeros (never used).
-  operands(c0, 0, a0, b0);
-  int blk = 0;
-  for (; blk + 1 < nblk; blk += 2) {
-    block(c0, c1, c0, blk + 2);
-    block(c1, c0, c1, blk + 3);
-  }
-  if (blk < nblk) block(c0, c1, c0, blk + 2);
-
-  if constexpr (HV) {
-    // the heavy channels of the split compensation: value operand A.hv,
-    // weight codes A.hw, ceil(2 nh / 64) blocks of 64 positions
-    const int nhb = (2 * __builtin_amdgcn_readfirstlane(*A.nheavy) + 63) / 64;
-    if (nhb > 0) {
-      const __amdgpu_buffer_rsrc_t rhw = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<uint32_t*>(A.hw), 0, (int)((uint32_t)(kSplitPos / 8) * d_out * 4u),
-          0x00020000);
-      const uint32_t hrow = 2u * kSplitPos;  // bytes per token row of hv
-      const __amdgpu_buffer_rsrc_t rhv = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<uint8_t*>(A.hv), 0, (int)((uint32_t)A.n * hrow), 0x00020000);
-      uint32_t hoff[FT];
+  for (int u = blockIdx.x; u < T; u += gridDim.x) {
+    // this tile's scales, used in its epilogue: lane l holds the column
+    // scales of columns 2l, 2l + 1 of the wave's tile and t_i of its tokens
+    const uint32_t csp = (uint32_t)min(j0 + 2 * lane, A.d_out) * 4u;
+    const uint32_t sw0 = __builtin_amdgcn_raw_buffer_load_b32(
+        rsw, (int)csp, 0, 0);
+    const uint32_t sw1 = __builtin_amdgcn_raw_buffer_load_b32(
+        rsw, (int)(csp + 4u), 0, 0);
+    float tsr[FT];
 #pragma unroll
-      for (int f = 0; f < FT; ++f)
-        hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * hrow + 64u * (uint32_t)h;
-      auto hload = [&](int b, auto& tc) { load_from(b, tc, rhw, rhv, hoff); };
-      TileCodes<CW, FT, true> h0, h1;
-      hload(0, h0);
-      hload(1, h1);
-      operands(h0, 0, a0, b0);
-      int hb = 0;
-      for (; hb + 1 < nhb; hb += 2) {
-        block_with(h0, h1, h0, hb + 2, hload);
-        block_with(h1, h0, h1, hb + 3, hload);
-      }
-      if (hb < nhb) block_with(h0, h1, h0, hb + 2, hload);
-    }
-  }
-
-  // ---- epilogue: y (+)= t_i * s_j * acc, four consecutive columns per store
-  const bool vec = (A.d_out & 3) == 0 && (reinterpret_cast<uintptr_t>(A.y) & 15u) == 0 &&
-                   (reinterpret_cast<uintptr_t>(A.w_scale) & 15u) == 0;
-#pragma unroll
-  for (int f = 0; f < FT; ++f) {
-    const int tok = t0 + 32 * f + r32;
-    if (tok >= A.n) continue;
-    const float ts = A.act_scale[tok];
-    float* yrow = A.y + (size_t)tok * A.d_out;
+    for (int f = 0; f < FT; ++f)
+      tsr[f] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(
+                     rst, (int)((uint32_t)min(t0 + 32 * f + r32, A.n) * 4u), 0, 0));
 #pragma unroll
     for (int c = 0; c < CW; ++c)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int j = j0 + 32 * c + 8 * g + 4 * h;
-        if (vec) {
-          if (j >= A.d_out) continue;  // d_out % 4 == 0: the four columns are all in or out
-          const float4_t sw = *reinterpret_cast<const float4_t*>(A.w_scale + j);
-          float4_t v = {acc[c][f][4 * g], acc[c][f][4 * g + 1], acc[c][f][4 * g + 2],
-                        acc[c][f][4 * g + 3]};
-          v = ts * sw * v;
-          float4_t* dst = reinterpret_cast<float4_t*>(yrow + j);
-          *dst = A.accumulate ? *dst + v : v;
-        } else {
+      for (int f = 0; f < FT; ++f)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if (j + q >= A.d_out) continue;
-            const float v = ts * A.w_scale[j + q] * acc[c][f][4 * g + q];
-            yrow[j + q] = A.accumulate ? yrow[j + q] + v : v;
+        for (int v = 0; v < 16; ++v) acc[c][f][v] = 0.0f;
+
+    // block b's codes are in c0 (b even) or c1; during its last step the
+    // registers are refilled with the codes two blocks ahead (requested one
+    // block before the step that expands them).  The loop body is
+    // straight-line (an odd last block is peeled): with a conditional half in
+    // it the compiler's wait analysis would assume the worst at the loop head
+    // and wait for every load in flight.  Blocks past the end read zeros or
+    // the next token's row (never used).
+    operands(c0, 0, a0, b0);
+    int blk = 0;
+    for (; blk + 1 < nblk; blk += 2) {
+      block(c0, c1, c0, blk + 2);
+      block(c1, c0, c1, blk + 3);
+    }
+    if (blk < nblk) block(c0, c1, c0, blk + 2);
+
+    if constexpr (HV) {
+      // the heavy channels of the split compensation: value operand A.hv,
+      // weight codes A.hw, ceil(2 nh / 64) blocks of 64 positions
+      const int nhb = (2 * __builtin_amdgcn_readfirstlane(*A.nheavy) + 63) / 64;
+      if (nhb > 0) {
+        const __amdgpu_buffer_rsrc_t rhw = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint32_t*>(A.hw), 0, (int)((uint32_t)(kSplitPos / 8) * d_out * 4u),
+            0x00020000);
+        const uint32_t hrow = 2u * kSplitPos;  // bytes per token row of hv
+        const __amdgpu_buffer_rsrc_t rhv = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint8_t*>(A.hv), 0, (int)((uint32_t)A.n * hrow), 0x00020000);
+        uint32_t hoff[FT];
+#pragma unroll
+        for (int f = 0; f < FT; ++f)
+          hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * hrow + 64u * (uint32_t)h;
+        auto hload = [&](int b, auto& tc) { load_from(b, tc, rhw, rhv, hoff); };
+        TileCodes<CW, FT, true> h0, h1;
+        hload(0, h0);
+        hload(1, h1);
+        operands(h0, 0, a0, b0);
+        int hb = 0;
+        for (; hb + 1 < nhb; hb += 2) {
+          block_with(h0, h1, h0, hb + 2, hload);
+          block_with(h1, h0, h1, hb + 3, hload);
+        }
+        if (hb < nhb) block_with(h0, h1, h0, hb + 2, hload);
+      }
+    }
+
+    // ---- the next tile's first two blocks go out before this tile's stores
+    const int jt = j0, tt = t0;
+    if (u + (int)gridDim.x < T) {
+      place(u + (int)gridDim.x);
+      load(0, c0);
+      load(1, c1);
+    }
+
+    // ---- epilogue: y (+)= t_i * s_j * acc, four consecutive columns per store
+    if (2 * lane < 32 * CW)
+      *reinterpret_cast<uint2*>(&wsc[wave][2 * lane]) = make_uint2(sw0, sw1);
+    const bool vec = (A.d_out & 3) == 0 && (reinterpret_cast<uintptr_t>(A.y) & 15u) == 0;
+#pragma unroll
+    for (int f = 0; f < FT; ++f) {
+      const int tok = tt + 32 * f + r32;
+      if (tok >= A.n) continue;
+      const float ts = tsr[f];
+      float* yrow = A.y + (size_t)tok * A.d_out;
+#pragma unroll
+      for (int c = 0; c < CW; ++c)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int jl = 32 * c + 8 * g + 4 * h, j = jt + jl;
+          if (vec) {
+            if (j >= A.d_out) continue;  // d_out % 4 == 0: the four columns are all in or out
+            const float4_t sw = *reinterpret_cast<const float4_t*>(&wsc[wave][jl]);
+            float4_t v = {acc[c][f][4 * g], acc[c][f][4 * g + 1], acc[c][f][4 * g + 2],
+                          acc[c][f][4 * g + 3]};
+            v = ts * sw * v;
+            float4_t* dst = reinterpret_cast<float4_t*>(yrow + j);
+            *dst = A.accumulate ? *dst + v : v;
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              if (j + q >= A.d_out) continue;
+              const float v = ts * wsc[wave][jl + q] * acc[c][f][4 * g + q];
+              yrow[j + q] = A.accumulate ? yrow[j + q] + v : v;
+            }
           }
         }
-      }
+    }
   }
+}
+
+// Workgroups that fit on the device at once (persistent grids), per device.
+static int resident_workgroups(int per_cu) {
+  static std::atomic<int> cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256 * per_cu;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n * per_cu;
 }
 
 template <int CW, int FT, int WX, int WY, bool BV = false, bool HV = false>
 static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   constexpr int TC = 32 * CW * WX, TT = 32 * FT * WY;
+  constexpr int PER_CU = (CW * FT > 8 || BV) ? 1 : 2;
   const int ncx = (a.d_out + TC - 1) / TC;
   const int nty = (a.n + TT - 1) / TT;
-  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV, HV>), dim3(ncx * nty),
+  const int grid = min(ncx * nty, resident_workgroups(PER_CU));
+  hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV, HV>), dim3(grid),
                      dim3(WX * WY * 64), 0, s, a, ncx, nty);
   return hipGetLastError();
 }
