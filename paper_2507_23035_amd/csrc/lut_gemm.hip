@@ -799,12 +799,26 @@ struct TileCodes {
 // matrix cores cost 11 % of the time at 4096 x 8192 x 28672).  The tile's
 // scales are requested at its start and kept in registers (the column
 // scales pass through a 512-byte LDS row per wave in the epilogue).
-template <int CW, int FT, int WX, int WY, bool BV, bool HV = false>
+//
+// QL (one workgroup per CU, d_in a multiple of 512): the activation codes
+// pass through LDS.  A token's codes for 4 blocks are 128 contiguous bytes;
+// loaded straight into LDS (buffer_load_dwordx4 ... lds, full 128-byte
+// pieces of 8 rows per instruction) they cost a quarter of the L2 requests
+// of per-lane 16-byte loads, which touch 32 rows x 32 bytes each.  Two
+// buffers of 4 blocks (quads) per token group; the waves of a group each
+// load half of its rows, so one barrier per quad publishes a quad (after
+// each wave's own wait for its copies).  16-byte chunk c of row R sits at
+// chunk c ^ ((R >> 1) & 7): the 16 lanes of a ds_read_b128 then hit 16
+// distinct bank groups.
+template <int CW, int FT, int WX, int WY, bool BV, bool HV = false, bool QL = false>
 __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
   static_assert(CW == 4, "the column scales of a wave are two per lane");
+  static_assert(!QL || (!BV && WX == 2 && FT == 4), "quad staging: 128 rows per group, 2 loaders");
   __shared__ uint32_t tab[256 * 64];          // 64 KiB dual decode table
   __shared__ float wsc[WX * WY][32 * CW];     // column scales of each wave's tile
+  constexpr int QB = QL ? WY * 32 * FT * 128 : 16;  // bytes of one quad buffer
+  __shared__ __align__(16) unsigned char actq0[QB], actq1[QB];
   const char* tb = reinterpret_cast<const char*>(tab);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -832,6 +846,23 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
       const_cast<float*>(A.act_scale), 0, (int)((uint32_t)A.n * 4u), 0x00020000);
   int j0 = 0, t0 = 0;
   uint32_t woff[CW], aoff[FT];
+  // QL: byte offsets of this lane's 16-byte pieces of the quad copies (8 per
+  // wave: rows 64 gx + 8 i + lane / 8 of the group), for this tile and the
+  // workgroup's next one
+  constexpr int NDMA = QL ? 8 : 1;
+  uint32_t dcur[NDMA], dnext[NDMA];
+  auto dma_offsets = [&](int u, uint32_t (&d)[NDMA]) {
+    if constexpr (QL) {
+      const int tile = xcd_tile(min(u, T - 1), T);
+      const int tg = ((tile % nty) * WY + wave / WX) * 32 * FT;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int R = 64 * (wave % WX) + 8 * i + (lane >> 3);
+        const uint32_t c = (uint32_t)(lane & 7) ^ (uint32_t)((R >> 1) & 7);
+        d[i] = (uint32_t)min(tg + R, A.n - 1) * arow + 16u * c;
+      }
+    }
+  };
   // origin and per-lane code offsets of tile u
   auto place = [&](int u) {
     const int tile = xcd_tile(u, T);
@@ -844,6 +875,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
 #pragma unroll
     for (int f = 0; f < FT; ++f)
       aoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * arow + (BV ? 64u : 16u) * (uint32_t)h;
+    dma_offsets(u, dcur);
+    dma_offsets(u + (int)gridDim.x, dnext);
   };
   const uint32_t wrow = d_out * 4u, wblk = 8u * d_out * 4u;
 
@@ -873,6 +906,42 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
             rwx, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
   };
   auto load = [&](int blk, auto& tc) { load_from(blk, tc, rw, ra, aoff); };
+  // QL: the weight words of block blk only
+  auto wload = [&](int blk, auto& tc) {
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int c = 0; c < CW; ++c)
+        tc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
+            rw, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
+  };
+  // QL: copy a quad (8 pieces per lane, at offsets d + qoff) into buffer q
+  const uint32_t gbase = (uint32_t)(wave / WX) * (uint32_t)(32 * FT * 128);
+  auto dma = [&](unsigned char* q, const uint32_t (&d)[NDMA], uint32_t qoff) {
+    if constexpr (QL) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            ra, (__attribute__((address_space(3))) void*)(q + gbase + (64u * (uint32_t)(wave % WX) + 8u * (uint32_t)i) * 128u),
+            16, (int)(d[i] + qoff), 0, 0, 0);
+    }
+  };
+  // QL: lane (r, h) reads chunk 2 bq + h of rows 32 f + r of its group
+  const uint32_t xr = (uint32_t)((r32 >> 1) & 7);
+  const uint32_t rbase = gbase + (uint32_t)r32 * 128u;
+  auto aload = [&](const unsigned char* q, int bq, auto& tc) {
+    const uint32_t co = (((uint32_t)(2 * bq + h)) ^ xr) * 16u;
+#pragma unroll
+    for (int f = 0; f < FT; ++f)
+      tc.a[0][f] = *reinterpret_cast<const uint4_t*>(q + rbase + co + 4096u * (uint32_t)f);
+  };
+  // QL: wait for this wave's quad copies (everything but the last block's 16
+  // weight loads), then for every wave's
+  auto publish = [&]() {
+    // s_waitcnt vmcnt(16): vmcnt bits [3:0] = 0 and [15:14] = 1, expcnt 7, lgkmcnt 15
+    __builtin_amdgcn_s_waitcnt(0x4F70);
+    __builtin_amdgcn_s_barrier();
+  };
 
   float16_t acc[CW][FT];
   const uint32_t l4w = (uint32_t)r32 * 4u, l4a = l4w + 128u;
@@ -943,14 +1012,25 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   // ---- prologue: the first tile's first two blocks requested, then the table
   TileCodes<CW, FT, BV> c0, c1;
   place(blockIdx.x);
-  load(0, c0);
-  load(1, c1);
+  if constexpr (QL) {
+    dma(actq0, dcur, 0u);
+    wload(0, c0);
+    wload(1, c1);
+  } else {
+    load(0, c0);
+    load(1, c1);
+  }
   if (wave < 4) {
     DualTableLoader dt;
     dt.load(A.lut, (uint32_t)wave);
     dt.store(tab, (uint32_t)wave, lane);
   }
+  if constexpr (QL) __builtin_amdgcn_s_waitcnt(0);  // this wave's quad copies
   __syncthreads();
+  if constexpr (QL) {
+    aload(actq0, 0, c0);
+    aload(actq0, 1, c1);
+  }
 
   for (int u = blockIdx.x; u < T; u += gridDim.x) {
     // this tile's scales, used in its epilogue: lane l holds the column
@@ -981,12 +1061,44 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     // and wait for every load in flight.  Blocks past the end read zeros or
     // the next token's row (never used).
     operands(c0, 0, a0, b0);
-    int blk = 0;
-    for (; blk + 1 < nblk; blk += 2) {
-      block(c0, c1, c0, blk + 2);
-      block(c1, c0, c1, blk + 3);
+    if constexpr (QL) {
+      // two quads per iteration: quad m in actq0, m + 1 in actq1; the copy
+      // of quad m + 2 goes to actq0 once quad m is read - in the last
+      // iteration the next tile's quad 0, so the next tile starts on it
+      const int nq = nblk >> 2;  // even
+      for (int m = 0; m < nq; m += 2) {
+        const int b = 4 * m;
+        auto ld = [&](const unsigned char* q, int bq) {
+          return [&, q, bq](int blk, auto& tc) {
+            wload(blk, tc);
+            aload(q, bq, tc);
+          };
+        };
+        dma(actq1, dcur, (uint32_t)(m + 1) * 128u);
+        block_with(c0, c1, c0, b + 2, ld(actq0, 2));
+        block_with(c1, c0, c1, b + 3, ld(actq0, 3));
+        publish();
+        block_with(c0, c1, c0, b + 4, ld(actq1, 0));
+        block_with(c1, c0, c1, b + 5, ld(actq1, 1));
+        const bool last = m + 2 >= nq;
+        uint32_t dq[NDMA];
+#pragma unroll
+        for (int i = 0; i < NDMA; ++i) dq[i] = last ? dnext[i] : dcur[i] + (uint32_t)(m + 2) * 128u;
+        dma(actq0, dq, 0u);
+        block_with(c0, c1, c0, b + 6, ld(actq1, 2));
+        block_with(c1, c0, c1, b + 7, ld(actq1, 3));
+        publish();
+        block_with(c0, c1, c0, b + 8, ld(actq0, 0));
+        block_with(c1, c0, c1, b + 9, ld(actq0, 1));
+      }
+    } else {
+      int blk = 0;
+      for (; blk + 1 < nblk; blk += 2) {
+        block(c0, c1, c0, blk + 2);
+        block(c1, c0, c1, blk + 3);
+      }
+      if (blk < nblk) block(c0, c1, c0, blk + 2);
     }
-    if (blk < nblk) block(c0, c1, c0, blk + 2);
 
     if constexpr (HV) {
       // the heavy channels of the split compensation: value operand A.hv,
@@ -1021,8 +1133,15 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     const int jt = j0, tt = t0;
     if (u + (int)gridDim.x < T) {
       place(u + (int)gridDim.x);
-      load(0, c0);
-      load(1, c1);
+      if constexpr (QL) {  // its quad 0 is in actq0 (published in the last iteration)
+        wload(0, c0);
+        wload(1, c1);
+        aload(actq0, 0, c0);
+        aload(actq0, 1, c1);
+      } else {
+        load(0, c0);
+        load(1, c1);
+      }
     }
 
     // ---- epilogue: y (+)= t_i * s_j * acc, four consecutive columns per store
@@ -1083,6 +1202,13 @@ static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   const int ncx = (a.d_out + TC - 1) / TC;
   const int nty = (a.n + TT - 1) / TT;
   const int grid = min(ncx * nty, resident_workgroups(PER_CU));
+  if constexpr (!BV && FT == 4 && WX == 2) {
+    if (a.d_in % 512 == 0) {
+      hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV, HV, true>), dim3(grid),
+                         dim3(WX * WY * 64), 0, s, a, ncx, nty);
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV, HV>), dim3(grid),
                      dim3(WX * WY * 64), 0, s, a, ncx, nty);
   return hipGetLastError();
