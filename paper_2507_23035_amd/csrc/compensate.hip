@@ -411,14 +411,18 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   const int tend = min(A.n, tok0 + tt);
   const int ntw = tw < tend ? (tend - tw + 3) / 4 : 0;
   // units per token: the whole list, or with compacted lists the token's own
-  // entries (at least one unit: a token's last unit writes y).  Lane j < ntw
-  // holds the first unit past token tw + 4j (inclusive prefix sum); units are
-  // numbered over the wave's tokens in order.
+  // entries (at least one unit when y is overwritten: a token's last unit
+  // writes y; none for a token without entries when adding into y).  Lane
+  // j < ntw holds the first unit past token tw + 4j (inclusive prefix sum);
+  // units are numbered over the wave's tokens in order.
   const int nch = (E + WR_U - 1) / WR_U;
   int nu = 0;
   if (lane < ntw) {
     nu = nch;
-    if (A.cnt) nu = max(1, (min(max(A.cnt[tw + 4 * lane], 0), E) + WR_U - 1) / WR_U);
+    if (A.cnt) {
+      nu = (min(max(A.cnt[tw + 4 * lane], 0), E) + WR_U - 1) / WR_U;
+      if (!A.accumulate) nu = max(1, nu);
+    }
   }
   const int uend = (int)wave_incl_scan((uint32_t)nu);
   const int U = __builtin_amdgcn_readlane(uend, 63);
@@ -527,7 +531,17 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   float acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
+  // adding into y: the token's y words are requested at its first unit and
+  // used at its last (a load right before the store would wait for memory)
+  float4 yv[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
   auto consume = [&](int u, float rl, const uint32_t (&w)[WR_U]) {
+    int slot_j, ubeg;
+    unit_token(u, slot_j, ubeg);
+    if (A.accumulate && vec && u == ubeg) {
+      const float4* s4 = reinterpret_cast<const float4*>(A.y + (size_t)(tw + 4 * slot_j) * d_out + 8u * m);
+      yv[0] = s4[0];
+      yv[1] = s4[1];
+    }
     // a unit without a live entry (the unused places of OASIS-S lists sit at
     // the end of each list) adds nothing: skip its products
     if (__ballot(rl != 0.0f) != 0) {
@@ -545,8 +559,6 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
         }
       }
     }
-    int slot_j, ubeg;
-    unit_token(u, slot_j, ubeg);
     if (u != __builtin_amdgcn_readlane(uend, slot_j) - 1) return;
     // the token's last unit: y (+)= s_j * acc
     const int i = tw + 4 * slot_j;
@@ -558,11 +570,10 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
         float4 o = make_float4(sw[4 * h] * acc[4 * h], sw[4 * h + 1] * acc[4 * h + 1],
                                sw[4 * h + 2] * acc[4 * h + 2], sw[4 * h + 3] * acc[4 * h + 3]);
         if (A.accumulate) {
-          const float4 y0 = d4[h];
-          o.x += y0.x;
-          o.y += y0.y;
-          o.z += y0.z;
-          o.w += y0.w;
+          o.x += yv[h].x;
+          o.y += yv[h].y;
+          o.z += yv[h].z;
+          o.w += yv[h].w;
         }
         d4[h] = o;
       }

@@ -809,7 +809,10 @@ struct TileCodes {
 // load half of its rows, so one barrier per quad publishes a quad (after
 // each wave's own wait for its copies).  16-byte chunk c of row R sits at
 // chunk c ^ ((R >> 1) & 7): the 16 lanes of a ds_read_b128 then hit 16
-// distinct bank groups.
+// distinct bank groups.  With the activation words read from LDS one block
+// ahead, the weight words are requested three blocks ahead (four slots):
+// with one block of lead the table lookups waited for them (a variant whose
+// lookups did not depend on the loaded words ran 15 % faster).
 template <int CW, int FT, int WX, int WY, bool BV, bool HV = false, bool QL = false>
 __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
@@ -906,15 +909,6 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
             rwx, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
   };
   auto load = [&](int blk, auto& tc) { load_from(blk, tc, rw, ra, aoff); };
-  // QL: the weight words of block blk only
-  auto wload = [&](int blk, auto& tc) {
-#pragma unroll
-    for (int st = 0; st < 4; ++st)
-#pragma unroll
-      for (int c = 0; c < CW; ++c)
-        tc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
-            rw, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
-  };
   // QL: copy a quad (8 pieces per lane, at offsets d + qoff) into buffer q
   const uint32_t gbase = (uint32_t)(wave / WX) * (uint32_t)(32 * FT * 128);
   auto dma = [&](unsigned char* q, const uint32_t (&d)[NDMA], uint32_t qoff) {
@@ -926,21 +920,36 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
             16, (int)(d[i] + qoff), 0, 0, 0);
     }
   };
-  // QL: lane (r, h) reads chunk 2 bq + h of rows 32 f + r of its group
+  // QL: lane (r, h) reads chunk 2 bq + h of rows 32 f + r of its group (aload4)
   const uint32_t xr = (uint32_t)((r32 >> 1) & 7);
   const uint32_t rbase = gbase + (uint32_t)r32 * 128u;
-  auto aload = [&](const unsigned char* q, int bq, auto& tc) {
+  // QL: wait for this wave's quad copy (issued four blocks of weight loads
+  // ago; the last two blocks' 32 loads may stay in flight), then for every
+  // wave's
+  auto publish = [&]() {
+    // s_waitcnt vmcnt(32): vmcnt bits [3:0] = 0 and [15:14] = 2, expcnt 7, lgkmcnt 15
+    __builtin_amdgcn_s_waitcnt(0x8F70);
+    __builtin_amdgcn_s_barrier();
+  };
+  struct WCodes {
+    uint32_t w[4][CW];  // weight word 4h + s of column group c
+  };
+  struct ACodes {
+    uint4_t a[FT];  // words 4h .. 4h + 3 of token group f
+  };
+  auto wload4 = [&](int blk, WCodes& wc) {
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int c = 0; c < CW; ++c)
+        wc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
+            rw, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
+  };
+  auto aload4 = [&](const unsigned char* q, int bq, ACodes& ac) {
     const uint32_t co = (((uint32_t)(2 * bq + h)) ^ xr) * 16u;
 #pragma unroll
     for (int f = 0; f < FT; ++f)
-      tc.a[0][f] = *reinterpret_cast<const uint4_t*>(q + rbase + co + 4096u * (uint32_t)f);
-  };
-  // QL: wait for this wave's quad copies (everything but the last block's 16
-  // weight loads), then for every wave's
-  auto publish = [&]() {
-    // s_waitcnt vmcnt(16): vmcnt bits [3:0] = 0 and [15:14] = 1, expcnt 7, lgkmcnt 15
-    __builtin_amdgcn_s_waitcnt(0x4F70);
-    __builtin_amdgcn_s_barrier();
+      ac.a[f] = *reinterpret_cast<const uint4_t*>(q + rbase + co + 4096u * (uint32_t)f);
   };
 
   float16_t acc[CW][FT];
@@ -1008,14 +1017,64 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   auto block = [&](const auto& cur, const auto& nxt, auto& refill_into, int refill) {
     block_with(cur, nxt, refill_into, refill, load);
   };
+  // QL: operands of step st from a weight slot and an activation slot
+  auto qoperands = [&](const WCodes& wc, const ACodes& ac, int st, half8_t (&a)[CW],
+                       half8_t (&b)[FT]) {
+#pragma unroll
+    for (int c = 0; c < CW; ++c) a[c] = expand_dual(wc.w[st][c], tb, l4w);
+#pragma unroll
+    for (int f = 0; f < FT; ++f) b[f] = expand_dual(ac.a[f][st], tb, l4a);
+  };
+  // QL: one block on (wc, ac); in the last step the next block's activation
+  // words are read from quad buffer qn (chunk pair bqn) into an, its step 0
+  // operands expanded from (wn, an) and slot wr refilled with the weights of
+  // block rblk.  The words are read right before the weight-operand lookups
+  // of that expansion: LDS operations retire in order and a wait can leave at
+  // most 15 of them in flight, so words read earlier would make that wait
+  // drain the lookups issued after them.
+  auto qblock = [&](const WCodes& wc, const ACodes& ac, const WCodes& wn, ACodes& an,
+                    const unsigned char* qn, int bqn, WCodes& wr, int rblk) {
+    qoperands(wc, ac, 1, a1, b1);
+    mma(a0, b0);
+    interleave(false);
+    __builtin_amdgcn_sched_barrier(0);
+    qoperands(wc, ac, 2, a0, b0);
+    mma(a1, b1);
+    interleave(false);
+    __builtin_amdgcn_sched_barrier(0);
+    qoperands(wc, ac, 3, a1, b1);
+    mma(a0, b0);
+    interleave(false);
+    __builtin_amdgcn_sched_barrier(0);
+    aload4(qn, bqn, an);
+    qoperands(wn, an, 0, a0, b0);
+    wload4(rblk, wr);
+    mma(a1, b1);
+    interleave(true);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // QL: quad Q of this tile, or from nq on the workgroup's next tile
+  auto dma_quad = [&](unsigned char* q, int Q, int nq) {
+    uint32_t dq[NDMA];
+    const bool nxt = Q >= nq;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i)
+      dq[i] = nxt ? dnext[i] + (uint32_t)(Q - nq) * 128u : dcur[i] + (uint32_t)Q * 128u;
+    dma(q, dq, 0u);
+  };
 
   // ---- prologue: the first tile's first two blocks requested, then the table
   TileCodes<CW, FT, BV> c0, c1;
+  WCodes W0, W1, W2, W3;
+  ACodes A0, A1;
   place(blockIdx.x);
   if constexpr (QL) {
     dma(actq0, dcur, 0u);
-    wload(0, c0);
-    wload(1, c1);
+    dma(actq1, dcur, 128u);
+    wload4(0, W0);
+    wload4(1, W1);
+    wload4(2, W2);
+    wload4(3, W3);
   } else {
     load(0, c0);
     load(1, c1);
@@ -1027,10 +1086,7 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   }
   if constexpr (QL) __builtin_amdgcn_s_waitcnt(0);  // this wave's quad copies
   __syncthreads();
-  if constexpr (QL) {
-    aload(actq0, 0, c0);
-    aload(actq0, 1, c1);
-  }
+  if constexpr (QL) aload4(actq0, 0, A0);
 
   for (int u = blockIdx.x; u < T; u += gridDim.x) {
     // this tile's scales, used in its epilogue: lane l holds the column
@@ -1060,38 +1116,32 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     // it the compiler's wait analysis would assume the worst at the loop head
     // and wait for every load in flight.  Blocks past the end read zeros or
     // the next token's row (never used).
-    operands(c0, 0, a0, b0);
     if constexpr (QL) {
-      // two quads per iteration: quad m in actq0, m + 1 in actq1; the copy
-      // of quad m + 2 goes to actq0 once quad m is read - in the last
-      // iteration the next tile's quad 0, so the next tile starts on it
+      // two quads per iteration, blocks b .. b + 7: quad m in actq0, m + 1
+      // in actq1 (published before block b + 3), m + 2 copied into actq0
+      // after that and published before block b + 7, m + 3 copied into
+      // actq1 after that.  Block x's weights are in slot x mod 4, its
+      // activation words in slot x mod 2.  In the last iteration the copies
+      // are the next tile's quads 0 and 1, so it starts on them.
       const int nq = nblk >> 2;  // even
+      qoperands(W0, A0, 0, a0, b0);
       for (int m = 0; m < nq; m += 2) {
         const int b = 4 * m;
-        auto ld = [&](const unsigned char* q, int bq) {
-          return [&, q, bq](int blk, auto& tc) {
-            wload(blk, tc);
-            aload(q, bq, tc);
-          };
-        };
-        dma(actq1, dcur, (uint32_t)(m + 1) * 128u);
-        block_with(c0, c1, c0, b + 2, ld(actq0, 2));
-        block_with(c1, c0, c1, b + 3, ld(actq0, 3));
+        qblock(W0, A0, W1, A1, actq0, 1, W0, b + 4);
+        qblock(W1, A1, W2, A0, actq0, 2, W1, b + 5);
+        qblock(W2, A0, W3, A1, actq0, 3, W2, b + 6);
         publish();
-        block_with(c0, c1, c0, b + 4, ld(actq1, 0));
-        block_with(c1, c0, c1, b + 5, ld(actq1, 1));
-        const bool last = m + 2 >= nq;
-        uint32_t dq[NDMA];
-#pragma unroll
-        for (int i = 0; i < NDMA; ++i) dq[i] = last ? dnext[i] : dcur[i] + (uint32_t)(m + 2) * 128u;
-        dma(actq0, dq, 0u);
-        block_with(c0, c1, c0, b + 6, ld(actq1, 2));
-        block_with(c1, c0, c1, b + 7, ld(actq1, 3));
+        dma_quad(actq0, m + 2, nq);
+        qblock(W3, A1, W0, A0, actq1, 0, W3, b + 7);
+        qblock(W0, A0, W1, A1, actq1, 1, W0, b + 8);
+        qblock(W1, A1, W2, A0, actq1, 2, W1, b + 9);
+        qblock(W2, A0, W3, A1, actq1, 3, W2, b + 10);
         publish();
-        block_with(c0, c1, c0, b + 8, ld(actq0, 0));
-        block_with(c1, c0, c1, b + 9, ld(actq0, 1));
+        dma_quad(actq1, m + 3, nq);
+        qblock(W3, A1, W0, A0, actq0, 0, W3, b + 11);
       }
     } else {
+      operands(c0, 0, a0, b0);
       int blk = 0;
       for (; blk + 1 < nblk; blk += 2) {
         block(c0, c1, c0, blk + 2);
@@ -1134,10 +1184,11 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     if (u + (int)gridDim.x < T) {
       place(u + (int)gridDim.x);
       if constexpr (QL) {  // its quad 0 is in actq0 (published in the last iteration)
-        wload(0, c0);
-        wload(1, c1);
-        aload(actq0, 0, c0);
-        aload(actq0, 1, c1);
+        wload4(0, W0);
+        wload4(1, W1);
+        wload4(2, W2);
+        wload4(3, W3);
+        aload4(actq0, 0, A0);
       } else {
         load(0, c0);
         load(1, c1);
@@ -1165,8 +1216,14 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
             float4_t v = {acc[c][f][4 * g], acc[c][f][4 * g + 1], acc[c][f][4 * g + 2],
                           acc[c][f][4 * g + 3]};
             v = ts * sw * v;
+            // non-temporal where the reduction is long: streaming y past the
+            // L2 leaves that to the code streams (measured 1868 -> 1729 us at
+            // 4096 x 8192 x 28672); with the short value operand the kernel is
+            // bound by these stores, which then run slower (194 -> 507 us)
             float4_t* dst = reinterpret_cast<float4_t*>(yrow + j);
-            *dst = A.accumulate ? *dst + v : v;
+            const float4_t o = A.accumulate ? *dst + v : v;
+            if constexpr (BV) *dst = o;
+            else __builtin_nontemporal_store(o, dst);
           } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {

@@ -323,25 +323,28 @@ hipError_t launch_compensate_split(const CompArgs& a, const uint32_t* idx_w_gemm
 }
 
 // Main branch and compensation with the heavy channels inside the GEMM: the
-// compacted lists first (y (+)= their Y'), then the GEMM over the codes and
-// the dense positions (y += Y* + Y' of the heavy channels).  g: the main
-// GEMM's arguments (n > 32 tokens, d_in % 64 == 0).
+// GEMM over the codes and the dense positions (y (+)= Y* + Y' of the heavy
+// channels), then the compacted lists (y += their Y').  g: the main GEMM's
+// arguments (n > 32 tokens, d_in % 64 == 0).
 hipError_t launch_gemm_compensated_split(const GemmArgs& g, const CompArgs& a,
                                          const uint32_t* idx_w_gemm, void* ws, hipStream_t s) {
   hipError_t e = split_prepass(a, idx_w_gemm, ws, g.act_scale, s);
   if (e != hipSuccess) return e;
-  if ((e = launch_compensate_wr(sparse_args(a, ws, a.accumulate), s)) != hipSuccess) return e;
+  // the GEMM (with the heavy channels) first, with the caller's accumulate;
+  // the lists' kernel then adds into y.  That kernel hides the read of y
+  // behind its arithmetic, where the GEMM's epilogue would wait for it.
   const SplitLayout L = split_layout(a.n, a.d_in, a.d_out, a.k);
   char* base = static_cast<char*>(ws);
   GemmArgs m = g;
-  m.accumulate = 1;
+  m.accumulate = a.accumulate;
   m.nheavy = reinterpret_cast<const int*>(base + L.hlist) + kSplitHeavy;
   m.hv = reinterpret_cast<const uint8_t*>(base + L.rh);
   m.hw = reinterpret_cast<const uint32_t*>(base + L.idxh);
   // (expanding the activation codes once, to fp16 values the GEMM reads,
   // measured slower: 3.29 vs 2.73 ms at 4096x8192x28672 - four times the
   // activation bytes through L2 for every column tile)
-  return launch_gemm_heavy(m, s);
+  if ((e = launch_gemm_heavy(m, s)) != hipSuccess) return e;
+  return launch_compensate_wr(sparse_args(a, ws, 1), s);
 }
 
 // ----------------------------------------------------------------------------
