@@ -57,6 +57,7 @@ def test_status_strings(lib):
 BUF = np.zeros(1 << 16, dtype=np.uint8)
 P = BUF.ctypes.data          # 16-byte aligned by numpy for this size
 MIS = P + 2                  # misaligned
+A256 = (P + 255) & ~255      # 256-byte aligned, inside BUF (workspace checks)
 
 
 def _cb(vals):
@@ -272,8 +273,8 @@ def test_compensate_split_errors(lib):
     assert c(P, P, P, 4, 3, P, None, P, 4, P, 16, 8, P, 1, P, need, None) == -1   # idx_wr
     assert c(P, P, P, 4, 3, MIS, P, P, 4, P, 16, 8, P, 1, P, need, None) == -6
     assert c(*ok, None, need, None) == -10                       # no workspace
-    assert c(*ok, P + 16, need, None) == -10                     # not 256-byte aligned
-    assert c(*ok, P, 64, None) == -10                            # too small (need > 64)
+    assert c(*ok, A256 + 16, need, None) == -10                  # not 256-byte aligned
+    assert c(*ok, A256, 64, None) == -10                         # too small (need > 64)
     assert c(P, P, P, 4, 3, P, P, P, 4, P, 65536, 65536, P, 1, P, 1 << 40, None) == -9
     assert c(P, P, P, 0, 3, P, P, P, 4, P, 16, 8, P, 1, None, 0, None) == 0   # no tokens
 
@@ -292,6 +293,6 @@ def test_gemm_compensated_split_errors(lib):
     assert g(P, P, 40, 64, MIS, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P, 1 << 20, None) == -6
     # many tokens with lists: the workspace is required, 256-byte aligned, large enough
     assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, None, 1 << 20, None) == -10
-    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P + 16, 1 << 20, None) == -10
-    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, P, 64, None) == -10
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, A256 + 16, 1 << 20, None) == -10
+    assert g(P, P, 40, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, A256, 64, None) == -10
     assert g(P, P, 0, 64, P, P, P, 8, P, 4, 4, P, P, P, 2, P, 0, None, 0, None) == 0

@@ -536,6 +536,17 @@ def test_w4a3_layers(name):
     run_full(L, tokens=tokens)
 
 
+def test_persistent_tiles_ragged():
+    """The many-token GEMM in its one-workgroup-per-CU form (128 x 128 per
+    wave, activation codes staged in LDS four blocks at a time, several tiles
+    per workgroup, the next tile's codes fetched during the last blocks) on a
+    ragged layer: 1000 tokens (a partial last token tile) and 49112 columns (a
+    partial last column tile) make 768 tiles, three per workgroup on 256 CUs;
+    d_in = 1024 runs two iterations of the 8-block loop."""
+    L = synth.make_layer(synth.custom(1000, 1024, 49112, 16, seed=21))
+    run_full(L, algos=(oasis.ALGO_MFMA,), tokens=sampled_tokens(1000, 5))
+
+
 @pytest.mark.parametrize("name", FULL)
 def test_full_size_layers(name):
     L = synth.make_layer(synth.config(name))
