@@ -1166,16 +1166,40 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
         for (int f = 0; f < FT; ++f)
           hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * hrow + 64u * (uint32_t)h;
         auto hload = [&](int b, auto& tc) { load_from(b, tc, rhw, rhv, hoff); };
-        TileCodes<CW, FT, true> h0, h1;
-        hload(0, h0);
-        hload(1, h1);
-        operands(h0, 0, a0, b0);
-        int hb = 0;
-        for (; hb + 1 < nhb; hb += 2) {
-          block_with(h0, h1, h0, hb + 2, hload);
-          block_with(h1, h0, h1, hb + 3, hload);
+        if constexpr (CW * FT > 8) {
+          TileCodes<CW, FT, true> h0, h1;
+          hload(0, h0);
+          hload(1, h1);
+          operands(h0, 0, a0, b0);
+          int hb = 0;
+          for (; hb + 1 < nhb; hb += 2) {
+            block_with(h0, h1, h0, hb + 2, hload);
+            block_with(h1, h0, h1, hb + 3, hload);
+          }
+          if (hb < nhb) block_with(h0, h1, h0, hb + 2, hload);
+        } else {
+          // two workgroups per CU (256 registers a lane): one value block at a
+          // time - a second one in flight spilled the main loop's registers
+          TileCodes<CW, FT, true> h0;
+          for (int hb = 0; hb < nhb; ++hb) {
+            hload(hb, h0);
+            operands(h0, 0, a0, b0);
+            operands(h0, 1, a1, b1);
+            mma(a0, b0);
+            interleave(false);
+            __builtin_amdgcn_sched_barrier(0);
+            operands(h0, 2, a0, b0);
+            mma(a1, b1);
+            interleave(false);
+            __builtin_amdgcn_sched_barrier(0);
+            operands(h0, 3, a1, b1);
+            mma(a0, b0);
+            interleave(false);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
-        if (hb < nhb) block_with(h0, h1, h0, hb + 2, hload);
       }
     }
 
