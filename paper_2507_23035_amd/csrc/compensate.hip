@@ -375,41 +375,44 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
 // output columns 8m .. 8m + 7 (column 8m + c in bits 4c .. 4c + 3).  One
 // listed outlier reads exactly its own row, d_out / 2 bytes.
 //
-// Workgroup = 4 waves over a slab of 64 words (512 columns) and a tile of
-// tt tokens; wave w takes tokens w, w + 4, ... of the tile.  Lane l owns
+// Workgroup = 16 waves over a slab of 64 words (512 columns) and a tile of
+// tt tokens; wave w takes tokens w, w + 16, ... of the tile.  Lane l owns
 // word 64 * slab + l and 8 fp32 accumulators per token.  A token's listed
 // entries are wave-uniform: lane e holds entry e, readlane hands them out in
 // list order, and each entry fetches one word per lane (one contiguous
 // 256-byte piece of row p per wave, 3 * WR_U entries in flight).  A word's four
-// bytes become four pairs of weight centroids through a 32 KiB LDS table -
-// row `byte` holds 32 copies of pair(C_W, byte), lane l reads copy l mod 32,
-// so the reads are conflict free - and each centroid meets the residual in
-// one fp32 FMA (v_fma_mix_f32 takes the fp16 half directly).  48 KiB of LDS
-// per workgroup keeps three workgroups on a CU to hide the row loads (a
-// 64-copy table, whose offsets need no shift, left two and measured slower).
+// bytes become four pairs of weight centroids through a 64 KiB LDS table -
+// row `byte` holds 64 copies of pair(C_W, byte), lane l reads copy l, so the
+// reads are conflict free and the offset is one v_perm_b32 - and each
+// centroid meets the residual in one fp32 FMA (v_fma_mix_f32 takes the fp16
+// half directly).  Sixteen waves share the table (128 KiB of LDS with their
+// lists): four waves per SIMD hide the row loads, where 4-wave workgroups
+// with their own table fit two (64 copies) or three (32 copies, one more
+// shift per lookup) on a CU.
 // ----------------------------------------------------------------------------
 constexpr int WR_U = 16;    // entries per unit of word loads
 constexpr int WR_C = 512;   // list entries per wave held in LDS at a time
+constexpr int WR_W = 16;    // waves per workgroup
 
-__global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int nslab,
+__global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn, int nslab,
                                                         int ntile, int tt) {
   // the pair table at a fixed LDS address; dynamic LDS: per wave WR_C
   // channels and WR_C residuals of its lists
-  __shared__ uint32_t tab[256 * 32];
+  __shared__ uint32_t tab[256 * 64];
   extern __shared__ __align__(16) unsigned char smem_wr[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int* lp = reinterpret_cast<int*>(smem_wr) + wave * WR_C;
-  float* lr = reinterpret_cast<float*>(smem_wr + 4 * 4 * WR_C) + wave * WR_C;
+  float* lr = reinterpret_cast<float*>(smem_wr + 4 * WR_W * WR_C) + wave * WR_C;
   const int r = xcd_tile(blockIdx.x, nslab * ntile);
   const int slab = r / ntile, tile = r % ntile;  // token tiles of a slab on one XCD
   const int k = A.k, E = 2 * k, d_in = A.d_in, d_out = A.d_out;
 
   // ---- this wave's tokens, in units of WR_U entries
   const int tok0 = tile * tt;
-  const int tw = tok0 + wave;  // first token of this wave; then every fourth
+  const int tw = tok0 + wave;  // first token of this wave; then every WR_W-th
   const int tend = min(A.n, tok0 + tt);
-  const int ntw = tw < tend ? (tend - tw + 3) / 4 : 0;
+  const int ntw = tw < tend ? (tend - tw + WR_W - 1) / WR_W : 0;
   // units per token: the whole list, or with compacted lists the token's own
   // entries (at least one unit when y is overwritten: a token's last unit
   // writes y; none for a token without entries when adding into y).  Lane
@@ -420,7 +423,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   if (lane < ntw) {
     nu = nch;
     if (A.cnt) {
-      nu = (min(max(A.cnt[tw + 4 * lane], 0), E) + WR_U - 1) / WR_U;
+      nu = (min(max(A.cnt[tw + WR_W * lane], 0), E) + WR_U - 1) / WR_U;
       if (!A.accumulate) nu = max(1, nu);
     }
   }
@@ -452,7 +455,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
       const int u = c0 + f / WR_U;
       int slot_j, ubeg;
       unit_token(u, slot_j, ubeg);
-      const int i = tw + 4 * slot_j, e = WR_U * (u - ubeg) + f % WR_U;
+      const int i = tw + WR_W * slot_j, e = WR_U * (u - ubeg) + f % WR_U;
       pv[j] = -1;
       rv[j] = 0.0f;
       if (f < (c1 - c0) * WR_U && e < E) {
@@ -478,18 +481,19 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   };
   fill(0, min(U, WR_C / WR_U));  // the first chunk's loads overlap the table build
 
-  // pair table, 32 KiB: row `byte` holds 32 copies of pair(C_W, byte).
-  // Thread t writes chunks c = t + 256 s (s < 8) of 16 bytes: row c / 8 (low
-  // code (t / 8) mod 16, high code t / 128 + 2 s), copies 4 (c mod 8) ..
-  // 4 (c mod 8) + 3
+  // pair table, 64 KiB: row `byte` holds 64 copies of pair(C_W, byte).
+  // Thread t writes chunks c = t + 1024 s (s < 4) of 16 bytes: row c / 16
+  // (low code (t / 16) mod 16, high code t / 256 + 4 s), copies 4 (c mod 16)
+  // .. 4 (c mod 16) + 3
   {
+    static_assert(WR_W == 16, "the table build takes 1024 threads");
     const uint16_t* cb = A.lut->cb_wgt;
-    const uint32_t lo = cb[(tid >> 3) & 15];
+    const uint32_t lo = cb[(tid >> 4) & 15];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const uint32_t v = lo | ((uint32_t)cb[(tid >> 7) + 2 * s] << 16);
-      const uint32_t c = (uint32_t)tid + 256u * (uint32_t)s;
-      *reinterpret_cast<uint4_t*>(&tab[(c >> 3) * 32u + (c & 7u) * 4u]) = uint4_t{v, v, v, v};
+    for (int s = 0; s < 4; ++s) {
+      const uint32_t v = lo | ((uint32_t)cb[(tid >> 8) + 4 * s] << 16);
+      const uint32_t c = (uint32_t)tid + 1024u * (uint32_t)s;
+      *reinterpret_cast<uint4_t*>(&tab[(c >> 4) * 64u + (c & 15u) * 4u]) = uint4_t{v, v, v, v};
     }
   }
 
@@ -500,9 +504,8 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
   const uint32_t row_bytes = (uint32_t)wn * 4u;
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(A.idx_w), 0, (int)((uint32_t)d_in * row_bytes), 0x00020000);
-  // the offset of byte b's entry, b * 128 + (lane mod 32) * 4, is one
-  // v_perm_b32 (b << 8 | (lane mod 32) * 8) and one shift
-  const uint32_t lane8 = (uint32_t)(lane & 31) * 8u;
+  // the offset of byte b's entry, b * 256 + lane * 4, is one v_perm_b32
+  const uint32_t lane4 = (uint32_t)lane * 4u;
   const char* tb = reinterpret_cast<const char*>(tab);
   float sw[8];
 #pragma unroll
@@ -538,7 +541,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
     int slot_j, ubeg;
     unit_token(u, slot_j, ubeg);
     if (A.accumulate && vec && u == ubeg) {
-      const float4* s4 = reinterpret_cast<const float4*>(A.y + (size_t)(tw + 4 * slot_j) * d_out + 8u * m);
+      const float4* s4 = reinterpret_cast<const float4*>(A.y + (size_t)(tw + WR_W * slot_j) * d_out + 8u * m);
       yv[0] = s4[0];
       yv[1] = s4[1];
     }
@@ -551,8 +554,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
             float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rl), e));
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const uint32_t off =
-              __builtin_amdgcn_perm(w[e], lane8, 0x0C0C0000u | ((4u + b) << 8)) >> 1;
+          const uint32_t off = __builtin_amdgcn_perm(w[e], lane4, 0x0C0C0000u | ((4u + b) << 8));
           const uint32_t pr = *reinterpret_cast<const uint32_t*>(tb + off);
           acc[2 * b] = fmaf(re, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * b]);
           acc[2 * b + 1] = fmaf(re, h2f((uint16_t)(pr >> 16)), acc[2 * b + 1]);
@@ -561,7 +563,7 @@ __global__ void __launch_bounds__(256) k_compensate_wr(CompArgs A, int wn, int n
     }
     if (u != __builtin_amdgcn_readlane(uend, slot_j) - 1) return;
     // the token's last unit: y (+)= s_j * acc
-    const int i = tw + 4 * slot_j;
+    const int i = tw + WR_W * slot_j;
     float* dst = A.y + (size_t)i * d_out + 8u * m;
     if (vec) {
       float4* d4 = reinterpret_cast<float4*>(dst);
@@ -635,16 +637,16 @@ hipError_t launch_compensate_wr(const CompArgs& a, hipStream_t s) {
   }
   const int wn = (a.d_out + 7) / 8;
   // tokens per tile: every wave's lists fit its LDS area at once (one copy,
-  // no pipeline drain) when 2k <= WR_C / 4 ... WR_C; at most 32
+  // no pipeline drain) when 2k <= WR_C / 8 ... WR_C; at most 8 per wave
   const int E = 2 * a.k;
-  const int tt = 4 * max(1, min(8, WR_C / E));
+  const int tt = WR_W * max(1, min(8, WR_C / E));
   const int nslab = (wn + 63) / 64, ntile = (a.n + tt - 1) / tt;
-  const size_t lds = 4 * 8 * WR_C;  // dynamic part: the lists
+  const size_t lds = 8 * WR_W * WR_C;  // dynamic part: the lists
   hipError_t e = hipFuncSetAttribute((const void*)k_compensate_wr,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_compensate_wr, dim3(nslab * ntile), dim3(256), lds, s, a, wn, nslab, ntile,
-                     tt);
+  hipLaunchKernelGGL(k_compensate_wr, dim3(nslab * ntile), dim3(64 * WR_W), lds, s, a, wn, nslab,
+                     ntile, tt);
   return hipGetLastError();
 }
 
