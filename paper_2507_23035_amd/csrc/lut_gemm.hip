@@ -814,10 +814,10 @@ struct TileCodes {
 // with one block of lead the table lookups waited for them (a variant whose
 // lookups did not depend on the loaded words ran 15 % faster).
 template <int CW, int FT, int WX, int WY, bool BV, bool HV = false, bool QL = false>
-__global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
+__global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 4 ? 1 : 2))
     k_gemm_mfma_tile(GemmArgs A, int ncx, int nty) {
   static_assert(CW == 4, "the column scales of a wave are two per lane");
-  static_assert(!QL || (!BV && WX == 2 && FT == 4), "quad staging: 128 rows per group, 2 loaders");
+  static_assert(!QL || (!BV && WX == 2 && (FT == 4 || FT == 2)), "quad staging: 2 loaders a group");
   __shared__ uint32_t tab[256 * 64];          // 64 KiB dual decode table
   __shared__ float wsc[WX * WY][32 * CW];     // column scales of each wave's tile
   constexpr int QB = QL ? WY * 32 * FT * 128 : 16;  // bytes of one quad buffer
@@ -852,15 +852,16 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   // QL: byte offsets of this lane's 16-byte pieces of the quad copies (8 per
   // wave: rows 64 gx + 8 i + lane / 8 of the group), for this tile and the
   // workgroup's next one
-  constexpr int NDMA = QL ? 8 : 1;
+  constexpr int RPW = 32 * FT / WX;              // rows of a group each of its waves copies
+  constexpr int NDMA = QL ? RPW / 8 : 1;
   uint32_t dcur[NDMA], dnext[NDMA];
   auto dma_offsets = [&](int u, uint32_t (&d)[NDMA]) {
     if constexpr (QL) {
       const int tile = xcd_tile(min(u, T - 1), T);
       const int tg = ((tile % nty) * WY + wave / WX) * 32 * FT;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int R = 64 * (wave % WX) + 8 * i + (lane >> 3);
+      for (int i = 0; i < NDMA; ++i) {
+        const int R = RPW * (wave % WX) + 8 * i + (lane >> 3);
         const uint32_t c = (uint32_t)(lane & 7) ^ (uint32_t)((R >> 1) & 7);
         d[i] = (uint32_t)min(tg + R, A.n - 1) * arow + 16u * c;
       }
@@ -914,9 +915,9 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   auto dma = [&](unsigned char* q, const uint32_t (&d)[NDMA], uint32_t qoff) {
     if constexpr (QL) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < NDMA; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            ra, (__attribute__((address_space(3))) void*)(q + gbase + (64u * (uint32_t)(wave % WX) + 8u * (uint32_t)i) * 128u),
+            ra, (__attribute__((address_space(3))) void*)(q + gbase + ((uint32_t)RPW * (uint32_t)(wave % WX) + 8u * (uint32_t)i) * 128u),
             16, (int)(d[i] + qoff), 0, 0, 0);
     }
   };
@@ -955,21 +956,30 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   float16_t acc[CW][FT];
   const uint32_t l4w = (uint32_t)r32 * 4u, l4a = l4w + 128u;
   // operands of step st (every block is full: d_in is a multiple of 64)
+  // The MFMAs of a step run token group by token group (all column groups
+  // of b[0], then of b[1], ...), and the table reads of the next step are
+  // issued in the order their MFMAs need them: a[0], b[0], a[1..], b[1..].
+  // Each operand then has at least CW + FT + 1 MFMAs between its last read
+  // and its first use (with a[] first and the MFMAs column by column, the
+  // last-read b[] were needed within four MFMAs of the step start).
   auto operands = [&](const auto& tc, int st, half8_t (&a)[CW], half8_t (&b)[FT]) {
     constexpr bool VALS = sizeof(tc.a) / sizeof(tc.a[0]) == 4;
-#pragma unroll
-    for (int c = 0; c < CW; ++c) a[c] = expand_dual(tc.w[st][c], tb, l4w);
-#pragma unroll
-    for (int f = 0; f < FT; ++f) {
+    auto bop = [&](int f) {
       if constexpr (VALS) b[f] = __builtin_bit_cast(half8_t, tc.a[st][f]);
       else b[f] = expand_dual(tc.a[0][f][st], tb, l4a);
-    }
+    };
+    a[0] = expand_dual(tc.w[st][0], tb, l4w);
+    bop(0);
+#pragma unroll
+    for (int c = 1; c < CW; ++c) a[c] = expand_dual(tc.w[st][c], tb, l4w);
+#pragma unroll
+    for (int f = 1; f < FT; ++f) bop(f);
   };
   auto mma = [&](const half8_t (&a)[CW], const half8_t (&b)[FT]) {
 #pragma unroll
-    for (int c = 0; c < CW; ++c)
+    for (int f = 0; f < FT; ++f)
 #pragma unroll
-      for (int f = 0; f < FT; ++f)
+      for (int c = 0; c < CW; ++c)
         acc[c][f] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[c], b[f], acc[c][f], 0, 0, 0);
   };
   // Instruction order of one step: each MFMA keeps the matrix unit busy for
@@ -1020,20 +1030,22 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
   // QL: operands of step st from a weight slot and an activation slot
   auto qoperands = [&](const WCodes& wc, const ACodes& ac, int st, half8_t (&a)[CW],
                        half8_t (&b)[FT]) {
+    a[0] = expand_dual(wc.w[st][0], tb, l4w);
+    b[0] = expand_dual(ac.a[0][st], tb, l4a);
 #pragma unroll
-    for (int c = 0; c < CW; ++c) a[c] = expand_dual(wc.w[st][c], tb, l4w);
+    for (int c = 1; c < CW; ++c) a[c] = expand_dual(wc.w[st][c], tb, l4w);
 #pragma unroll
-    for (int f = 0; f < FT; ++f) b[f] = expand_dual(ac.a[f][st], tb, l4a);
+    for (int f = 1; f < FT; ++f) b[f] = expand_dual(ac.a[f][st], tb, l4a);
   };
-  // QL: one block on (wc, ac); in the last step the next block's activation
-  // words are read from quad buffer qn (chunk pair bqn) into an, its step 0
-  // operands expanded from (wn, an) and slot wr refilled with the weights of
-  // block rblk.  The words are read right before the weight-operand lookups
-  // of that expansion: LDS operations retire in order and a wait can leave at
-  // most 15 of them in flight, so words read earlier would make that wait
-  // drain the lookups issued after them.
+  // QL: one block on (wc, ac); the next block's activation words are read
+  // from quad buffer qn (chunk pair bqn) into an during step 0 (three steps
+  // before their first use: read right before it, the wait for them drained
+  // the table reads issued in between), its step 0 operands expanded from
+  // (wn, an) in the last step, where slot wr is refilled with the weights of
+  // block rblk
   auto qblock = [&](const WCodes& wc, const ACodes& ac, const WCodes& wn, ACodes& an,
                     const unsigned char* qn, int bqn, WCodes& wr, int rblk) {
+    aload4(qn, bqn, an);
     qoperands(wc, ac, 1, a1, b1);
     mma(a0, b0);
     interleave(false);
@@ -1046,7 +1058,6 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV ? 1 : 2))
     mma(a0, b0);
     interleave(false);
     __builtin_amdgcn_sched_barrier(0);
-    aload4(qn, bqn, an);
     qoperands(wn, an, 0, a0, b0);
     wload4(rblk, wr);
     mma(a1, b1);
@@ -1279,11 +1290,11 @@ static int resident_workgroups(int per_cu) {
 template <int CW, int FT, int WX, int WY, bool BV = false, bool HV = false>
 static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   constexpr int TC = 32 * CW * WX, TT = 32 * FT * WY;
-  constexpr int PER_CU = (CW * FT > 8 || BV) ? 1 : 2;
+  constexpr int PER_CU = (CW * FT > 8 || BV || WX * WY > 4) ? 1 : 2;
   const int ncx = (a.d_out + TC - 1) / TC;
   const int nty = (a.n + TT - 1) / TT;
   const int grid = min(ncx * nty, resident_workgroups(PER_CU));
-  if constexpr (!BV && FT == 4 && WX == 2) {
+  if constexpr (!BV && WX == 2 && (FT == 4 || WY == 4)) {
     if (a.d_in % 512 == 0) {
       hipLaunchKernelGGL((k_gemm_mfma_tile<CW, FT, WX, WY, BV, HV, true>), dim3(grid),
                          dim3(WX * WY * 64), 0, s, a, ncx, nty);
