@@ -61,25 +61,37 @@ __device__ __forceinline__ bool split_entry(const CompArgs& A, size_t f, int& p,
 // per touched channel - the heavy channels are listed by most tokens, and
 // global atomics on them from every entry would serialize.
 constexpr int kSplitLdsBins = 16384;
-template <bool LDS>
-__global__ void __launch_bounds__(256) k_split_count(CompArgs A, int* __restrict__ count) {
+template <bool LDS, int NT>
+__global__ void __launch_bounds__(NT) k_split_count(CompArgs A, int* __restrict__ count) {
   __shared__ int hist[LDS ? kSplitLdsBins : 1];
   const size_t tot = (size_t)A.n * 2 * A.k;
   if constexpr (LDS) {
-    for (int p = threadIdx.x; p < A.d_in; p += 256) hist[p] = 0;
+    for (int p = threadIdx.x; p < A.d_in; p += NT) hist[p] = 0;
     __syncthreads();
   }
-  for (size_t f = (size_t)blockIdx.x * 256 + threadIdx.x; f < tot; f += (size_t)gridDim.x * 256) {
-    int p;
-    float r;
-    if (split_entry(A, f, p, r)) {
-      if constexpr (LDS) atomicAdd(&hist[p], 1);
-      else atomicAdd(&count[p], 1);
+  // eight entries' loads in flight before their counts
+  constexpr int U = 8;
+  const size_t stride = (size_t)gridDim.x * NT;
+  for (size_t f0 = (size_t)blockIdx.x * NT + threadIdx.x; f0 < tot; f0 += U * stride) {
+    int p[U];
+    float r[U];
+    bool live[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const size_t f = f0 + (size_t)u * stride;
+      live[u] = f < tot && split_entry(A, f, p[u], r[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (live[u]) {
+        if constexpr (LDS) atomicAdd(&hist[p[u]], 1);
+        else atomicAdd(&count[p[u]], 1);
+      }
     }
   }
   if constexpr (LDS) {
     __syncthreads();
-    for (int p = threadIdx.x; p < A.d_in; p += 256)
+    for (int p = threadIdx.x; p < A.d_in; p += NT)
       if (hist[p]) atomicAdd(&count[p], hist[p]);
   }
 }
@@ -95,13 +107,21 @@ __global__ void __launch_bounds__(1024) k_split_select(int d_in, int thr,
   const int t = threadIdx.x;
   const int per = (d_in + 1023) / 1024;
   const int p0 = min(d_in, t * per), p1 = min(d_in, p0 + per);
+  // the counts of up to 16 channels per thread are read at once (d_in <=
+  // 16384, the LDS count's limit; beyond it, a second pass reads them again)
+  constexpr int PR = 16;
+  int cnt[PR];
+#pragma unroll
+  for (int q = 0; q < PR; ++q) cnt[q] = p0 + q < p1 ? count[p0 + q] : 0;
   uint64_t mine = 0;
-  for (int p = p0; p < p1; ++p) mine += count[p] >= thr;
+#pragma unroll
+  for (int q = 0; q < PR; ++q) mine += cnt[q] >= thr;
+  for (int p = p0 + PR; p < p1; ++p) mine += count[p] >= thr;
   const uint64_t incl = block_scan64<1024>(mine, tmp);
   int idx = (int)(incl - mine);
-  for (int p = p0; p < p1; ++p) {
+  auto place = [&](int p, int c) {
     int sl = -1;
-    if (count[p] >= thr) {
+    if (c >= thr) {
       if (idx < kSplitHeavy) {
         sl = idx;
         hlist[idx] = p;
@@ -109,7 +129,11 @@ __global__ void __launch_bounds__(1024) k_split_select(int d_in, int thr,
       ++idx;
     }
     slot[p] = sl;
-  }
+  };
+#pragma unroll
+  for (int q = 0; q < PR; ++q)
+    if (p0 + q < p1) place(p0 + q, cnt[q]);
+  for (int p = p0 + PR; p < p1; ++p) place(p, count[p]);
   if (t == 1023) total = (int)min((uint64_t)kSplitHeavy, incl);  // the last prefix is the total
   __syncthreads();
   const int nh = total;
@@ -255,12 +279,14 @@ static hipError_t split_prepass(const CompArgs& a, const uint32_t* idx_w_gemm, v
   if (e != hipSuccess) return e;
   const size_t tot = (size_t)a.n * 2 * a.k;
   if (a.d_in <= kSplitLdsBins) {
-    // about 64 workgroups: each flushes at most d_in counts
-    const unsigned cblocks = (unsigned)std::min<size_t>((tot + 255) / 256, 64);
-    hipLaunchKernelGGL(k_split_count<true>, dim3(cblocks), dim3(256), 0, s, a, count);
+    // at most 16 workgroups of 1024 threads: each flushes the counts it
+    // touched with global adds, and 64 workgroups of 256 spent most of the
+    // kernel on those (the heavy channels' counters serialize)
+    const unsigned cblocks = (unsigned)std::min<size_t>((tot + 1023) / 1024, 16);
+    hipLaunchKernelGGL((k_split_count<true, 1024>), dim3(cblocks), dim3(1024), 0, s, a, count);
   } else {
     const unsigned cblocks = (unsigned)std::min<size_t>((tot + 255) / 256, 4096);
-    hipLaunchKernelGGL(k_split_count<false>, dim3(cblocks), dim3(256), 0, s, a, count);
+    hipLaunchKernelGGL((k_split_count<false, 256>), dim3(cblocks), dim3(256), 0, s, a, count);
   }
   const int thr = std::max(2, a.n / 8);
   hipLaunchKernelGGL(k_split_select, dim3(1), dim3(1024), 0, s, a.d_in, thr, count, slot, hlist);
