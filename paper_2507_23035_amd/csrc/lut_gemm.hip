@@ -190,13 +190,14 @@ __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
 // Expand the codes of one block to fp16 centroid values and run its MFMAs:
 // CW column tiles (tile c holds columns j0 + CW*m + c) by TF token tiles.
 // Steps are taken SB at a time: all their table reads are issued before the
-// first MFMA, so the LDS latency is paid once per batch.  Activations of
-// tokens past n (tok_ok false) are not expanded (one branch per token tile);
-// MASK also zeroes the words past d_in of a partial last block.
+// first MFMA, so the LDS latency is paid once per batch.  Tokens past n read
+// code words of zero (buffer loads past the end) and are expanded like the
+// others: they only reach MFMA output columns that are never stored.  MASK
+// zeroes the words past d_in of a partial last block.
 template <int CW, int TF, bool MASK>
 __device__ __forceinline__ void mma_block(int KB, int blk, const BlockCodes<CW, TF>& bc,
                                           const char* tab, uint32_t l4w, uint32_t l4a,
-                                          const bool (&tok_ok)[TF], float4_t (&acc)[CW][TF]) {
+                                          float4_t (&acc)[CW][TF]) {
   constexpr int SB = CW * TF >= 4 ? 2 : 4;
   const int g = (threadIdx.x & 63) >> 4;
   const int kw0 = blk * 16 + 4 * g;
@@ -209,15 +210,9 @@ __device__ __forceinline__ void mma_block(int KB, int blk, const BlockCodes<CW, 
 #pragma unroll
       for (int c = 0; c < CW; ++c) af[s][c] = expand_dual(bc.wv[s0 + s][c], tab, l4w);
 #pragma unroll
-    for (int f = 0; f < TF; ++f) {
-      if (tok_ok[f]) {
+    for (int f = 0; f < TF; ++f)
 #pragma unroll
-        for (int s = 0; s < SB; ++s) bf[s][f] = expand_dual(bc.av[f][s0 + s], tab, l4a);
-      } else {
-#pragma unroll
-        for (int s = 0; s < SB; ++s) bf[s][f] = zero;
-      }
-    }
+      for (int s = 0; s < SB; ++s) bf[s][f] = expand_dual(bc.av[f][s0 + s], tab, l4a);
     if constexpr (MASK) {  // words past the end contribute nothing
 #pragma unroll
       for (int s = 0; s < SB; ++s)
@@ -246,14 +241,12 @@ template <int CW, int TF, int PF, bool FULLK>
 __device__ __forceinline__ void gemv_blocks(int KB, const GemvAddr& ad, int blk_begin,
                                             int blk_end, int blk_stride,
                                             BlockCodes<CW, TF> (&buf)[PF], const char* tab,
-                                            uint32_t l4w, uint32_t l4a, const bool (&tok_ok)[TF],
-                                            float4_t (&acc)[CW][TF]) {
+                                            uint32_t l4w, uint32_t l4a, float4_t (&acc)[CW][TF]) {
   if (blk_end <= blk_begin + PF * blk_stride) {  // the preloaded blocks are all: no refills
 #pragma unroll
     for (int d = 0; d < PF; ++d)
       if (blk_begin + d * blk_stride < blk_end)
-        mma_block<CW, TF, !FULLK>(KB, blk_begin + d * blk_stride, buf[d], tab, l4w, l4a, tok_ok,
-                                  acc);
+        mma_block<CW, TF, !FULLK>(KB, blk_begin + d * blk_stride, buf[d], tab, l4w, l4a, acc);
     return;
   }
   for (int blk = blk_begin; blk < blk_end; blk += PF * blk_stride) {
@@ -261,7 +254,7 @@ __device__ __forceinline__ void gemv_blocks(int KB, const GemvAddr& ad, int blk_
     for (int d = 0; d < PF; ++d) {
       const int b = blk + d * blk_stride;
       if (b < blk_end) {
-        mma_block<CW, TF, !FULLK>(KB, b, buf[d], tab, l4w, l4a, tok_ok, acc);
+        mma_block<CW, TF, !FULLK>(KB, b, buf[d], tab, l4w, l4a, acc);
         load_block_buf<CW, TF>(ad, b + PF * blk_stride, buf[d]);
       }
     }
@@ -520,9 +513,6 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) acc[c][f] = float4_t{0.f, 0.f, 0.f, 0.f};
-  bool tok_ok[TF];
-#pragma unroll
-  for (int f = 0; f < TF; ++f) tok_ok[f] = 16 * f + (lane & 15) < A.n;
   const char* tb = reinterpret_cast<const char*>(tab);
   // weight entries: copy lane mod 32 of the shared codebook, or (per column)
   // position 2 m + (g mod 2) of lane (g, m)'s column m
@@ -545,7 +535,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
     else comp_rows<BE>(A, ad, ccol4, ce0, crow0);
   }
   if (wave < nblk)
-    gemv_blocks<CW, TF, PF, FULLK>(KB, ad, wave, nblk, NW, buf, tb, l4w, l4a, tok_ok, acc);
+    gemv_blocks<CW, TF, PF, FULLK>(KB, ad, wave, nblk, NW, buf, tb, l4w, l4a, acc);
 
   // outlier branch: reads only rows 0..15 of the table (weight centroids),
   // which nothing overwrites before the next barrier

@@ -232,6 +232,21 @@ def test_ragged_shapes(n, d_in, d_out, k, b_a, b_w, seed):
     run_full(synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed, b_a=b_a, b_w=b_w)))
 
 
+FUSED_ROWS = [
+    # n, d_in, d_out, k, b_a, b_w, seed: the fused GEMV with row-layout
+    # compensation (8 n k >= d_in) at each column-tile width
+    (16, 1024, 520, 24, 4, 4, 30),   # 16-column tiles: half the waves get no K block
+    (5, 2048, 16400, 52, 4, 4, 31),  # 64-column tiles (257, the last partial): two K
+                                     # blocks per wave, 26 entries per thread
+    (24, 1024, 9000, 40, 3, 4, 32),  # two token tiles, 32-column tiles
+]
+
+
+@pytest.mark.parametrize("n,d_in,d_out,k,b_a,b_w,seed", FUSED_ROWS)
+def test_fused_rows_tile_widths(n, d_in, d_out, k, b_a, b_w, seed):
+    run_full(synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed, b_a=b_a, b_w=b_w)))
+
+
 def test_split_heavy_channels_out_of_range():
     """Scale mode NONE (t = 1) with a channel of +-40000 in every token: its
     residual over t cannot be an fp16 hi/lo pair below 2^15, so the GEMM with
