@@ -178,6 +178,9 @@ __device__ __forceinline__ void load_block_buf(const GemvAddr& ad, int blk,
       const uint4_t v =
           __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(ad.rw, o, 0, 0));
       bc.wv[s][0] = v[0]; bc.wv[s][1] = v[1]; bc.wv[s][2] = v[2]; bc.wv[s][3] = v[3];
+    } else if constexpr (CW == 3) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b96(ad.rw, o, 0, 0);
+      bc.wv[s][0] = v[0]; bc.wv[s][1 % CW] = v[1]; bc.wv[s][2 % CW] = v[2];
     } else if constexpr (CW == 2) {
       const auto v = __builtin_amdgcn_raw_buffer_load_b64(ad.rw, o, 0, 0);
       bc.wv[s][0] = v[0]; bc.wv[s][CW - 1] = v[1];
@@ -286,6 +289,9 @@ struct CompEntries {
   float r[B];
 };
 
+// All B entries are requested before any is checked: a check placed next to
+// its load makes the compiler wait for that load, and then only two or three
+// entries are in flight whatever B is.
 template <int B>
 __device__ __forceinline__ void comp_entries(const GemmArgs& A, int i, int e0, int nslices,
                                              CompEntries<B>& ce) {
@@ -293,13 +299,18 @@ __device__ __forceinline__ void comp_entries(const GemmArgs& A, int i, int e0, i
   const float* res = A.residual + (size_t)i * E;
   const int32_t* mx = A.max_idx + (size_t)i * k;
   const int32_t* mn = A.min_idx + (size_t)i * k;
+  int praw[B];
 #pragma unroll
   for (int b = 0; b < B; ++b) {
     const int e = min(e0 + b * nslices, E - 1);
-    const bool live = e0 + b * nslices < E;
-    const int p = e < k ? mx[e] : mn[e - k];
-    ce.p[b] = live && p >= 0 && p < A.d_in ? p : -1;
+    praw[b] = e < k ? mx[e] : mn[e - k];
     ce.r[b] = res[e];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const bool live = e0 + b * nslices < E;
+    ce.p[b] = live && praw[b] >= 0 && praw[b] < A.d_in ? praw[b] : -1;
   }
 }
 
@@ -416,23 +427,25 @@ __device__ __forceinline__ void tile_compensation_wr(const GemmArgs& A,
 // the codebooks, and the entries are checked after the table barrier, behind
 // the weight loads in flight.
 // ----------------------------------------------------------------------------
-template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS, bool PERCOL = false>
-__global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
+// One column tile (columns j0 .. j0 + 16 CW - 1) of the few-token kernels;
+// `tab` is the workgroup's 64 KiB decode table, reused for the reduction.
+template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS, bool PERCOL>
+__device__ __forceinline__ void gemv_tile(const GemmArgs& A, const int j0, uint32_t* tab) {
   static_assert(!PERCOL || (CW == 1 && !ROWS), "per-column codebooks: 16-column tiles, GEMM layout");
   constexpr int NT = NW * 64;
   constexpr int SLOTS = 16 * TF, COLS = 16 * CW;
   constexpr int CG = ROWS ? 8 : 4;  // columns per compensation thread
-  constexpr int NSLICES = (NT / SLOTS) / (COLS / CG) > 0 ? (NT / SLOTS) / (COLS / CG) : 1;
-  static_assert((NT / SLOTS) % (COLS / CG) == 0, "threads per token must cover the columns");
+  constexpr int GROUPS = COLS / CG;  // compensation threads per token and slice
+  static_assert(NT / SLOTS >= GROUPS, "a token's threads cover its columns");
+  // threads per token NT / SLOTS: NSLICES * GROUPS of them compensate
+  constexpr int NSLICES = (NT / SLOTS) / GROUPS;
   constexpr int RED_FLOATS = 4 * NW * CW * TF * 64;
   constexpr int PART_FLOATS = SLOTS * NSLICES * COLS;
   static_assert(4 * (RED_FLOATS + PART_FLOATS) <= 64 * 1024, "reduction buffers fit in the table");
   constexpr int EPT = (SLOTS * COLS + NT - 1) / NT;  // outputs per thread in the epilogue
-  __shared__ uint32_t tab[256 * 64];  // 64 KiB decode table; after the main loop the reduction
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  const int j0 = xcd_tile(blockIdx.x, ntiles) * COLS;
   const int KB = A.d_in >> 3;
   const int nblk = (KB + 15) / 16;
   constexpr bool fused = B > 0;  // B = 0: no outlier lists (k = 0)
@@ -487,13 +500,14 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
     swj[q] = A.w_scale[j];
     ts[q] = A.act_scale[tok];
   }
-  const int T = NT / SLOTS;  // compensation threads per token
+  const int T = NT / SLOTS;  // threads per token
   const int ci = tid / T, cu = tid - ci * T;
-  const int cquad = cu % (COLS / CG), cslice = cu / (COLS / CG);  // column group, slice
+  const int cquad = cu % GROUPS, cslice = cu / GROUPS;  // column group, slice
+  const bool cact = cslice < NSLICES;  // a compensating thread
   // a few entries are worth holding through the main loop, many are not
   constexpr bool PRE = fused && B <= 4 && TF == 1 && CW <= 2;
   CompEntries<BE> ce0;
-  if (PRE && ci < A.n) comp_entries<BE>(A, ci, cslice, NSLICES, ce0);
+  if (PRE && cact && ci < A.n) comp_entries<BE>(A, ci, cslice, NSLICES, ce0);
   BlockCodes<CW, TF> buf[PF];
 #pragma unroll
   for (int d = 0; d < PF; ++d)
@@ -530,7 +544,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
                                             (int)((uint32_t)A.d_in * wr_row), 0x00020000);
   uint4_t crow0[ROWS ? 1 : BE];
   uint32_t crw0[ROWS ? BE : 1];
-  if (PRE && ci < A.n) {
+  if (PRE && cact && ci < A.n) {
     if constexpr (ROWS) comp_rows_wr<BE>(rwr, wr_row, wr_off, ce0, crw0);
     else comp_rows<BE>(A, ad, ccol4, ce0, crow0);
   }
@@ -542,7 +556,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   float cacc[CG];
 #pragma unroll
   for (int c = 0; c < CG; ++c) cacc[c] = 0.0f;
-  if (fused && ci < A.n) {
+  if (fused && cact && ci < A.n) {
     if constexpr (ROWS)
       tile_compensation_wr<BE, PRE>(A, rwr, wr_row, wr_off, tb, NSLICES, ci, cslice, ce0, crw0,
                                    cacc);
@@ -557,7 +571,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
   for (int c = 0; c < CW; ++c)
 #pragma unroll
     for (int f = 0; f < TF; ++f) red[wave][c * TF + f][lane] = acc[c][f];
-  if (fused && ci < SLOTS) {
+  if (fused && cact && ci < SLOTS) {
 #pragma unroll
     for (int c = 0; c < CG; ++c) part[(ci * NSLICES + cslice) * COLS + CG * cquad + c] = cacc[c];
   }
@@ -586,6 +600,29 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntil
     float* dst = A.y + (size_t)tok * A.d_out + j;
     *dst = A.accumulate ? *dst + val : val;
   }
+}
+
+template <int CW, int TF, int NW, int PF, bool FULLK, int B, bool ROWS, bool PERCOL = false>
+__global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv(GemmArgs A, int ntiles) {
+  __shared__ uint32_t tab[256 * 64];  // 64 KiB decode table; after the main loop the reduction
+  gemv_tile<CW, TF, NW, PF, FULLK, B, ROWS, PERCOL>(A, xcd_tile(blockIdx.x, ntiles) * 16 * CW,
+                                                    tab);
+}
+
+// Two tile widths in one launch, so that the columns spread evenly over the
+// CUs: the first na workgroups (one per CU) take 16*CWA columns each, the
+// other nb take 16*CWB.  Workgroups start in id order and the first na fill
+// every CU once, so each CU ends up with one tile of each width (at 28672
+// columns: 64 + 48 per CU instead of two 64-column tiles on 192 CUs).
+template <int CWA, int CWB, int NW, int PF, bool FULLK, int B, bool ROWS>
+__global__ void __launch_bounds__(NW * 64) k_gemm_mfma_gemv2(GemmArgs A, int na, int nb) {
+  __shared__ uint32_t tab[256 * 64];
+  const int b = blockIdx.x;
+  if (b < na)
+    gemv_tile<CWA, 1, NW, PF, FULLK, B, ROWS, false>(A, xcd_tile(b, na) * 16 * CWA, tab);
+  else
+    gemv_tile<CWB, 1, NW, PF, FULLK, B, ROWS, false>(
+        A, na * 16 * CWA + xcd_tile(b - na, nb) * 16 * CWB, tab);
 }
 
 // ----------------------------------------------------------------------------
@@ -1408,12 +1445,53 @@ static void launch_gemv(const GemmArgs& a, hipStream_t s) {
     launch_gemv_r<CW, TF, NW, false>(a, s);
 }
 
+// Two tile widths (k_gemm_mfma_gemv2): na = one workgroup per CU of 16*CWA
+// columns, the rest in tiles of 16*CWB; the outlier lists as in launch_gemv
+// (entries in flight chosen for the wider tiles).
+// Whole K blocks only (d_in a multiple of 128): with a masked last block the
+// wider body needs more than 128 VGPRs and two workgroups no longer fit a CU.
+template <int CWA, int CWB, int NW, int B, bool ROWS>
+static void launch_gemv2_b(const GemmArgs& a, int na, int nb, hipStream_t s) {
+  constexpr int PF = 2;
+  hipLaunchKernelGGL((k_gemm_mfma_gemv2<CWA, CWB, NW, PF, true, B, ROWS>), dim3(na + nb),
+                     dim3(NW * 64), 0, s, a, na, nb);
+}
+
+template <int CWA, int CWB, int NW>
+static void launch_gemv2(const GemmArgs& a, int na, hipStream_t s) {
+  const int nb = (a.d_out - na * 16 * CWA + 16 * CWB - 1) / (16 * CWB);
+  const bool rows = a.idx_wr && 8ll * a.n * a.k >= (long long)a.d_in;
+  const int nsl = (NW * 4) / (16 * CWA / (rows ? 8 : 4));  // slices of the wider tiles
+  if (a.k == 0)
+    launch_gemv2_b<CWA, CWB, NW, 0, false>(a, na, nb, s);
+  else if (rows && 2 * a.k <= 4 * nsl)
+    launch_gemv2_b<CWA, CWB, NW, 4, true>(a, na, nb, s);
+  else if (rows)
+    launch_gemv2_b<CWA, CWB, NW, 8, true>(a, na, nb, s);
+  else if (2 * a.k <= 4 * nsl)
+    launch_gemv2_b<CWA, CWB, NW, 4, false>(a, na, nb, s);
+  else
+    launch_gemv2_b<CWA, CWB, NW, 8, false>(a, na, nb, s);
+}
+
 template <int TF>
 static void launch_gemv_tf(const GemmArgs& a, hipStream_t s) {
   // widest column tile that still gives >= 256 workgroups.  LDS: reduction
-  // buffer NW * CW * TF KiB <= 32 KiB; the fused compensation needs the
-  // threads per token (NW * 64 / (16 * TF)) to be a multiple of CW * 4.
+  // buffer NW * CW * TF KiB <= 32 KiB; the fused compensation takes a
+  // token's threads (NW * 64 / (16 * TF)) in slices of CW * 4 (row layout:
+  // CW * 2).  Between 64 and 112 columns per CU (16384 < d_out <= 28672 on
+  // 256 CUs, whole K blocks) every CU gets two workgroups of about equal
+  // width - 48 + 32, 48 + 48 or 64 + 48 columns - instead of a second
+  // 64-column tile on some CUs only: the busiest CU sets the time.
   if constexpr (TF == 1) {
+    const int ncu = resident_workgroups(1);
+    const int per = ((a.d_out + 15) / 16 + ncu - 1) / ncu;  // 16-column tiles per CU
+    if ((a.d_in / 8) % 16 == 0 && per >= 5 && per <= 7) {
+      if (per == 5) launch_gemv2<3, 2, 8>(a, ncu, s);
+      else if (per == 6) launch_gemv<3, 1, 8>(a, s);
+      else launch_gemv2<4, 3, 8>(a, ncu, s);
+      return;
+    }
     if ((a.d_out + 63) / 64 >= 256) launch_gemv<4, 1, 8>(a, s);
     else if ((a.d_out + 31) / 32 >= 256) launch_gemv<2, 1, 16>(a, s);
     else launch_gemv<1, 1, 16>(a, s);

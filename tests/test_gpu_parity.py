@@ -247,6 +247,21 @@ def test_fused_rows_tile_widths(n, d_in, d_out, k, b_a, b_w, seed):
     run_full(synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed, b_a=b_a, b_w=b_w)))
 
 
+BALANCED = [
+    # n, d_in, d_out, k, b_a, b_w, seed: few-token GEMV where the columns are
+    # dealt two workgroups per CU (256 CUs; d_in % 128 == 0), ragged d_out
+    (16, 1024, 27000, 16, 4, 4, 40),  # 64 + 48 columns per CU, row-layout lists
+    (7, 2048, 24000, 8, 4, 4, 41),    # 48 + 48, GEMM-layout lists
+    (12, 512, 18000, 40, 3, 4, 42),   # 48 + 32, row-layout lists, 8 entries in flight
+    (16, 1024, 20000, 0, 4, 4, 43),   # 48 + 32, no lists
+]
+
+
+@pytest.mark.parametrize("n,d_in,d_out,k,b_a,b_w,seed", BALANCED)
+def test_gemv_balanced_tiles(n, d_in, d_out, k, b_a, b_w, seed):
+    run_full(synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed, b_a=b_a, b_w=b_w)))
+
+
 def test_split_heavy_channels_out_of_range():
     """Scale mode NONE (t = 1) with a channel of +-40000 in every token: its
     residual over t cannot be an fp16 hi/lo pair below 2^15, so the GEMM with
