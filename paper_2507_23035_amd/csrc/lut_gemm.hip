@@ -1476,28 +1476,29 @@ static void launch_gemv2(const GemmArgs& a, int na, hipStream_t s) {
 
 template <int TF>
 static void launch_gemv_tf(const GemmArgs& a, hipStream_t s) {
-  // widest column tile that still gives >= 256 workgroups.  LDS: reduction
-  // buffer NW * CW * TF KiB <= 32 KiB; the fused compensation takes a
-  // token's threads (NW * 64 / (16 * TF)) in slices of CW * 4 (row layout:
-  // CW * 2).  Between 64 and 112 columns per CU (16384 < d_out <= 28672 on
-  // 256 CUs, whole K blocks) every CU gets two workgroups of about equal
-  // width - 48 + 32, 48 + 48 or 64 + 48 columns - instead of a second
-  // 64-column tile on some CUs only: the busiest CU sets the time.
+  // The columns are dealt evenly over the CUs (per = 16-column tiles per CU):
+  // the busiest CU sets the time.  Up to 64 columns per CU, one workgroup per
+  // CU of 16 * per columns (16 waves at 16 or 32 columns, 8 at 48 or 64); a
+  // 1024-thread workgroup fills a CU, so more of them than CUs would run in
+  // two rounds.  Between 64 and 112 columns per CU (whole K blocks) two
+  // workgroups per CU of about equal width, 48 + 32, 48 + 48 or 64 + 48
+  // columns; beyond that, 64-column tiles.  LDS: reduction buffer
+  // NW * CW * TF KiB <= 32 KiB; the fused compensation takes a token's
+  // threads (NW * 64 / (16 * TF)) in slices of CW * 4 (row layout: CW * 2).
+  const int ncu = resident_workgroups(1);
+  const int per = ((a.d_out + 15) / 16 + ncu - 1) / ncu;
   if constexpr (TF == 1) {
-    const int ncu = resident_workgroups(1);
-    const int per = ((a.d_out + 15) / 16 + ncu - 1) / ncu;  // 16-column tiles per CU
-    if ((a.d_in / 8) % 16 == 0 && per >= 5 && per <= 7) {
-      if (per == 5) launch_gemv2<3, 2, 8>(a, ncu, s);
-      else if (per == 6) launch_gemv<3, 1, 8>(a, s);
-      else launch_gemv2<4, 3, 8>(a, ncu, s);
-      return;
-    }
-    if ((a.d_out + 63) / 64 >= 256) launch_gemv<4, 1, 8>(a, s);
-    else if ((a.d_out + 31) / 32 >= 256) launch_gemv<2, 1, 16>(a, s);
-    else launch_gemv<1, 1, 16>(a, s);
+    if (per <= 1) launch_gemv<1, 1, 16>(a, s);
+    else if (per == 2) launch_gemv<2, 1, 16>(a, s);
+    else if (per == 3) launch_gemv<3, 1, 8>(a, s);
+    else if (per == 4) launch_gemv<4, 1, 8>(a, s);
+    else if ((a.d_in / 8) % 16 == 0 && per == 5) launch_gemv2<3, 2, 8>(a, ncu, s);
+    else if ((a.d_in / 8) % 16 == 0 && per == 6) launch_gemv<3, 1, 8>(a, s);
+    else if ((a.d_in / 8) % 16 == 0 && per == 7) launch_gemv2<4, 3, 8>(a, ncu, s);
+    else launch_gemv<4, 1, 8>(a, s);
   } else {
-    if ((a.d_out + 31) / 32 >= 256) launch_gemv<2, TF, 8>(a, s);
-    else launch_gemv<1, TF, 16>(a, s);
+    if (per <= 1) launch_gemv<1, TF, 16>(a, s);
+    else launch_gemv<2, TF, 8>(a, s);
   }
 }
 

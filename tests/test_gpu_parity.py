@@ -248,12 +248,17 @@ def test_fused_rows_tile_widths(n, d_in, d_out, k, b_a, b_w, seed):
 
 
 BALANCED = [
-    # n, d_in, d_out, k, b_a, b_w, seed: few-token GEMV where the columns are
-    # dealt two workgroups per CU (256 CUs; d_in % 128 == 0), ragged d_out
+    # n, d_in, d_out, k, b_a, b_w, seed: few-token GEMV with the columns dealt
+    # evenly over 256 CUs, ragged d_out
     (16, 1024, 27000, 16, 4, 4, 40),  # 64 + 48 columns per CU, row-layout lists
     (7, 2048, 24000, 8, 4, 4, 41),    # 48 + 48, GEMM-layout lists
     (12, 512, 18000, 40, 3, 4, 42),   # 48 + 32, row-layout lists, 8 entries in flight
     (16, 1024, 20000, 0, 4, 4, 43),   # 48 + 32, no lists
+    (16, 1024, 6000, 24, 4, 4, 44),   # one 32-column workgroup per CU (16 waves)
+    (16, 1024, 11008, 32, 4, 4, 45),  # one 48-column workgroup per CU, row layout
+    (5, 1032, 11000, 16, 4, 4, 46),   # 48 columns, a masked last K block, GEMM layout
+    (12, 1024, 14000, 40, 4, 4, 47),  # one 64-column workgroup per CU
+    (20, 2048, 7000, 24, 4, 3, 48),   # two token tiles, one 32-column workgroup per CU
 ]
 
 
