@@ -1126,6 +1126,16 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
   __syncthreads();
   if constexpr (QL) aload4(actq0, 0, A0);
 
+  // HV: the heavy channels' blocks (ceil(2 nh / 64) of 64 positions) and
+  // their descriptors, read once per workgroup
+  const int nhb = HV ? (2 * __builtin_amdgcn_readfirstlane(*A.nheavy) + 63) / 64 : 0;
+  const __amdgpu_buffer_rsrc_t rhw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(A.hw), 0, HV ? (int)((uint32_t)(kSplitPos / 8) * d_out * 4u) : 0,
+      0x00020000);
+  const uint32_t hrow = 2u * kSplitPos;  // bytes per token row of hv
+  const __amdgpu_buffer_rsrc_t rhv = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(A.hv), 0, HV ? (int)((uint32_t)A.n * hrow) : 0, 0x00020000);
+
   for (int u = blockIdx.x; u < T; u += gridDim.x) {
     // this tile's scales, used in its epilogue: lane l holds the column
     // scales of columns 2l, 2l + 1 of the wave's tile and t_i of its tokens
@@ -1190,15 +1200,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
 
     if constexpr (HV) {
       // the heavy channels of the split compensation: value operand A.hv,
-      // weight codes A.hw, ceil(2 nh / 64) blocks of 64 positions
-      const int nhb = (2 * __builtin_amdgcn_readfirstlane(*A.nheavy) + 63) / 64;
+      // weight codes A.hw, nhb blocks
       if (nhb > 0) {
-        const __amdgpu_buffer_rsrc_t rhw = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint32_t*>(A.hw), 0, (int)((uint32_t)(kSplitPos / 8) * d_out * 4u),
-            0x00020000);
-        const uint32_t hrow = 2u * kSplitPos;  // bytes per token row of hv
-        const __amdgpu_buffer_rsrc_t rhv = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint8_t*>(A.hv), 0, (int)((uint32_t)A.n * hrow), 0x00020000);
         uint32_t hoff[FT];
 #pragma unroll
         for (int f = 0; f < FT; ++f)
@@ -1216,26 +1219,51 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
           }
           if (hb < nhb) block_with(h0, h1, h0, hb + 2, hload);
         } else {
-          // two workgroups per CU (256 registers a lane): one value block at a
-          // time - a second one in flight spilled the main loop's registers
-          TileCodes<CW, FT, true> h0;
+          // two workgroups per CU (256 registers a lane): a second whole value
+          // block in flight spilled the main loop's registers, so a block is
+          // taken one token group at a time (its weight words read again for
+          // each): units (block, group) alternate between two buffers, the
+          // next unit's words in flight while one is multiplied
+          static_assert(FT == 2, "two token groups a wave");
+          struct HUnit {
+            uint32_t w[4][CW];  // weight word 4h + s of column group c
+            uint4_t a[4];       // values 8 (4h + s) .. + 7 of the unit's group, step s
+          };
+          auto uload = [&](int b, int f, HUnit& hu) {
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+              hu.a[st] = __builtin_bit_cast(
+                  uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                               rhv, (int)(hoff[f] + (uint32_t)b * 128u + 16u * (uint32_t)st), 0, 0));
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+              for (int c = 0; c < CW; ++c)
+                hu.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
+                    rhw, (int)(woff[c] + (uint32_t)b * wblk + (uint32_t)st * wrow), 0, 0);
+          };
+          auto umma = [&](const HUnit& hu, auto fc) {
+            constexpr int f = decltype(fc)::value;
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+              half8_t a[CW];
+#pragma unroll
+              for (int c = 0; c < CW; ++c) a[c] = expand_dual(hu.w[st][c], tb, l4w);
+              const half8_t bv = __builtin_bit_cast(half8_t, hu.a[st]);
+#pragma unroll
+              for (int c = 0; c < CW; ++c)
+                acc[c][f] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[c], bv, acc[c][f], 0, 0, 0);
+            }
+          };
+          // blocks past the last read zeros (or the next token's row): never used
+          HUnit x, y;
+          uload(0, 0, x);
+          uload(0, 1, y);
           for (int hb = 0; hb < nhb; ++hb) {
-            hload(hb, h0);
-            operands(h0, 0, a0, b0);
-            operands(h0, 1, a1, b1);
-            mma(a0, b0);
-            interleave(false);
-            __builtin_amdgcn_sched_barrier(0);
-            operands(h0, 2, a0, b0);
-            mma(a1, b1);
-            interleave(false);
-            __builtin_amdgcn_sched_barrier(0);
-            operands(h0, 3, a1, b1);
-            mma(a0, b0);
-            interleave(false);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
+            umma(x, std::integral_constant<int, 0>{});
+            uload(hb + 1, 0, x);
+            umma(y, std::integral_constant<int, 1>{});
+            uload(hb + 1, 1, y);
           }
         }
       }
