@@ -353,8 +353,11 @@ def run_workload(args, layer, weights, dev, side):
         "outlier_compensate": lambda c: oasis.outlier_compensate_split(
             q["max_idx"], q["min_idx"], q["residual"], idx_w[c], idx_wr[c], lut, b_w, s_w, d_in,
             y=y, accumulate=False, workspace=ws),
+        # adds into y only where the path merges there (the separate schedule);
+        # the split and look-ahead schedules run it first, writing y
         "lut_gemm": lambda c: oasis.lut_gemm(q["idx_act"], q["act_scale"], idx_w[c], s_w, lut,
-                                             b_a, b_w, algo, y=y, accumulate=True),
+                                             b_a, b_w, algo, y=y,
+                                             accumulate=path == "separate"),
         "lut_gemm_compensated": lambda c: oasis.lut_gemm_compensated(
             q["idx_act"], q["act_scale"], idx_w[c], s_w, lut, b_a, b_w, q["max_idx"],
             q["min_idx"], q["residual"], y=y),

@@ -862,10 +862,9 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
   const uint32_t arow = BV ? (uint32_t)A.a_row : KB * 4u;  // bytes per token row
   const uint32_t d_out = (uint32_t)A.d_out;
 
-  // Reads past either tensor return 0 (the descriptor's size check covers the
-  // whole per-lane offset); the two blocks past the last one are requested
-  // too, so every refill is unconditional.  Columns and tokens past the end
-  // are clamped to the last one (their outputs are never stored).
+  // The blocks past the last one are requested too (every refill is
+  // unconditional) and read zeros (see load_from); columns and tokens past
+  // the end are clamped to the last one (their outputs are never stored).
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(A.idx_w), 0, (int)(KB * d_out * 4u), 0x00020000);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
@@ -911,11 +910,23 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
   };
   const uint32_t wrow = d_out * 4u, wblk = 8u * d_out * 4u;
 
+  // Code and value loads take the per-lane part of the offset in the VGPR
+  // and the block's uniform part in soffset (no VALU add per load: two per
+  // load were an eighth of the main loop's VALU instructions).  A block past
+  // the tensor's last (index bl), which the loops request but never
+  // multiply, goes through rz, a descriptor of size 0, at soffset 0: it
+  // returns zeros without touching memory, whatever part of the offset the
+  // range check covers.
+  const __amdgpu_buffer_rsrc_t rz = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(A.idx_w), 0, 0, 0x00020000);
+  auto sblk = [](int blk, int bl) { return blk <= bl ? (uint32_t)max(0, blk) : 0u; };
   // codes (or values) of block blk from the descriptors rwx / rax at the
   // per-lane offsets aoffx; the type of tc says which operand B is
-  auto load_from = [&](int blk, auto& tc, __amdgpu_buffer_rsrc_t rwx,
+  auto load_from = [&](int blk, int bl, auto& tc, __amdgpu_buffer_rsrc_t rwx,
                        __amdgpu_buffer_rsrc_t rax, const uint32_t (&aoffx)[FT]) {
     constexpr bool VALS = sizeof(tc.a) / sizeof(tc.a[0]) == 4;
+    const uint32_t bc = sblk(blk, bl);
+    if (blk > bl) rwx = rax = rz;
 #pragma unroll
     for (int f = 0; f < FT; ++f) {
       if constexpr (VALS) {
@@ -923,10 +934,10 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
         for (int st = 0; st < 4; ++st)
           tc.a[st][f] = __builtin_bit_cast(
               uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                           rax, (int)(aoffx[f] + (uint32_t)blk * 128u + 16u * (uint32_t)st), 0, 0));
+                           rax, (int)aoffx[f], (int)(bc * 128u + 16u * (uint32_t)st), 0));
       } else {
         tc.a[0][f] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                     rax, (int)(aoffx[f] + (uint32_t)blk * 32u), 0, 0));
+                                                     rax, (int)aoffx[f], (int)(bc * 32u), 0));
       }
     }
 #pragma unroll
@@ -934,10 +945,11 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
 #pragma unroll
       for (int c = 0; c < CW; ++c)
         tc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
-            rwx, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
+            rwx, (int)woff[c], (int)(bc * wblk + (uint32_t)st * wrow), 0);
   };
-  auto load = [&](int blk, auto& tc) { load_from(blk, tc, rw, ra, aoff); };
-  // QL: copy a quad (8 pieces per lane, at offsets d + qoff) into buffer q
+  auto load = [&](int blk, auto& tc) { load_from(blk, nblk - 1, tc, rw, ra, aoff); };
+  // QL: copy a quad (8 pieces per lane, at offsets d + qoff; qoff uniform,
+  // in soffset) into buffer q
   const uint32_t gbase = (uint32_t)(wave / WX) * (uint32_t)(32 * FT * 128);
   auto dma = [&](unsigned char* q, const uint32_t (&d)[NDMA], uint32_t qoff) {
     if constexpr (QL) {
@@ -945,7 +957,7 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
       for (int i = 0; i < NDMA; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             ra, (__attribute__((address_space(3))) void*)(q + gbase + ((uint32_t)RPW * (uint32_t)(wave % WX) + 8u * (uint32_t)i) * 128u),
-            16, (int)(d[i] + qoff), 0, 0, 0);
+            16, (int)d[i], (int)qoff, 0, 0);
     }
   };
   // QL: lane (r, h) reads chunk 2 bq + h of rows 32 f + r of its group (aload4)
@@ -966,12 +978,14 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
     uint4_t a[FT];  // words 4h .. 4h + 3 of token group f
   };
   auto wload4 = [&](int blk, WCodes& wc) {
+    const uint32_t sb = sblk(blk, nblk - 1) * wblk;
+    const __amdgpu_buffer_rsrc_t rwb = blk < nblk ? rw : rz;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int c = 0; c < CW; ++c)
         wc.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
-            rw, (int)(woff[c] + (uint32_t)blk * wblk + (uint32_t)st * wrow), 0, 0);
+            rwb, (int)woff[c], (int)(sb + (uint32_t)st * wrow), 0);
   };
   auto aload4 = [&](const unsigned char* q, int bq, ACodes& ac) {
     const uint32_t co = (((uint32_t)(2 * bq + h)) ^ xr) * 16u;
@@ -1096,9 +1110,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
     uint32_t dq[NDMA];
     const bool nxt = Q >= nq;
 #pragma unroll
-    for (int i = 0; i < NDMA; ++i)
-      dq[i] = nxt ? dnext[i] + (uint32_t)(Q - nq) * 128u : dcur[i] + (uint32_t)Q * 128u;
-    dma(q, dq, 0u);
+    for (int i = 0; i < NDMA; ++i) dq[i] = nxt ? dnext[i] : dcur[i];
+    dma(q, dq, (uint32_t)(nxt ? Q - nq : Q) * 128u);
   };
 
   // ---- prologue: the first tile's first two blocks requested, then the table
@@ -1162,8 +1175,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
     // block before the step that expands them).  The loop body is
     // straight-line (an odd last block is peeled): with a conditional half in
     // it the compiler's wait analysis would assume the worst at the loop head
-    // and wait for every load in flight.  Blocks past the end read zeros or
-    // the next token's row (never used).
+    // and wait for every load in flight.  Blocks past the end read zeros
+    // (never used).
     if constexpr (QL) {
       // two quads per iteration, blocks b .. b + 7: quad m in actq0, m + 1
       // in actq1 (published before block b + 3), m + 2 copied into actq0
@@ -1206,7 +1219,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
 #pragma unroll
         for (int f = 0; f < FT; ++f)
           hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * hrow + 64u * (uint32_t)h;
-        auto hload = [&](int b, auto& tc) { load_from(b, tc, rhw, rhv, hoff); };
+        // kSplitPos / 64 blocks in both tensors
+        auto hload = [&](int b, auto& tc) { load_from(b, kSplitPos / 64 - 1, tc, rhw, rhv, hoff); };
         if constexpr (CW * FT > 8) {
           TileCodes<CW, FT, true> h0, h1;
           hload(0, h0);
@@ -1230,17 +1244,20 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
             uint4_t a[4];       // values 8 (4h + s) .. + 7 of the unit's group, step s
           };
           auto uload = [&](int b, int f, HUnit& hu) {
+            const uint32_t bc = sblk(b, kSplitPos / 64 - 1);
+            const bool in = b <= kSplitPos / 64 - 1;
+            const __amdgpu_buffer_rsrc_t rvb = in ? rhv : rz, rwb = in ? rhw : rz;
 #pragma unroll
             for (int st = 0; st < 4; ++st)
               hu.a[st] = __builtin_bit_cast(
                   uint4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                               rhv, (int)(hoff[f] + (uint32_t)b * 128u + 16u * (uint32_t)st), 0, 0));
+                               rvb, (int)hoff[f], (int)(bc * 128u + 16u * (uint32_t)st), 0));
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
               for (int c = 0; c < CW; ++c)
                 hu.w[st][c] = __builtin_amdgcn_raw_buffer_load_b32(
-                    rhw, (int)(woff[c] + (uint32_t)b * wblk + (uint32_t)st * wrow), 0, 0);
+                    rwb, (int)woff[c], (int)(bc * wblk + (uint32_t)st * wrow), 0);
           };
           auto umma = [&](const HUnit& hu, auto fc) {
             constexpr int f = decltype(fc)::value;
@@ -1255,7 +1272,7 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
                 acc[c][f] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[c], bv, acc[c][f], 0, 0, 0);
             }
           };
-          // blocks past the last read zeros (or the next token's row): never used
+          // blocks past the last read zeros: never used
           HUnit x, y;
           uload(0, 0, x);
           uload(0, 1, y);
@@ -1306,14 +1323,11 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
             float4_t v = {acc[c][f][4 * g], acc[c][f][4 * g + 1], acc[c][f][4 * g + 2],
                           acc[c][f][4 * g + 3]};
             v = ts * sw * v;
-            // non-temporal where the reduction is long: streaming y past the
-            // L2 leaves that to the code streams (measured 1868 -> 1729 us at
-            // 4096 x 8192 x 28672); with the short value operand the kernel is
-            // bound by these stores, which then run slower (194 -> 507 us)
+            // plain stores: non-temporal ones (cache policy nt) measured
+            // slower at every shape, 1804 -> 1683 us at 4096 x 8192 x 28672
+            // and 226 -> 184 us at 2048 x 4096 x 11008 when replaced by these
             float4_t* dst = reinterpret_cast<float4_t*>(yrow + j);
-            const float4_t o = A.accumulate ? *dst + v : v;
-            if constexpr (BV) *dst = o;
-            else __builtin_nontemporal_store(o, dst);
+            *dst = A.accumulate ? *dst + v : v;
           } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
