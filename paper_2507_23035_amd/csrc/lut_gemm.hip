@@ -1219,8 +1219,10 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
 #pragma unroll
         for (int f = 0; f < FT; ++f)
           hoff[f] = (uint32_t)min(t0 + 32 * f + r32, A.n - 1) * hrow + 64u * (uint32_t)h;
-        // kSplitPos / 64 blocks in both tensors
-        auto hload = [&](int b, auto& tc) { load_from(b, kSplitPos / 64 - 1, tc, rhw, rhv, hoff); };
+        // blocks past the last heavy one (the tensors hold kSplitPos / 64)
+        // read zeros: fetched, the two refills past it cost 2 / nhb more of
+        // these reads per tile
+        auto hload = [&](int b, auto& tc) { load_from(b, nhb - 1, tc, rhw, rhv, hoff); };
         if constexpr (CW * FT > 8) {
           TileCodes<CW, FT, true> h0, h1;
           hload(0, h0);
@@ -1244,8 +1246,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
             uint4_t a[4];       // values 8 (4h + s) .. + 7 of the unit's group, step s
           };
           auto uload = [&](int b, int f, HUnit& hu) {
-            const uint32_t bc = sblk(b, kSplitPos / 64 - 1);
-            const bool in = b <= kSplitPos / 64 - 1;
+            const uint32_t bc = sblk(b, nhb - 1);
+            const bool in = b < nhb;
             const __amdgpu_buffer_rsrc_t rvb = in ? rhv : rz, rwb = in ? rhw : rz;
 #pragma unroll
             for (int st = 0; st < 4; ++st)
