@@ -25,6 +25,7 @@ from __future__ import annotations
 import argparse
 import dataclasses
 import json
+import re
 import os
 import sys
 import time
@@ -169,8 +170,11 @@ def summarize_pmc(root, workload, path):
         vals = {}
         for c, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
             rs = [r for r in _pmc_rows(os.path.join(root, sub), c) if sym in r["Kernel_Name"]]
-            if call == "lut_gemm":  # the main-branch kernel alone, not its variants with
-                rs = [r for r in rs if "true>" not in r["Kernel_Name"]]   # value blocks
+            if call == "lut_gemm":  # the main-branch kernel alone: a tile kernel's value
+                # operand and heavy-block variants (5th and 6th template arguments) are not
+                rs = [r for r in rs if not re.search(
+                    r"k_gemm_mfma_tile<\d+, \d+, \d+, \d+, (true, \w+|\w+, true)",
+                    r["Kernel_Name"])]
             if call in ("cluster_act", "detect_outliers", "quantize_act",
                         "build_lut_quantize_act"):
                 want = {"cluster_act": "true, false", "detect_outliers": "false, true",

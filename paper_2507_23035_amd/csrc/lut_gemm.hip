@@ -806,6 +806,22 @@ __global__ void __launch_bounds__(WX * WY * 64) k_gemm_mfma_prefill(GemmArgs A, 
 // ----------------------------------------------------------------------------
 typedef float float16_t __attribute__((ext_vector_type(16)));
 
+// Tile t of ncx x nty (column x token tiles) in groups of kTileGroup token
+// tiles: inside a group the token tile runs fastest, then the column tile.
+// The tiles an XCD holds at once (consecutive ones, see xcd_tile) then span
+// a few column and a few token tiles: at 4096 x 8192 x 28672 one round of an
+// XCD read 16 token tiles' activation codes and 2 column tiles' weight codes
+// with the token tile fastest over all 16, 8 and 4 in groups of 8 (12 MB
+// instead of 18 MB of operands per round and XCD).
+constexpr int kTileGroup = 8;
+__device__ __forceinline__ void tile_xy(int t, int ncx, int nty, int& cx, int& ty) {
+  const int gb = t / (kTileGroup * ncx) * kTileGroup;  // the group's first token tile
+  const int gt = min(kTileGroup, nty - gb);              // its token tiles
+  const int r = t - gb * ncx;
+  cx = r / gt;
+  ty = gb + r % gt;
+}
+
 // BV: the B operand is an fp16 value matrix (GemmArgs::kdyn), one 16-byte load
 // per lane, step and token group, instead of activation codes.
 template <int CW, int FT, bool BV>
@@ -820,10 +836,11 @@ struct TileCodes {
 //
 // Persistent: workgroup b takes tiles b, b + G, b + 2G, ... (G = gridDim.x,
 // at most what the CUs hold at once).  The decode table is built once; the
-// codes of a workgroup's next tile are requested before the current tile's
-// epilogue, so its output stores drain while the next tile's first MFMAs run
-// (all workgroups of a round finish together, and a store burst with idle
-// matrix cores cost 11 % of the time at 4096 x 8192 x 28672).  The tile's
+// codes of a workgroup's next tile are requested right after the current
+// tile's stores.  Requested before them, they were live through the
+// epilogue, where the compiler then kept about twice as many values in
+// scratch, and every reload there waited for those loads (the heavy-block
+// GEMM at 4096 x 8192 x 28672: 1733 -> 1648 us with them moved).  The tile's
 // scales are requested at its start and kept in registers (the column
 // scales pass through a 512-byte LDS row per wave in the epilogue).
 //
@@ -883,8 +900,9 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
   uint32_t dcur[NDMA], dnext[NDMA];
   auto dma_offsets = [&](int u, uint32_t (&d)[NDMA]) {
     if constexpr (QL) {
-      const int tile = xcd_tile(min(u, T - 1), T);
-      const int tg = ((tile % nty) * WY + wave / WX) * 32 * FT;
+      int cx, ty;
+      tile_xy(xcd_tile(min(u, T - 1), T), ncx, nty, cx, ty);
+      const int tg = (ty * WY + wave / WX) * 32 * FT;
 #pragma unroll
       for (int i = 0; i < NDMA; ++i) {
         const int R = RPW * (wave % WX) + 8 * i + (lane >> 3);
@@ -895,8 +913,8 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
   };
   // origin and per-lane code offsets of tile u
   auto place = [&](int u) {
-    const int tile = xcd_tile(u, T);
-    const int cx = tile / nty, ty = tile % nty;
+    int cx, ty;
+    tile_xy(xcd_tile(u, T), ncx, nty, cx, ty);
     j0 = (cx * WX + wave % WX) * 32 * CW;
     t0 = (ty * WY + wave / WX) * 32 * FT;
 #pragma unroll
@@ -1288,21 +1306,7 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
       }
     }
 
-    // ---- the next tile's first two blocks go out before this tile's stores
     const int jt = j0, tt = t0;
-    if (u + (int)gridDim.x < T) {
-      place(u + (int)gridDim.x);
-      if constexpr (QL) {  // its quad 0 is in actq0 (published in the last iteration)
-        wload4(0, W0);
-        wload4(1, W1);
-        wload4(2, W2);
-        wload4(3, W3);
-        aload4(actq0, 0, A0);
-      } else {
-        load(0, c0);
-        load(1, c1);
-      }
-    }
 
     // ---- epilogue: y (+)= t_i * s_j * acc, four consecutive columns per store
     if (2 * lane < 32 * CW)
@@ -1339,6 +1343,21 @@ __global__ void __launch_bounds__(WX * WY * 64, (CW * FT > 8 || BV || WX * WY > 
             }
           }
         }
+    }
+
+    // ---- the next tile's first blocks, requested after this tile's stores
+    if (u + (int)gridDim.x < T) {
+      place(u + (int)gridDim.x);
+      if constexpr (QL) {  // its quad 0 is in actq0 (published in the last iteration)
+        wload4(0, W0);
+        wload4(1, W1);
+        wload4(2, W2);
+        wload4(3, W3);
+        aload4(actq0, 0, A0);
+      } else {
+        load(0, c0);
+        load(1, c1);
+      }
     }
   }
 }
