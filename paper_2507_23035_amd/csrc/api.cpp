@@ -66,13 +66,19 @@ const char* oasis_status_str(int status) {
 
 const char* oasis_version(void) { return "oasis 0.1 gfx950"; }
 
-// Inlier scale: the quantize launch (absmax scale) writes the lists, then a
-// second launch recomputes t, the codes and the residuals from them.
+// Inlier scale: with top-k lists the quantize launch computes t, the codes
+// and the residuals itself once its lists exist; with fixed thresholds the
+// quantize launch (absmax scale) writes the lists, then a second launch
+// recomputes t, the codes and the residuals from them.
+// The fused form also needs the listed-channel bitmap and the entries in
+// LDS; where they do not fit, the two launches are used as well.
 static int quantize_launch(oasis::QuantArgs a, hipStream_t stream) {
   const bool inlier = a.scale_mode == OASIS_SCALE_INLIER;
-  if (inlier) a.scale_mode = OASIS_SCALE_ABSMAX;
+  const bool fused = inlier && !a.static_thr && a.k > 0 &&
+                     oasis::quantize_lds_bytes(a.d_in, a.k, true) <= kMaxLds;
+  if (inlier && !fused) a.scale_mode = OASIS_SCALE_ABSMAX;
   hipError_t e = oasis::launch_quantize(a, stream);
-  if (e != hipSuccess || !inlier) return launched(e);
+  if (e != hipSuccess || !inlier || fused) return launched(e);
   if (a.lut_out) a.lut = a.lut_out;
   return launched(oasis::launch_inlier_codes(a, stream));
 }

@@ -197,7 +197,7 @@ hipError_t launch_gemm_compensated_split(const GemmArgs& g, const CompArgs& a,
 
 // Bytes of dynamic LDS the quantize kernel needs for a token of d_in values
 // and k outliers per side.
-size_t quantize_lds_bytes(int d_in, int k);
+size_t quantize_lds_bytes(int d_in, int k, bool inlier = false);
 
 hipError_t launch_build_lut(const uint16_t* cb_act, int b_a, const uint16_t* cb_wgt, int b_w,
                             oasis_lut_block* out, hipStream_t s);

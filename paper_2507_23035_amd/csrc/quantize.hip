@@ -63,7 +63,18 @@ __host__ __device__ inline uint32_t list_cap(int k) {
 // list, then min list).
 static size_t dyn_bytes(int d_in, int k) { return (size_t)d_in * 2 + 16 * (size_t)list_cap(k); }
 
-size_t quantize_lds_bytes(int d_in, int k) { return sizeof(QuantSmem) + dyn_bytes(d_in, k); }
+// Inlier scale computed in the same launch (top-k lists, no fixed
+// thresholds): after the lists, a bitmap of the listed channels (d_in bits,
+// whole 16-byte rows) and the 2k list entries (channel | 1 << 31 for a min
+// entry whose channel is on the max list too).
+__host__ __device__ inline uint32_t inlier_words(int d_in) {
+  return (((uint32_t)d_in + 31u) / 32u + 3u) & ~3u;
+}
+static size_t inlier_bytes(int d_in, int k) { return 4 * (size_t)inlier_words(d_in) + 8 * (size_t)k; }
+
+size_t quantize_lds_bytes(int d_in, int k, bool inlier) {
+  return sizeof(QuantSmem) + dyn_bytes(d_in, k) + (inlier ? inlier_bytes(d_in, k) : 0);
+}
 
 // fp16 bits -> order-preserving key; -0 and +0 share key 0x8000.
 __device__ __forceinline__ uint32_t ord_key(uint32_t bits) {
@@ -90,6 +101,10 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   uint32_t* amax_ = cmax + lcap;
   uint32_t* cmin = amax_ + lcap;
   uint32_t* amin_ = cmin + lcap;
+  // inlier scale in this launch (uniform): see inlier_bytes
+  const bool inl = topk && A.scale_mode == OASIS_SCALE_INLIER && !A.static_thr;
+  uint32_t* lbits = amin_ + lcap;
+  uint32_t* lent = lbits + inlier_words(d_in);
 
   // ---- the token into registers (runs tid*VR .. tid*VR + VR - 1)
   uint4 xv[VR];
@@ -126,6 +141,8 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     S.hist2[1][tid] = 0;
   }
   if (tid == 0) S.nalloc = 0;
+  if (inl)
+    for (uint32_t w = (uint32_t)tid; w < inlier_words(d_in); w += NT) lbits[w] = 0u;
   __syncthreads();  // histograms cleared
 
   // keys, two per word (even channel low)
@@ -177,19 +194,23 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     amax = max(amax, max(max(m.x, m.y), max(m.z, m.w)));
   }
   const float t = (A.scale_mode == OASIS_SCALE_NONE) ? 1.0f : h2f((uint16_t)amax);
-  if (CLUSTER && tid == 0) A.act_scale[i] = t;
+  if (CLUSTER && !inl && tid == 0) A.act_scale[i] = t;
 
   // ---- boundary keys: lane c computes key(Q_c), Q_c = the smallest fp16 not
-  // below P_c = fp32(t * b_c)
+  // below P_c = fp32(ts * b_c)
   uint32_t kq_lane = 0x10000u;  // above every key: boundaries past the last one
-  if (lane < nb) {
-    const float P = t * bc;
-    const _Float16 h = (_Float16)P;  // round to nearest even
-    kq_lane = ord_key(__builtin_bit_cast(uint16_t, h)) + ((float)h < P ? 1u : 0u);
-  }
   uint32_t KQ[15];
+  auto boundaries = [&](float ts) {
+    kq_lane = 0x10000u;
+    if (lane < nb) {
+      const float P = ts * bc;
+      const _Float16 h = (_Float16)P;  // round to nearest even
+      kq_lane = ord_key(__builtin_bit_cast(uint16_t, h)) + ((float)h < P ? 1u : 0u);
+    }
 #pragma unroll
-  for (int c = 0; c < 15; ++c) KQ[c] = (uint32_t)__builtin_amdgcn_readlane((int)kq_lane, c);
+    for (int c = 0; c < 15; ++c) KQ[c] = (uint32_t)__builtin_amdgcn_readlane((int)kq_lane, c);
+  };
+  boundaries(t);
   // cluster index by the full count
   auto code_full = [&](uint32_t kk) -> uint32_t {
     uint32_t a = 0;
@@ -197,18 +218,21 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
     for (int c = 0; c < 15; ++c) a += kk >= KQ[c] ? 1u : 0u;
     return a;
   };
-  if (tid < 256) {  // bucket tid: keys tid*256 .. tid*256 + 255
-    const uint32_t base = (uint32_t)tid << 8;
-    uint32_t first = 0, upto = 0;
+  auto build_bucket = [&]() {
+    if (tid < 256) {  // bucket tid: keys tid*256 .. tid*256 + 255
+      const uint32_t base = (uint32_t)tid << 8;
+      uint32_t first = 0, upto = 0;
 #pragma unroll
-    for (int c = 0; c < 15; ++c) {
-      first += KQ[c] <= base ? 1u : 0u;
-      upto += KQ[c] <= base + 255u ? 1u : 0u;
+      for (int c = 0; c < 15; ++c) {
+        first += KQ[c] <= base ? 1u : 0u;
+        upto += KQ[c] <= base + 255u ? 1u : 0u;
+      }
+      // KQ[first], the first boundary inside if any, from lane `first` of this wave
+      const uint32_t kf = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(first << 2), (int)kq_lane);
+      S.bucket[tid] = (uint16_t)(first | ((upto - first) << 4) | ((kf & 0xFFu) << 8));
     }
-    // KQ[first], the first boundary inside if any, from lane `first` of this wave
-    const uint32_t kf = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(first << 2), (int)kq_lane);
-    S.bucket[tid] = (uint16_t)(first | ((upto - first) << 4) | ((kf & 0xFFu) << 8));
-  }
+  };
+  build_bucket();
   // cluster index of one key from the table (visible after the next barrier);
   // `multi` flags a bucket with two or more boundaries (then use code_full)
   auto code_fast = [&](uint32_t kk, bool& multi) -> uint32_t {
@@ -470,7 +494,7 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
   }
 
   make_codes();
-  if (CLUSTER) store_codes();
+  if (CLUSTER && !inl) store_codes();
 
   // ---- list membership, one bit per channel
   mask_t mmax = 0, mmin = 0;
@@ -616,19 +640,89 @@ __global__ void __launch_bounds__(NT) k_quantize(QuantArgs A) {
         const float r = (ax & 16u) ? 0.0f : h2f((uint16_t)bits) - xhat;
         if (is_max) {
           A.max_idx[krow + rank] = (int)p;
-          A.residual[rrow + rank] = r;
+          if (!inl) A.residual[rrow + rank] = r;
         } else {
           A.min_idx[krow + rank] = (int)p;
-          A.residual[rrow + k + rank] = r;
+          if (!inl) A.residual[rrow + k + rank] = r;
+        }
+        if (inl) {  // the residual waits for the inlier scale
+          lent[(is_max ? 0u : (uint32_t)k) + rank] = p | ((ax & 16u) ? 0x80000000u : 0u);
+          atomicOr(&lbits[p >> 5], 1u << (p & 31u));
         }
       }
     }
+  }
+  if (!inl) return;
+
+  // ---- inlier scale: t = max |x| over the channels in neither list (0 when
+  // every channel is listed), then the codes under t and the residuals of
+  // the listed channels (by the same boundary rule)
+  __syncthreads();  // lists, bitmap
+  uint32_t mi = 0;
+#pragma unroll
+  for (int u = 0; u < VR; ++u) {
+    const int v = tid * VR + u;
+    if (v >= nvec) continue;
+    const uint32_t lst = (lbits[v >> 2] >> (8 * (v & 3))) & 0xFFu;  // channels 8v .. 8v + 7
+    const uint4 xw = reinterpret_cast<const uint4*>(xs)[v];
+    const uint32_t w[4] = {xw.x, xw.y, xw.z, xw.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {  // |x| of finite fp16 values orders like its 15 low bits
+      if (!((lst >> (2 * q)) & 1u)) mi = max(mi, w[q] & 0x7FFFu);
+      if (!((lst >> (2 * q + 1)) & 1u)) mi = max(mi, (w[q] >> 16) & 0x7FFFu);
+    }
+  }
+  mi = wave_max(mi);
+  if (lane == 0) S.wmax[wave] = mi;
+  __syncthreads();  // inlier maxima
+#pragma unroll
+  for (int j = 0; j < NW / 4; ++j) {
+    const uint4 mm = reinterpret_cast<const uint4*>(S.wmax)[j];
+    mi = max(mi, max(max(mm.x, mm.y), max(mm.z, mm.w)));
+  }
+  const float ti = h2f((uint16_t)mi);
+  if (CLUSTER && tid == 0) A.act_scale[i] = ti;
+  boundaries(ti);
+  build_bucket();
+  __syncthreads();  // bucket table
+  if (CLUSTER) {
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      const int v = tid * VR + u;
+      if (v >= nvec) continue;
+      const uint4 xw = reinterpret_cast<const uint4*>(xs)[v];
+      const uint32_t w[4] = {xw.x, xw.y, xw.z, xw.w};
+      bool multi = false;
+      uint32_t packed = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        packed |= code_fast(ord_key(w[q] & 0xFFFFu), multi) << (8 * q);
+        packed |= code_fast(ord_key(w[q] >> 16), multi) << (8 * q + 4);
+      }
+      if (multi) {
+        packed = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          packed |= (code_full(ord_key(w[q] & 0xFFFFu)) << (8 * q)) |
+                    (code_full(ord_key(w[q] >> 16)) << (8 * q + 4));
+      }
+      arow[v] = packed;
+    }
+  }
+  // t * C_A[a] is exact, a product of two fp16 values
+  for (int e = tid; e < 2 * k; e += NT) {
+    const uint32_t ent = lent[e], p = ent & 0x7FFFFFFFu;
+    const uint32_t bits = xs[p];
+    const float r = (ent >> 31) ? 0.0f : h2f((uint16_t)bits) - ti * S.ca[code_full(ord_key(bits))];
+    A.residual[rrow + e] = r;
   }
 }
 
 template <int NT, int VR, bool CL, bool TK>
 static hipError_t launch_nt(const QuantArgs& a, hipStream_t s) {
-  const size_t lds = sizeof(QuantSmem) + (TK ? dyn_bytes(a.d_in, a.k) : 0);
+  const bool inl = TK && a.k > 0 && a.scale_mode == OASIS_SCALE_INLIER && !a.static_thr;
+  const size_t lds = sizeof(QuantSmem) + (TK ? dyn_bytes(a.d_in, a.k) : 0) +
+                     (inl ? inlier_bytes(a.d_in, a.k) : 0);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)k_quantize<NT, VR, CL, TK>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

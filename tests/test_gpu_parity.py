@@ -394,6 +394,19 @@ def test_inlier_scale(case):
     check_quant(q_s, ref_s, s.k)
 
 
+def test_inlier_scale_two_launches():
+    """Inlier scale where the listed-channel bitmap and the entries do not fit
+    beside the token and the lists in LDS (65536 channels, k = 1024): the
+    quantize launch with the absmax scale, then the inlier pass, bit for bit."""
+    L = synth.make_layer(synth.custom(2, 65536, 16, 1024, seed=44))
+    s = L.spec
+    x = torch.from_numpy(L.x.view(np.int16).copy()).to(dev())
+    ref = O.quantize_act(L.x, L.cb_a, s.b_a, s.k, mode=O.SCALE_INLIER)
+    _, q = oasis.build_lut_quantize_act(L.cb_a, s.b_a, L.cb_w, s.b_w, x, s.k,
+                                        scale_mode=oasis.SCALE_INLIER)
+    check_quant(q, ref, s.k)
+
+
 @pytest.mark.parametrize("n", [8, 40])   # GEMV and prefill epilogues
 def test_outputs_and_scales_4_byte_aligned(n):
     """y and w_scale at 4-byte (not 16-byte) aligned addresses, as the
