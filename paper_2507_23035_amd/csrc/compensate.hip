@@ -378,8 +378,9 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
 // Workgroup = 16 waves over a slab of 64 words (512 columns) and a tile of
 // tt tokens; wave w takes tokens w, w + 16, ... of the tile.  Lane l owns
 // word 64 * slab + l and 8 fp32 accumulators per token.  A token's listed
-// entries are wave-uniform: lane e holds entry e, readlane hands them out in
-// list order, and each entry fetches one word per lane (one contiguous
+// entries are wave-uniform: lane e holds entry e, readlane hands out the
+// channels and a broadcast LDS read the residuals, in list order, and each
+// entry fetches one word per lane (one contiguous
 // 256-byte piece of row p per wave, 3 * WR_U entries in flight).  A word's four
 // bytes become four pairs of weight centroids through a 64 KiB LDS table -
 // row `byte` holds 64 copies of pair(C_W, byte), lane l reads copy l, so the
@@ -537,7 +538,11 @@ __global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn,
   // adding into y: the token's y words are requested at its first unit and
   // used at its last (a load right before the store would wait for memory)
   float4 yv[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-  auto consume = [&](int u, float rl, const uint32_t (&w)[WR_U]) {
+  // rl: the unit's residuals, lane e holding entry e (for the skip test);
+  // lrv: the same in LDS, read as one broadcast word per entry (a readlane
+  // per entry was one VALU instruction of about fourteen: 747 -> 710 us at
+  // 4096 x 8192 x 28672)
+  auto consume = [&](int u, float rl, const uint32_t (&w)[WR_U], const float* lrv) {
     int slot_j, ubeg;
     unit_token(u, slot_j, ubeg);
     if (A.accumulate && vec && u == ubeg) {
@@ -550,8 +555,7 @@ __global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn,
     if (__ballot(rl != 0.0f) != 0) {
 #pragma unroll
       for (int e = 0; e < WR_U; ++e) {
-        const float re = __builtin_bit_cast(
-            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rl), e));
+        const float re = lrv[e];  // the same LDS word in every lane
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const uint32_t off = __builtin_amdgcn_perm(w[e], lane4, 0x0C0C0000u | ((4u + b) << 8));
@@ -618,7 +622,7 @@ __global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn,
       const float ru = ra;
       rd(v + 2, pc, rc);
       if (v + 2 < V) issue(pc, wc);
-      consume(c0 + v, ru, wa);
+      consume(c0 + v, ru, wa, lr + v * WR_U);
     };
     for (int v = 0; v < V; v += 3) {
       step(v, r0, w0, p2, r2, w2);
