@@ -595,6 +595,19 @@ def test_persistent_tiles_ragged():
     run_full(L, algos=(oasis.ALGO_MFMA,), tokens=sampled_tokens(1000, 5))
 
 
+@pytest.mark.parametrize("case", [
+    (3000, 512, 16400, 16, 61),   # 256 x 256 tiles: 12 token tiles, groups of 8 and 4
+    (1100, 1032, 5000, 16, 62),   # 256 x 128 tiles: 9 token tiles, groups of 8 and 1
+], ids=str)
+def test_grouped_tile_order(case):
+    """The many-token GEMM numbers its tiles in groups of 8 token tiles; a
+    last group with fewer token tiles (and a partial last column tile) is
+    placed as the full ones."""
+    n, d_in, d_out, k, seed = case
+    L = synth.make_layer(synth.custom(n, d_in, d_out, k, seed=seed))
+    run_full(L, algos=(oasis.ALGO_MFMA,), tokens=sampled_tokens(n, seed))
+
+
 @pytest.mark.parametrize("name", FULL)
 def test_full_size_layers(name):
     L = synth.make_layer(synth.config(name))
