@@ -383,10 +383,11 @@ __global__ void __launch_bounds__(NW * 64) k_compensate_rows(CompArgs A, int tt,
 // entry fetches one word per lane (one contiguous
 // 256-byte piece of row p per wave, 3 * WR_U entries in flight).  A word's four
 // bytes become four pairs of weight centroids through a 64 KiB LDS table -
-// row `byte` holds 64 copies of pair(C_W, byte), lane l reads copy l, so the
-// reads are conflict free and the offset is one v_perm_b32 - and each
-// centroid meets the residual in one fp32 FMA (v_fma_mix_f32 takes the fp16
-// half directly).  Sixteen waves share the table (128 KiB of LDS with their
+// row `byte` holds 32 copies of the pair as two fp32 values, lane l reads
+// copy l mod 32, so the 8-byte reads are conflict free and the offset is one
+// v_perm_b32 - and each centroid meets the residual in one v_fma_f32 (the
+// fp16-operand v_fma_mix_f32 issues at half its rate; fp32 pairs: 712 ->
+// 680 us at 4096 x 8192 x 28672).  Sixteen waves share the table (128 KiB of LDS with their
 // lists): four waves per SIMD hide the row loads, where 4-wave workgroups
 // with their own table fit two (64 copies) or three (32 copies, one more
 // shift per lookup) on a CU.
@@ -482,19 +483,19 @@ __global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn,
   };
   fill(0, min(U, WR_C / WR_U));  // the first chunk's loads overlap the table build
 
-  // pair table, 64 KiB: row `byte` holds 64 copies of pair(C_W, byte).
-  // Thread t writes chunks c = t + 1024 s (s < 4) of 16 bytes: row c / 16
-  // (low code (t / 16) mod 16, high code t / 256 + 4 s), copies 4 (c mod 16)
-  // .. 4 (c mod 16) + 3
+  // pair table, 64 KiB: row `byte` holds 32 copies of the fp32 pair
+  // (C_W[byte & 15], C_W[byte >> 4]).  Thread t writes chunks c = t + 1024 s
+  // (s < 4) of 16 bytes: row c / 16 (low code (t / 16) mod 16, high code
+  // t / 256 + 4 s), copies 2 (c mod 16) and 2 (c mod 16) + 1
   {
     static_assert(WR_W == 16, "the table build takes 1024 threads");
     const uint16_t* cb = A.lut->cb_wgt;
-    const uint32_t lo = cb[(tid >> 4) & 15];
+    const uint32_t lo = __builtin_bit_cast(uint32_t, h2f(cb[(tid >> 4) & 15]));
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const uint32_t v = lo | ((uint32_t)cb[(tid >> 8) + 4 * s] << 16);
+      const uint32_t hi = __builtin_bit_cast(uint32_t, h2f(cb[(tid >> 8) + 4 * s]));
       const uint32_t c = (uint32_t)tid + 1024u * (uint32_t)s;
-      *reinterpret_cast<uint4_t*>(&tab[(c >> 4) * 64u + (c & 15u) * 4u]) = uint4_t{v, v, v, v};
+      *reinterpret_cast<uint4_t*>(&tab[(c >> 4) * 64u + (c & 15u) * 4u]) = uint4_t{lo, hi, lo, hi};
     }
   }
 
@@ -505,8 +506,10 @@ __global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn,
   const uint32_t row_bytes = (uint32_t)wn * 4u;
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(A.idx_w), 0, (int)((uint32_t)d_in * row_bytes), 0x00020000);
-  // the offset of byte b's entry, b * 256 + lane * 4, is one v_perm_b32
-  const uint32_t lane4 = (uint32_t)lane * 4u;
+  // the offset of byte b's entry, b * 256 + (lane mod 32) * 8, is one
+  // v_perm_b32 (a ds_read_b64 serves 16 lanes at a time: 32 copies keep
+  // every group of 16 on distinct banks)
+  const uint32_t loff = (uint32_t)(lane & 31) * 8u;
   const char* tb = reinterpret_cast<const char*>(tab);
   float sw[8];
 #pragma unroll
@@ -558,10 +561,10 @@ __global__ void __launch_bounds__(64 * WR_W) k_compensate_wr(CompArgs A, int wn,
         const float re = lrv[e];  // the same LDS word in every lane
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const uint32_t off = __builtin_amdgcn_perm(w[e], lane4, 0x0C0C0000u | ((4u + b) << 8));
-          const uint32_t pr = *reinterpret_cast<const uint32_t*>(tb + off);
-          acc[2 * b] = fmaf(re, h2f((uint16_t)(pr & 0xFFFFu)), acc[2 * b]);
-          acc[2 * b + 1] = fmaf(re, h2f((uint16_t)(pr >> 16)), acc[2 * b + 1]);
+          const uint32_t off = __builtin_amdgcn_perm(w[e], loff, 0x0C0C0000u | ((4u + b) << 8));
+          const uint2 pr = *reinterpret_cast<const uint2*>(tb + off);
+          acc[2 * b] = fmaf(re, __builtin_bit_cast(float, pr.x), acc[2 * b]);
+          acc[2 * b + 1] = fmaf(re, __builtin_bit_cast(float, pr.y), acc[2 * b + 1]);
         }
       }
     }
