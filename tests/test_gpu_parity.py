@@ -224,6 +224,8 @@ RAGGED = [
     (66, 4104, 40, 2050, 4, 4, 16),  # lists too long for a tile: per-token kernel
     (64, 1024, 136, 256, 4, 4, 18),  # ~512 channels listed by every token: more heavy
                                      # channels than the dense part takes (256)
+    (40, 20544, 72, 64, 4, 4, 19),   # more channels than the split's LDS counts hold:
+                                     # global counts, selection in a launch of its own
 ]
 
 
