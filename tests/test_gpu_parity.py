@@ -261,6 +261,7 @@ BALANCED = [
     (5, 1032, 11000, 16, 4, 4, 46),   # 48 columns, a masked last K block, GEMM layout
     (12, 1024, 14000, 40, 4, 4, 47),  # one 64-column workgroup per CU
     (20, 2048, 7000, 24, 4, 3, 48),   # two token tiles, one 32-column workgroup per CU
+    (1, 8192, 28672, 64, 4, 4, 49),   # single-token decode at the largest layer shape
 ]
 
 
